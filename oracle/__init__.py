@@ -1,0 +1,26 @@
+"""Oracle for the branch-verification step -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, obviously correct CPU implementation (numpy) of what the
+MI355X path computes, written from the paper:
+
+* ``oracle.tree``     -- tree bookkeeping (parents, depths, ancestors);
+* ``oracle.decoder``  -- the target forward over a token tree that shares a
+  prefix KV cache (plain definition of a Llama-style decoder with a
+  branch-causal key set), in float64, float32 or bfloat16 emulation;
+* ``oracle.sampling`` -- row softmax statistics, target distributions, the
+  speculative accept test min(1, p/q) with residual norm(max(0, p - q))
+  (Preliminaries, "Speculative Decoding"), Branch Speculative Sampling
+  (Appendix, Algorithm 1) at multi-child nodes, and inverse-CDF draws;
+* ``oracle.rollback`` -- KV compaction to the accepted path.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's CPU baseline
+may import this package.  It shares no code with the HIP path and imports
+nothing from it; the product path never calls it.
+
+Every function is pinned by ``-m "not gpu"`` tests to something other than
+itself (an independent library implementation, exact enumeration of the
+output distribution, closed forms printed in the paper, hand-worked golden
+cases).  Nothing here is "parity unpinned".
+"""
+
+from . import tree, decoder, sampling, rollback  # noqa: F401
