@@ -1,0 +1,238 @@
+/*
+ * sb.h -- C ABI of the MI355X branch-verification step of SpecBranch
+ * (arXiv 2506.01979).
+ *
+ * One verify step of the paper's target model: a forward of a Llama-style
+ * decoder over a token tree whose rows share one prefix KV cache (the
+ * verification phase of Algorithm 2 scores every draft position with one
+ * target forward; Section "Branch Resampling" keeps the surviving branch and
+ * drops the others with their KV), row softmax statistics, the lossless
+ * accept/resample walk (Preliminaries, "Speculative Decoding"; Appendix,
+ * Algorithm 1 "Branch Speculative Sampling") and KV rollback.
+ *
+ * Conventions shared by every entry point:
+ *  - "d_" pointers are device pointers, "h_" pointers host pointers.  The
+ *    caller owns every buffer (weights, KV cache, logits, q, uniforms,
+ *    workspace, results); the library keeps only the pointers it is given
+ *    and, in sb_model_create, a small host-side model record.
+ *  - Every call is asynchronous on the given HIP stream and allocates no
+ *    device memory.  A model handle must not be used from two streams at
+ *    once, and two calls that share a workspace must not overlap.
+ *  - Errors a host can detect (null pointers, bad sizes, a malformed tree,
+ *    too little KV capacity or workspace, unsupported shapes) return an
+ *    SB_ERR_* code before anything is enqueued.  SB_ERR_HIP reports a failed
+ *    launch.  Numeric conditions met on the device are reported in flag
+ *    words (SB_FLAG_*), never as a trap.
+ *  - The tree: row 0 is the root (the last committed token, whose KV is not
+ *    yet cached); every other row is a draft token whose parent is an
+ *    earlier row: h_parents[0] == -1 and 0 <= h_parents[i] < i.  Row i sits
+ *    at position kv_len + depth(i) and its K/V go to cache slot
+ *    kv_len + i.  At most SB_MAX_ROWS rows.
+ */
+#ifndef SB_H
+#define SB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SB_MAX_ROWS 256
+
+typedef enum {
+  SB_OK = 0,
+  SB_ERR_INVALID_ARG = 1,   /* null pointer, non-positive size, bad enum */
+  SB_ERR_TREE = 2,          /* parents not a rooted tree in row order */
+  SB_ERR_CAPACITY = 3,      /* KV capacity or workspace too small */
+  SB_ERR_DTYPE = 4,         /* dtype not supported for this call */
+  SB_ERR_HIP = 5,           /* a HIP call or kernel launch failed */
+  SB_ERR_UNSUPPORTED = 6    /* shape outside what the kernels handle */
+} sb_status;
+
+typedef enum { SB_F32 = 0, SB_BF16 = 1 } sb_dtype;
+
+/* Decoder shape (the paper's Table 7 lists the Llama widths).  SB_BF16
+ * models store weights and KV in bfloat16 and accumulate in float32;
+ * SB_F32 models are float32 throughout.  rope_theta is the RoPE base,
+ * rms_eps the RMSNorm epsilon. */
+typedef struct {
+  int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
+  float rope_theta, rms_eps;
+  int32_t dtype; /* sb_dtype */
+} sb_model_config;
+
+/* Weight kinds for sb_pack_weight.  Sources are row-major [out][in]
+ * matrices in the model dtype, as a Llama checkpoint stores them. */
+typedef enum {
+  SB_W_QKV = 0,     /* src0 = Wq [n_heads*head_dim][hidden], src1 = Wk, src2 = Wv
+                       ([n_kv_heads*head_dim][hidden]) */
+  SB_W_O = 1,       /* src0 = Wo [hidden][n_heads*head_dim] */
+  SB_W_GATE_UP = 2, /* src0 = Wgate [ffn][hidden], src1 = Wup [ffn][hidden] */
+  SB_W_DOWN = 3,    /* src0 = Wdown [hidden][ffn] */
+  SB_W_LM_HEAD = 4  /* src0 = W_lm [vocab][hidden] (untied from the embedding) */
+} sb_weight_kind;
+
+/* Per-layer device pointers.  Norm gains are float32 [hidden]; the four
+ * matrices are in the layout sb_pack_weight writes. */
+typedef struct {
+  const float *attn_norm;
+  const void *qkv;
+  const void *o;
+  const float *mlp_norm;
+  const void *gate_up;
+  const void *down;
+} sb_layer_weights;
+
+typedef struct {
+  const void *embed;               /* [vocab][hidden], model dtype, row-major */
+  const float *final_norm;         /* [hidden] */
+  const void *lm_head;             /* packed SB_W_LM_HEAD */
+  const sb_layer_weights *layers;  /* host array of n_layers entries */
+} sb_model_weights;
+
+/* KV cache: k and v are [n_layers][n_kv_heads][capacity][head_dim] in the
+ * model dtype; slots [0, kv_len) hold the committed prefix. */
+typedef struct {
+  void *k;
+  void *v;
+  int32_t capacity;
+} sb_kv_cache;
+
+/* Softmax statistics of one logits row at temperature T (16 bytes):
+ *   T > 0: zmax = max_v fl32(l_v * fl32(1/T)),
+ *          total = sum_v fl32(exp(fl32(z_v - zmax))) in float64;
+ *   T = 0: zmax = max_v l_v, total = 1.
+ * argmax is the lowest index of the largest logit.  The target
+ * distribution is p(v) = fl32(exp(z_v - zmax)) / total (T > 0) or the one-hot
+ * at argmax (T = 0). */
+typedef struct {
+  float zmax;
+  int32_t argmax;
+  double total;
+} sb_row_stats;
+
+#define SB_FLAG_NONFINITE 1     /* a logits row holds NaN or Inf */
+#define SB_FLAG_QZERO 2         /* a tested draft token had q(x) == 0 */
+#define SB_FLAG_ZERO_RESIDUAL 4 /* a residual had no mass; p~ kept */
+
+/* Result of one accept/resample walk (device-resident, written by
+ * sb_accept_resample, read by sb_kv_rollback). */
+typedef struct {
+  int32_t n_accepted;  /* accepted draft rows on the kept path */
+  int32_t branch;      /* ordinal of the kept child of the root, -1 if none */
+  int32_t next_token;  /* residual draw, or bonus draw after a full accept */
+  int32_t path_len;    /* 1 + n_accepted */
+  int32_t flags;       /* SB_FLAG_* */
+  int32_t n_rejected;  /* candidate tests that failed along the walk */
+  int32_t bonus;       /* 1 if next_token came from p of an accepted leaf */
+  int32_t reserved;
+  int32_t path[SB_MAX_ROWS]; /* rows root .. last accepted, by depth */
+} sb_step_result;
+
+typedef struct sb_model sb_model;
+
+const char *sb_status_string(sb_status s);
+int32_t sb_version(void);
+
+/* ---- weights -------------------------------------------------------- */
+
+/* Bytes of the packed form of one weight kind (0 for a bad config/kind). */
+size_t sb_packed_bytes(const sb_model_config *cfg, int32_t kind);
+
+/* Re-lays one weight kind into the kernels' layout: for SB_BF16, 16-row x
+ * 32-column tiles in the operand order of the gfx950 bf16 matrix-core
+ * instruction (rows padded to 16 and columns to 32 with zeros; Q/K rows of
+ * every head reordered so a tile holds RoPE pairs (j, j + d/2); gate and up
+ * rows interleaved 8 by 8); for SB_F32, the source rows concatenated
+ * (Wq;Wk;Wv and Wgate;Wup).  src* and dst are device pointers, dst holds
+ * sb_packed_bytes(cfg, kind) bytes and must not alias a source. */
+sb_status sb_pack_weight(const sb_model_config *cfg, int32_t kind, const void *src0,
+                         const void *src1, const void *src2, void *dst, hipStream_t stream);
+
+/* Records the config and the device weight pointers (not copied; they must
+ * outlive the model).  No device memory is allocated. */
+sb_status sb_model_create(const sb_model_config *cfg, const sb_model_weights *w,
+                          sb_model **out);
+void sb_model_destroy(sb_model *m);
+
+/* ---- the verify step ------------------------------------------------ */
+
+/* Workspace bytes sb_verify_forward needs for up to max_rows rows. */
+size_t sb_workspace_bytes(const sb_model *m, int32_t max_rows, int32_t max_kv_len);
+
+/* Target forward over the token tree (verification phase of Algorithm 2,
+ * with every branch scored in one pass under a branch-causal mask).
+ *   kv:        prefix cache; slots [0, kv_len) are read, tree row i's K/V
+ *              are written to slot kv_len + i (needs kv_len + n_rows <=
+ *              capacity).
+ *   d_tokens:  [n_rows] token ids (row 0 = root).
+ *   h_parents: [n_rows] host array, the tree (see top of file).
+ *   temperature: T >= 0 for the statistics written to d_stats.
+ *   d_logits:  [n_rows][vocab] float32 output.
+ *   d_stats:   [n_rows] output (sb_row_stats at T).
+ *   d_ws:      workspace of at least sb_workspace_bytes(m, n_rows, kv_len)
+ *              bytes (ws_bytes). */
+sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
+                            const int32_t *d_tokens, const int32_t *h_parents, int32_t n_rows,
+                            float temperature, float *d_logits, sb_row_stats *d_stats,
+                            void *d_ws, size_t ws_bytes, hipStream_t stream);
+
+/* Row softmax statistics of [n_rows][vocab] float32 logits at T >= 0 (the
+ * fused LM-head softmax of the verify step, callable on its own). */
+sb_status sb_softmax_stats(int32_t vocab, int32_t n_rows, const float *d_logits,
+                           float temperature, sb_row_stats *d_stats, hipStream_t stream);
+
+/* Workspace bytes of sb_select_branch / sb_accept_resample for a vocab. */
+size_t sb_sample_workspace_bytes(int32_t vocab);
+
+/* Algorithm 1 (Branch Speculative Sampling) at one node.
+ *   d_logits_row/d_stats_row: the node's target row and its statistics at T.
+ *   d_cand_tokens: [n_cand] candidates in test order; d_q: [n_cand][vocab]
+ *   float32, row i the distribution candidate i was drawn from (i.i.d.
+ *   draws: the same row; top-k without replacement: the renormalised
+ *   remainder; deterministic top-k: one-hot).  d_u: [n_cand + 1] uniforms
+ *   in [0,1): u[i] tests candidate i, u[n_cand] drives the final draw.
+ *   d_out: int32[3] = {accepted candidate index or -1, emitted token, flags}.
+ * Accept iff float64(u) < p~(x) / float64(q(x)); after a rejection
+ * p~ <- max(0, p~ - q_i) / Z (float64); with no acceptance the token is the
+ * inverse-CDF draw min{v : C_v > u * C_last}. */
+sb_status sb_select_branch(int32_t vocab, const float *d_logits_row,
+                           const sb_row_stats *d_stats_row, float temperature, int32_t n_cand,
+                           const int32_t *d_cand_tokens, const float *d_q, const float *d_u,
+                           int32_t *d_out, void *d_ws, size_t ws_bytes, hipStream_t stream);
+
+/* The accept/resample walk over the whole tree: from the root, Algorithm 1
+ * over a node's children in ascending row order (the chain test where there
+ * is one child); an accepted child becomes the node; when a leaf is reached
+ * the bonus token is drawn from its p, otherwise from the residual.
+ *   d_tokens: [n_rows]; h_parents: [n_rows] host tree;
+ *   d_logits / d_stats: the verify forward's outputs at T;
+ *   d_q: [n_rows][vocab] float32, row i the distribution draft row i was
+ *   drawn from (row 0 unused);
+ *   d_u: [n_rows] uniforms in [0,1): u[i] tests draft row i, u[0] drives the
+ *   final draw;
+ *   d_result: one sb_step_result (device). */
+sb_status sb_accept_resample(int32_t vocab, int32_t n_rows, const int32_t *d_tokens,
+                             const int32_t *h_parents, const float *d_logits,
+                             const sb_row_stats *d_stats, float temperature, const float *d_q,
+                             const float *d_u, sb_step_result *d_result, void *d_ws,
+                             size_t ws_bytes, hipStream_t stream);
+
+/* KV rollback (Section "Branch Resampling": non-selected branches and their
+ * KV are discarded): copies the K/V of the rows on d_result->path from slot
+ * kv_len + path[j] to slot kv_len + j for j = 0..path_len-1, in ascending j,
+ * and writes kv_len + path_len to *d_new_len.  kv_len must be the value
+ * given to the verify forward that wrote the tree rows. */
+sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
+                         const sb_step_result *d_result, int32_t *d_new_len,
+                         hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SB_H */

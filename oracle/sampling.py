@@ -41,7 +41,7 @@ import numpy as np
 
 from . import tree
 
-FLAG_NONFINITE = 1        # a target row holds NaN or Inf
+FLAG_NONFINITE = 1        # a target row holds NaN or +Inf
 FLAG_QZERO = 2            # a drafted token has q(x) == 0
 FLAG_ZERO_RESIDUAL = 4    # a residual had no mass; p~ left unchanged
 
@@ -59,16 +59,20 @@ def inv_temperature(T: float) -> np.float32:
 
 
 def row_stats(logits_row, T: float) -> RowStats:
+    """Statistics of one logits row.  A -inf logit is a masked token (zero
+    probability); NaN or +inf make the row non-finite, and its total is NaN
+    so that every later use of the row can see it."""
     l = np.asarray(logits_row, dtype=np.float32)
-    nonfinite = not bool(np.all(np.isfinite(l)))
-    am = int(np.argmax(l))
+    nonfinite = bool(np.any(np.isnan(l) | (l == np.inf)))
+    am = int(np.argmax(np.where(np.isnan(l), -np.inf, l)))
     if T > 0:
         z = l * inv_temperature(T)
-        M = np.float32(z.max())
-        w = np.exp(z - M)
-        S = math.fsum(w.astype(np.float64).tolist())
+        M = np.float32(np.max(np.where(np.isnan(z), -np.inf, z)))
+        with np.errstate(invalid="ignore", over="ignore"):
+            w = np.exp(z - M)
+        S = math.fsum(w.astype(np.float64).tolist()) if not nonfinite else float("nan")
         return RowStats(float(M), am, S, nonfinite)
-    return RowStats(float(l[am]), am, 1.0, nonfinite)
+    return RowStats(float(l[am]), am, float("nan") if nonfinite else 1.0, nonfinite)
 
 
 def target_probs(logits_row, T: float, st: RowStats | None = None) -> np.ndarray:
@@ -171,7 +175,7 @@ def accept_resample(tokens, parents, logits, T: float, q, u, stats=None,
     if stats is None:
         stats = [row_stats(logits[i], T) for i in range(N)]
     flags = 0
-    if any(s.nonfinite for s in stats):
+    if any(not math.isfinite(s.total) for s in stats):
         flags |= FLAG_NONFINITE
     node = 0
     path = [0]

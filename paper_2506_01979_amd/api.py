@@ -1,0 +1,353 @@
+"""Thin Python binding of libsb (``include/sb.h``) over ctypes.
+
+Argument marshalling only: every step of the verify path runs in the HIP
+kernels behind the C ABI.  PyTorch supplies device memory and the stream.
+Importing this module loads ``libsb.so`` from the package directory and
+raises if it is missing (build it with ``python -m paper_2506_01979_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsb.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(f"{_LIB_PATH} is missing: run `python -m paper_2506_01979_amd.build`")
+lib = C.CDLL(_LIB_PATH)
+
+SB_MAX_ROWS = 256
+SB_F32, SB_BF16 = 0, 1
+SB_W_QKV, SB_W_O, SB_W_GATE_UP, SB_W_DOWN, SB_W_LM_HEAD = range(5)
+SB_FLAG_NONFINITE, SB_FLAG_QZERO, SB_FLAG_ZERO_RESIDUAL = 1, 2, 4
+
+STATUS = {0: "SB_OK", 1: "SB_ERR_INVALID_ARG", 2: "SB_ERR_TREE", 3: "SB_ERR_CAPACITY",
+          4: "SB_ERR_DTYPE", 5: "SB_ERR_HIP", 6: "SB_ERR_UNSUPPORTED"}
+
+EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight",
+           "sb_model_create", "sb_model_destroy", "sb_workspace_bytes", "sb_verify_forward",
+           "sb_softmax_stats", "sb_sample_workspace_bytes", "sb_select_branch",
+           "sb_accept_resample", "sb_kv_rollback")
+
+
+class SBError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        msg = lib.sb_status_string(code).decode()
+        super().__init__(f"{where}: {STATUS.get(code, code)} ({msg})")
+
+
+class ModelConfig(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("hidden", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn", C.c_int32),
+                ("vocab", C.c_int32), ("rope_theta", C.c_float), ("rms_eps", C.c_float),
+                ("dtype", C.c_int32)]
+
+
+class LayerWeights(C.Structure):
+    _fields_ = [("attn_norm", C.c_void_p), ("qkv", C.c_void_p), ("o", C.c_void_p),
+                ("mlp_norm", C.c_void_p), ("gate_up", C.c_void_p), ("down", C.c_void_p)]
+
+
+class ModelWeights(C.Structure):
+    _fields_ = [("embed", C.c_void_p), ("final_norm", C.c_void_p), ("lm_head", C.c_void_p),
+                ("layers", C.POINTER(LayerWeights))]
+
+
+class KVCache(C.Structure):
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("capacity", C.c_int32)]
+
+
+ROW_STATS_DTYPE = np.dtype([("zmax", "<f4"), ("argmax", "<i4"), ("total", "<f8")])
+STEP_RESULT_INTS = 8 + SB_MAX_ROWS
+
+_vp, _i32, _sz, _f = C.c_void_p, C.c_int32, C.c_size_t, C.c_float
+lib.sb_status_string.restype = C.c_char_p
+lib.sb_status_string.argtypes = [_i32]
+lib.sb_version.restype = _i32
+lib.sb_packed_bytes.restype = _sz
+lib.sb_packed_bytes.argtypes = [C.POINTER(ModelConfig), _i32]
+lib.sb_pack_weight.restype = _i32
+lib.sb_pack_weight.argtypes = [C.POINTER(ModelConfig), _i32, _vp, _vp, _vp, _vp, _vp]
+lib.sb_model_create.restype = _i32
+lib.sb_model_create.argtypes = [C.POINTER(ModelConfig), C.POINTER(ModelWeights), C.POINTER(_vp)]
+lib.sb_model_destroy.restype = None
+lib.sb_model_destroy.argtypes = [_vp]
+lib.sb_workspace_bytes.restype = _sz
+lib.sb_workspace_bytes.argtypes = [_vp, _i32, _i32]
+lib.sb_verify_forward.restype = _i32
+lib.sb_verify_forward.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, C.POINTER(_i32), _i32, _f,
+                                  _vp, _vp, _vp, _sz, _vp]
+lib.sb_softmax_stats.restype = _i32
+lib.sb_softmax_stats.argtypes = [_i32, _i32, _vp, _f, _vp, _vp]
+lib.sb_sample_workspace_bytes.restype = _sz
+lib.sb_sample_workspace_bytes.argtypes = [_i32]
+lib.sb_select_branch.restype = _i32
+lib.sb_select_branch.argtypes = [_i32, _vp, _vp, _f, _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+lib.sb_accept_resample.restype = _i32
+lib.sb_accept_resample.argtypes = [_i32, _i32, _vp, C.POINTER(_i32), _vp, _vp, _f, _vp, _vp, _vp,
+                                   _vp, _sz, _vp]
+lib.sb_kv_rollback.restype = _i32
+lib.sb_kv_rollback.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, _vp, _vp]
+
+
+def _check(code: int, where: str) -> None:
+    if code != 0:
+        raise SBError(code, where)
+
+
+def _need(t: torch.Tensor, nbytes: int, what: str, dtype=None) -> None:
+    """Host-side check that a device buffer is large enough before a launch."""
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{what}: expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: expected a contiguous tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{what}: expected {dtype}, got {t.dtype}")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{what}: {have} bytes < {nbytes} needed")
+
+
+def _stream(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _host_i32(a) -> tuple:
+    arr = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return arr, arr.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def make_config(shape) -> ModelConfig:
+    return ModelConfig(shape.n_layers, shape.hidden, shape.n_heads, shape.n_kv_heads,
+                       shape.head_dim, shape.ffn, shape.vocab, shape.rope_theta, shape.rms_eps,
+                       SB_BF16 if shape.dtype == "bf16" else SB_F32)
+
+
+# ----------------------------------------------------------------------------
+# entry points (same names as the C ABI)
+# ----------------------------------------------------------------------------
+
+def sb_packed_bytes(cfg: ModelConfig, kind: int) -> int:
+    return int(lib.sb_packed_bytes(C.byref(cfg), kind))
+
+
+def sb_pack_weight(cfg: ModelConfig, kind: int, srcs, dst: torch.Tensor, stream=None) -> None:
+    s = list(srcs) + [None] * (3 - len(srcs))
+    _check(lib.sb_pack_weight(C.byref(cfg), kind, _ptr(s[0]), _ptr(s[1]), _ptr(s[2]),
+                              dst.data_ptr(), _stream(stream)), "sb_pack_weight")
+
+
+def sb_softmax_stats(logits: torch.Tensor, temperature: float, stats: torch.Tensor,
+                     stream=None) -> None:
+    n, v = logits.shape
+    _need(logits, n * v * 4, "logits", torch.float32)
+    _need(stats, n * 16, "stats")
+    _check(lib.sb_softmax_stats(v, n, logits.data_ptr(), temperature, stats.data_ptr(),
+                                _stream(stream)), "sb_softmax_stats")
+
+
+def sb_select_branch(logits_row: torch.Tensor, stats_row: torch.Tensor, temperature: float,
+                     cand_tokens: torch.Tensor, q: torch.Tensor, u: torch.Tensor,
+                     out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+    v = logits_row.shape[-1]
+    nc = cand_tokens.shape[0]
+    _need(logits_row, v * 4, "logits_row", torch.float32)
+    _need(stats_row, 16, "stats_row")
+    _need(cand_tokens, nc * 4, "cand_tokens", torch.int32)
+    _need(q, nc * v * 4, "q", torch.float32)
+    _need(u, (nc + 1) * 4, "u", torch.float32)
+    _need(out, 12, "out", torch.int32)
+    _need(ws, sb_sample_workspace_bytes(v), "ws")
+    _check(lib.sb_select_branch(logits_row.shape[-1], logits_row.data_ptr(), stats_row.data_ptr(),
+                                temperature, cand_tokens.shape[0], cand_tokens.data_ptr(),
+                                q.data_ptr(), u.data_ptr(), out.data_ptr(), ws.data_ptr(),
+                                ws.numel() * ws.element_size(), _stream(stream)),
+           "sb_select_branch")
+
+
+def sb_accept_resample(tokens: torch.Tensor, parents, logits: torch.Tensor, stats: torch.Tensor,
+                       temperature: float, q: torch.Tensor, u: torch.Tensor,
+                       result: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+    n, v = logits.shape[0], logits.shape[1]
+    par, pp = _host_i32(parents)
+    m = len(par)
+    _need(tokens, m * 4, "tokens", torch.int32)
+    _need(logits, m * v * 4, "logits", torch.float32)
+    _need(stats, m * 16, "stats")
+    _need(q, m * v * 4, "q", torch.float32)
+    _need(u, m * 4, "u", torch.float32)
+    _need(result, STEP_RESULT_INTS * 4, "result", torch.int32)
+    _need(ws, sb_sample_workspace_bytes(v), "ws")
+    _check(lib.sb_accept_resample(v, len(par), tokens.data_ptr(), pp, logits.data_ptr(),
+                                  stats.data_ptr(), temperature, q.data_ptr(), u.data_ptr(),
+                                  result.data_ptr(), ws.data_ptr(),
+                                  ws.numel() * ws.element_size(), _stream(stream)),
+           "sb_accept_resample")
+
+
+def sb_sample_workspace_bytes(vocab: int) -> int:
+    return int(lib.sb_sample_workspace_bytes(vocab))
+
+
+def new_stats(n: int, device="cuda") -> torch.Tensor:
+    return torch.empty((n, 4), dtype=torch.int32, device=device)
+
+
+def new_result(device="cuda") -> torch.Tensor:
+    return torch.full((STEP_RESULT_INTS,), -7, dtype=torch.int32, device=device)
+
+
+def decode_stats(stats: torch.Tensor) -> np.ndarray:
+    return stats.cpu().numpy().view(ROW_STATS_DTYPE).reshape(-1)
+
+
+def decode_result(res: torch.Tensor) -> dict:
+    a = res.cpu().numpy()
+    plen = int(a[3])
+    return {"n_accepted": int(a[0]), "branch": int(a[1]), "next_token": int(a[2]),
+            "path_len": plen, "flags": int(a[4]), "n_rejected": int(a[5]), "bonus": int(a[6]),
+            "path": [int(x) for x in a[8:8 + max(0, min(plen, SB_MAX_ROWS))]]}
+
+
+def synth_tensors(shape, seed: int = 0, bits: bool = True):
+    """tensor_fn over the seeded synthetic weights (bf16 shapes as bit
+    patterns, so the upload moves 2 bytes per weight)."""
+    from . import synth
+
+    def fn(name, layer=None):
+        if name.endswith("norm"):
+            return synth.norm_gain(shape)
+        return synth.weight(shape, name, layer, seed, as_bits=bits and shape.dtype == "bf16")
+    return fn
+
+
+def dict_tensors(weights: dict):
+    """tensor_fn over a weights dict shaped like ``synth.model_weights``."""
+    def fn(name, layer=None):
+        if layer is None:
+            return weights[name]
+        return weights["layers"][layer][name]
+    return fn
+
+
+class Model:
+    """A model handle with its packed weights resident on the device.
+
+    ``tensor_fn(name, layer)`` returns one weight as a numpy array (float32,
+    or uint16 bfloat16 bit patterns); names are ``embed``, ``lm_head``,
+    ``final_norm`` and per layer ``wq wk wv wo wg wu wd attn_norm mlp_norm``.
+    Tensors are uploaded one at a time and packed with ``sb_pack_weight``;
+    the unpacked sources are freed once packed.
+    """
+
+    def __init__(self, shape, tensor_fn, device="cuda", stream=None):
+        self.shape = shape
+        self.cfg = make_config(shape)
+        self.device = device
+        self.bf16 = shape.dtype == "bf16"
+        self.wdtype = torch.bfloat16 if self.bf16 else torch.float32
+        self._keep = []
+        st = stream if stream is not None else torch.cuda.current_stream()
+
+        def up(name, layer=None):
+            a = np.ascontiguousarray(tensor_fn(name, layer))
+            if a.dtype == np.uint16:   # bfloat16 bit patterns
+                t = torch.from_numpy(a.view(np.int16)).to(device).view(torch.bfloat16)
+            else:
+                t = torch.from_numpy(a).to(device=device, dtype=self.wdtype)
+            return t.to(self.wdtype)
+
+        def norm(name, layer=None):
+            t = torch.from_numpy(np.ascontiguousarray(tensor_fn(name, layer), dtype=np.float32))
+            t = t.to(device)
+            self._keep.append(t)
+            return t
+
+        def pack(kind, names, layer=None):
+            srcs = [up(n, layer) for n in names]
+            dst = torch.empty(sb_packed_bytes(self.cfg, kind), dtype=torch.uint8, device=device)
+            sb_pack_weight(self.cfg, kind, srcs, dst, st)
+            st.synchronize()
+            del srcs
+            self._keep.append(dst)
+            return dst
+
+        self.embed = up("embed")
+        self._keep.append(self.embed)
+        fin = norm("final_norm")
+        self.lm_head = pack(SB_W_LM_HEAD, ["lm_head"])
+        layers = (LayerWeights * shape.n_layers)()
+        for l in range(shape.n_layers):
+            qkv = pack(SB_W_QKV, ["wq", "wk", "wv"], l)
+            o = pack(SB_W_O, ["wo"], l)
+            gu = pack(SB_W_GATE_UP, ["wg", "wu"], l)
+            dn = pack(SB_W_DOWN, ["wd"], l)
+            layers[l] = LayerWeights(norm("attn_norm", l).data_ptr(), qkv.data_ptr(),
+                                     o.data_ptr(), norm("mlp_norm", l).data_ptr(),
+                                     gu.data_ptr(), dn.data_ptr())
+        self._layers = layers
+        mw = ModelWeights(self.embed.data_ptr(), fin.data_ptr(), self.lm_head.data_ptr(), layers)
+        h = C.c_void_p()
+        _check(lib.sb_model_create(C.byref(self.cfg), C.byref(mw), C.byref(h)), "sb_model_create")
+        self.handle = h
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            lib.sb_model_destroy(self.handle)
+            self.handle = None
+
+    def _check_kv(self, k: torch.Tensor, v: torch.Tensor) -> None:
+        s = self.shape
+        for t, nm in ((k, "k"), (v, "v")):
+            if t.dim() != 4 or tuple(t.shape[:2]) != (s.n_layers, s.n_kv_heads) \
+                    or t.shape[3] != s.head_dim:
+                raise ValueError(f"{nm} cache must be [n_layers][n_kv][capacity][head_dim]")
+            _need(t, t.numel() * t.element_size(), nm, self.wdtype)
+        if k.shape != v.shape:
+            raise ValueError("k and v caches differ in shape")
+
+    def new_kv(self, capacity: int):
+        s = self.shape
+        shp = (s.n_layers, s.n_kv_heads, capacity, s.head_dim)
+        k = torch.zeros(shp, dtype=self.wdtype, device=self.device)
+        v = torch.zeros(shp, dtype=self.wdtype, device=self.device)
+        return k, v
+
+    def workspace(self, max_rows: int, max_kv_len: int) -> torch.Tensor:
+        n = int(lib.sb_workspace_bytes(self.handle, max_rows, max_kv_len))
+        if n == 0:
+            raise SBError(1, "sb_workspace_bytes")
+        return torch.empty(n, dtype=torch.uint8, device=self.device)
+
+    def sb_verify_forward(self, k: torch.Tensor, v: torch.Tensor, kv_len: int,
+                          tokens: torch.Tensor, parents, temperature: float,
+                          logits: torch.Tensor, stats: torch.Tensor, ws: torch.Tensor,
+                          stream=None) -> None:
+        self._check_kv(k, v)
+        kv = KVCache(k.data_ptr(), v.data_ptr(), k.shape[2])
+        par, pp = _host_i32(parents)
+        n = len(par)
+        _need(tokens, n * 4, "tokens", torch.int32)
+        _need(logits, n * self.shape.vocab * 4, "logits", torch.float32)
+        _need(stats, n * 16, "stats")
+        _check(lib.sb_verify_forward(self.handle, C.byref(kv), kv_len, tokens.data_ptr(), pp,
+                                     len(par), temperature, logits.data_ptr(), stats.data_ptr(),
+                                     ws.data_ptr(), ws.numel() * ws.element_size(),
+                                     _stream(stream)), "sb_verify_forward")
+
+    def sb_kv_rollback(self, k: torch.Tensor, v: torch.Tensor, kv_len: int,
+                       result: torch.Tensor, new_len: torch.Tensor, stream=None) -> None:
+        self._check_kv(k, v)
+        _need(result, STEP_RESULT_INTS * 4, "result", torch.int32)
+        _need(new_len, 4, "new_len", torch.int32)
+        kv = KVCache(k.data_ptr(), v.data_ptr(), k.shape[2])
+        _check(lib.sb_kv_rollback(self.handle, C.byref(kv), kv_len, result.data_ptr(),
+                                  new_len.data_ptr(), _stream(stream)), "sb_kv_rollback")

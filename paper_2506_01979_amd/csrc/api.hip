@@ -1,0 +1,450 @@
+// C ABI of libsb: argument validation, workspace layout and the launch
+// sequence of the verify step.  Every check runs on the host before anything
+// is enqueued; the device work is in k_*.hip.
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "sb_internal_fwd.h"
+
+struct sb_model {
+  sb_model_config cfg;
+  std::vector<sb_layer_weights> layers;
+  const void *embed;
+  const float *final_norm;
+  const void *lm_head;
+};
+
+namespace sb {
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kF32MaxKeys = 15360;  // scores of one row in 60 KB of LDS
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  size_t meta, rope, h;
+  // bf16
+  size_t xa, act, q, part_o, part_ml;
+  // f32
+  size_t fa, qkv, fq, fo, gu, fact;
+  size_t total;
+  int np, n_chunks, ks_h, ks_o, ks_f;
+};
+
+Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
+  Layout L{};
+  const int np = round_up(n_rows, 16);
+  const int H = c.hidden, d = c.head_dim, F = c.ffn;
+  const int qd = c.n_heads * d, kvd = c.n_kv_heads * d;
+  const int G = c.n_heads / c.n_kv_heads;
+  L.np = np;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.meta = take(sizeof(Meta));
+  L.rope = take((size_t)np * (d / 2) * sizeof(float2));
+  L.h = take((size_t)np * H * sizeof(float));
+  if (c.dtype == SB_BF16) {
+    L.ks_h = ceil_div(H, 32);
+    L.ks_o = ceil_div(qd, 32);
+    L.ks_f = round_up(F, 32) / 32;
+    const int ksx = L.ks_h > L.ks_o ? L.ks_h : L.ks_o;
+    L.n_chunks = ceil_div(kv_len + n_rows, kAttnChunk);
+    L.xa = take((size_t)np * ksx * 32 * 2);
+    L.act = take((size_t)np * L.ks_f * 32 * 2);
+    L.q = take((size_t)np * qd * 2);
+    L.part_o = take((size_t)c.n_kv_heads * L.n_chunks * n_rows * G * d * sizeof(float));
+    L.part_ml = take((size_t)c.n_kv_heads * L.n_chunks * n_rows * G * 2 * sizeof(float));
+  } else {
+    L.fa = take((size_t)np * H * sizeof(float));
+    L.qkv = take((size_t)np * (qd + 2 * kvd) * sizeof(float));
+    L.fq = take((size_t)np * qd * sizeof(float));
+    L.fo = take((size_t)np * qd * sizeof(float));
+    L.gu = take((size_t)np * 2 * F * sizeof(float));
+    L.fact = take((size_t)np * F * sizeof(float));
+  }
+  L.total = off;
+  return L;
+}
+
+bool config_ok(const sb_model_config *c) {
+  if (!c) return false;
+  if (c->n_layers <= 0 || c->hidden <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 ||
+      c->head_dim <= 0 || c->ffn <= 0 || c->vocab <= 0)
+    return false;
+  if (c->n_heads % c->n_kv_heads != 0) return false;
+  if (c->head_dim % 16 != 0) return false;
+  if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 0.0f)) return false;
+  if (c->dtype != SB_F32 && c->dtype != SB_BF16) return false;
+  return true;
+}
+
+sb_status shape_supported(const sb_model_config *c) {
+  if (c->dtype == SB_BF16) {
+    if (c->head_dim != 64 && c->head_dim != 128) return SB_ERR_UNSUPPORTED;
+  } else {
+    if (c->head_dim > 256) return SB_ERR_UNSUPPORTED;
+  }
+  return SB_OK;
+}
+
+sb_status check_tree(const int32_t *parents, int n, TreeArg *out) {
+  if (!parents) return SB_ERR_INVALID_ARG;
+  if (n < 1 || n > SB_MAX_ROWS) return SB_ERR_INVALID_ARG;
+  if (parents[0] != -1) return SB_ERR_TREE;
+  for (int i = 1; i < n; ++i)
+    if (parents[i] < 0 || parents[i] >= i) return SB_ERR_TREE;
+  if (out) {
+    memset(out, 0, sizeof(*out));
+    out->n = n;
+    for (int i = 0; i < n; ++i) out->parent[i] = (int16_t)parents[i];
+    for (int i = n; i < SB_MAX_ROWS; ++i) out->parent[i] = -2;  // no row
+  }
+  return SB_OK;
+}
+
+inline sb_status hip_status(hipError_t e) { return e == hipSuccess ? SB_OK : SB_ERR_HIP; }
+
+#define SB_TRY(expr)                              \
+  do {                                            \
+    hipError_t _e = (expr);                       \
+    if (_e != hipSuccess) return SB_ERR_HIP;      \
+  } while (0)
+
+size_t elem_bytes(const sb_model_config &c) { return c.dtype == SB_BF16 ? 2 : 4; }
+
+sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int32_t *tokens,
+                       const TreeArg &tree, int n, float temperature, float *logits,
+                       sb_row_stats *stats, char *ws, const Layout &L, hipStream_t s) {
+  const sb_model_config &c = m->cfg;
+  const int H = c.hidden, d = c.head_dim;
+  const int tt = L.np / 16;
+  Meta *meta = (Meta *)(ws + L.meta);
+  float2 *rope = (float2 *)(ws + L.rope);
+  float *h = (float *)(ws + L.h);
+  uint16_t *xa = (uint16_t *)(ws + L.xa);
+  uint16_t *act = (uint16_t *)(ws + L.act);
+  uint16_t *q = (uint16_t *)(ws + L.q);
+
+  EmbedArgs ea{tokens, m->embed, h, c.vocab, H, n, kv_len, meta, rope, d, c.rope_theta};
+  SB_TRY(launch_embed_meta(ea, tree, L.np, 1, s));
+
+  const PackGeom gq = pack_geom(c, SB_W_QKV), go = pack_geom(c, SB_W_O),
+                 gg = pack_geom(c, SB_W_GATE_UP), gd = pack_geom(c, SB_W_DOWN),
+                 gl = pack_geom(c, SB_W_LM_HEAD);
+  const size_t layer_kv = (size_t)c.n_kv_heads * kv->capacity * d;
+
+  GemmArgs ga{};
+  ga.n_tok = n;
+  ga.q = q;
+  ga.cap = kv->capacity;
+  ga.kv_len = kv_len;
+  ga.n_heads = c.n_heads;
+  ga.n_kv = c.n_kv_heads;
+  ga.head_dim = d;
+  ga.rope = rope;
+  ga.h = h;
+  ga.act = act;
+  ga.act_ks = L.ks_f;
+  ga.logits = logits;
+
+  AttnArgs aa{};
+  aa.q = q;
+  aa.cap = kv->capacity;
+  aa.kv_len = kv_len;
+  aa.n_tok = n;
+  aa.n_heads = c.n_heads;
+  aa.n_kv = c.n_kv_heads;
+  aa.head_dim = d;
+  aa.chunk = kAttnChunk;
+  aa.n_chunks = L.n_chunks;
+  aa.meta = meta;
+  aa.scale = 1.0f / sqrtf((float)d);
+  aa.part_o = (float *)(ws + L.part_o);
+  aa.part_ml = (float *)(ws + L.part_ml);
+
+  for (int l = 0; l < c.n_layers; ++l) {
+    const sb_layer_weights &lw = m->layers[l];
+    uint16_t *kc = (uint16_t *)kv->k + l * layer_kv;
+    uint16_t *vc = (uint16_t *)kv->v + l * layer_kv;
+    SB_TRY(launch_rmsnorm_pack(h, lw.attn_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+    ga.W = (const uint16_t *)lw.qkv;
+    ga.X = xa;
+    ga.ks = gq.ks;
+    ga.kc = kc;
+    ga.vc = vc;
+    SB_TRY(launch_gemm(EPI_QKV, ga, gq.tiles, tt, s));
+    aa.kc = kc;
+    aa.vc = vc;
+    SB_TRY(launch_attn_bf16(aa, s));
+    SB_TRY(launch_attn_merge_bf16(aa, xa, L.ks_o, s));
+    ga.W = (const uint16_t *)lw.o;
+    ga.X = xa;
+    ga.ks = go.ks;
+    ga.out_rows = H;
+    SB_TRY(launch_gemm(EPI_RESID, ga, go.tiles, tt, s));
+    SB_TRY(launch_rmsnorm_pack(h, lw.mlp_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+    ga.W = (const uint16_t *)lw.gate_up;
+    ga.X = xa;
+    ga.ks = gg.ks;
+    SB_TRY(launch_gemm(EPI_SWIGLU, ga, gg.tiles, tt, s));
+    ga.W = (const uint16_t *)lw.down;
+    ga.X = act;
+    ga.ks = gd.ks;
+    ga.out_rows = H;
+    SB_TRY(launch_gemm(EPI_RESID, ga, gd.tiles, tt, s));
+  }
+  SB_TRY(launch_rmsnorm_pack(h, m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+  ga.W = (const uint16_t *)m->lm_head;
+  ga.X = xa;
+  ga.ks = gl.ks;
+  ga.out_rows = c.vocab;
+  SB_TRY(launch_gemm(EPI_LOGITS, ga, gl.tiles, tt, s));
+  SB_TRY(launch_softmax_stats(c.vocab, n, logits, temperature, stats, s));
+  return SB_OK;
+}
+
+sb_status forward_f32(sb_model *m, const sb_kv_cache *kv, int kv_len, const int32_t *tokens,
+                      const TreeArg &tree, int n, float temperature, float *logits,
+                      sb_row_stats *stats, char *ws, const Layout &L, hipStream_t s) {
+  const sb_model_config &c = m->cfg;
+  const int H = c.hidden, d = c.head_dim, F = c.ffn;
+  const int qd = c.n_heads * d, kvd = c.n_kv_heads * d;
+  Meta *meta = (Meta *)(ws + L.meta);
+  float2 *rope = (float2 *)(ws + L.rope);
+  float *h = (float *)(ws + L.h);
+  float *a = (float *)(ws + L.fa);
+  float *qkv = (float *)(ws + L.qkv);
+  float *q = (float *)(ws + L.fq);
+  float *o = (float *)(ws + L.fo);
+  float *gu = (float *)(ws + L.gu);
+  float *act = (float *)(ws + L.fact);
+
+  EmbedArgs ea{tokens, m->embed, h, c.vocab, H, n, kv_len, meta, rope, d, c.rope_theta};
+  SB_TRY(launch_embed_meta(ea, tree, n, 0, s));
+  const size_t layer_kv = (size_t)c.n_kv_heads * kv->capacity * d;
+
+  AttnArgs aa{};
+  aa.q = q;
+  aa.cap = kv->capacity;
+  aa.kv_len = kv_len;
+  aa.n_tok = n;
+  aa.n_heads = c.n_heads;
+  aa.n_kv = c.n_kv_heads;
+  aa.head_dim = d;
+  aa.meta = meta;
+  aa.scale = 1.0f / sqrtf((float)d);
+
+  for (int l = 0; l < c.n_layers; ++l) {
+    const sb_layer_weights &lw = m->layers[l];
+    float *kc = (float *)kv->k + l * layer_kv;
+    float *vc = (float *)kv->v + l * layer_kv;
+    SB_TRY(launch_f32_rmsnorm(h, lw.attn_norm, H, n, c.rms_eps, a, s));
+    SB_TRY(launch_f32_gemm(a, (const float *)lw.qkv, qkv, n, qd + 2 * kvd, H, qd + 2 * kvd, 0, s));
+    SB_TRY(launch_f32_rope_qkv(qkv, c, n, rope, q, kc, vc, kv->capacity, kv_len, s));
+    aa.kc = kc;
+    aa.vc = vc;
+    SB_TRY(launch_f32_attn(aa, o, s));
+    SB_TRY(launch_f32_gemm(o, (const float *)lw.o, h, n, H, qd, H, 1, s));
+    SB_TRY(launch_f32_rmsnorm(h, lw.mlp_norm, H, n, c.rms_eps, a, s));
+    SB_TRY(launch_f32_gemm(a, (const float *)lw.gate_up, gu, n, 2 * F, H, 2 * F, 0, s));
+    SB_TRY(launch_f32_swiglu(gu, n, F, act, s));
+    SB_TRY(launch_f32_gemm(act, (const float *)lw.down, h, n, H, F, H, 1, s));
+  }
+  SB_TRY(launch_f32_rmsnorm(h, m->final_norm, H, n, c.rms_eps, a, s));
+  SB_TRY(launch_f32_gemm(a, (const float *)m->lm_head, logits, n, c.vocab, H, c.vocab, 0, s));
+  SB_TRY(launch_softmax_stats(c.vocab, n, logits, temperature, stats, s));
+  return SB_OK;
+}
+
+bool temperature_ok(float t) { return isfinite(t) && t >= 0.0f; }
+
+}  // namespace
+}  // namespace sb
+
+using namespace sb;
+
+extern "C" {
+
+const char *sb_status_string(sb_status st) {
+  switch (st) {
+    case SB_OK:
+      return "ok";
+    case SB_ERR_INVALID_ARG:
+      return "invalid argument";
+    case SB_ERR_TREE:
+      return "parents do not form a rooted tree in row order";
+    case SB_ERR_CAPACITY:
+      return "KV capacity or workspace too small";
+    case SB_ERR_DTYPE:
+      return "dtype not supported for this call";
+    case SB_ERR_HIP:
+      return "HIP call or kernel launch failed";
+    case SB_ERR_UNSUPPORTED:
+      return "shape not supported by the kernels";
+  }
+  return "unknown status";
+}
+
+int32_t sb_version(void) { return 1; }
+
+size_t sb_packed_bytes(const sb_model_config *cfg, int32_t kind) {
+  if (!config_ok(cfg) || kind < SB_W_QKV || kind > SB_W_LM_HEAD) return 0;
+  return pack_geom(*cfg, kind).bytes;
+}
+
+sb_status sb_pack_weight(const sb_model_config *cfg, int32_t kind, const void *src0,
+                         const void *src1, const void *src2, void *dst, hipStream_t stream) {
+  if (!config_ok(cfg) || kind < SB_W_QKV || kind > SB_W_LM_HEAD || !src0 || !dst)
+    return SB_ERR_INVALID_ARG;
+  if ((kind == SB_W_QKV && (!src1 || !src2)) || (kind == SB_W_GATE_UP && !src1))
+    return SB_ERR_INVALID_ARG;
+  const sb_model_config &c = *cfg;
+  if (c.dtype == SB_BF16) {
+    if (shape_supported(cfg) != SB_OK) return SB_ERR_UNSUPPORTED;
+    return hip_status(launch_pack_bf16(kind, c, src0, src1, src2, dst, stream));
+  }
+  // float32: concatenated row-major sources
+  const size_t H = c.hidden, qd = (size_t)c.n_heads * c.head_dim,
+               kvd = (size_t)c.n_kv_heads * c.head_dim, F = c.ffn;
+  char *o = (char *)dst;
+  auto cp = [&](const void *src, size_t bytes) -> hipError_t {
+    hipError_t e = hipMemcpyAsync(o, src, bytes, hipMemcpyDeviceToDevice, stream);
+    o += bytes;
+    return e;
+  };
+  hipError_t e = hipSuccess;
+  switch (kind) {
+    case SB_W_QKV:
+      if ((e = cp(src0, qd * H * 4)) != hipSuccess) break;
+      if ((e = cp(src1, kvd * H * 4)) != hipSuccess) break;
+      e = cp(src2, kvd * H * 4);
+      break;
+    case SB_W_O:
+      e = cp(src0, H * qd * 4);
+      break;
+    case SB_W_GATE_UP:
+      if ((e = cp(src0, F * H * 4)) != hipSuccess) break;
+      e = cp(src1, F * H * 4);
+      break;
+    case SB_W_DOWN:
+      e = cp(src0, H * F * 4);
+      break;
+    case SB_W_LM_HEAD:
+      e = cp(src0, (size_t)c.vocab * H * 4);
+      break;
+  }
+  return hip_status(e);
+}
+
+sb_status sb_model_create(const sb_model_config *cfg, const sb_model_weights *w, sb_model **out) {
+  if (!out) return SB_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!config_ok(cfg) || !w) return SB_ERR_INVALID_ARG;
+  sb_status st = shape_supported(cfg);
+  if (st != SB_OK) return st;
+  if (!w->embed || !w->final_norm || !w->lm_head || !w->layers) return SB_ERR_INVALID_ARG;
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const sb_layer_weights &lw = w->layers[l];
+    if (!lw.attn_norm || !lw.qkv || !lw.o || !lw.mlp_norm || !lw.gate_up || !lw.down)
+      return SB_ERR_INVALID_ARG;
+  }
+  sb_model *m = new (std::nothrow) sb_model;
+  if (!m) return SB_ERR_INVALID_ARG;
+  m->cfg = *cfg;
+  m->layers.assign(w->layers, w->layers + cfg->n_layers);
+  m->embed = w->embed;
+  m->final_norm = w->final_norm;
+  m->lm_head = w->lm_head;
+  *out = m;
+  return SB_OK;
+}
+
+void sb_model_destroy(sb_model *m) { delete m; }
+
+size_t sb_workspace_bytes(const sb_model *m, int32_t max_rows, int32_t max_kv_len) {
+  if (!m || max_rows < 1 || max_rows > SB_MAX_ROWS || max_kv_len < 0) return 0;
+  return make_layout(m->cfg, max_rows, max_kv_len).total;
+}
+
+sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
+                            const int32_t *d_tokens, const int32_t *h_parents, int32_t n_rows,
+                            float temperature, float *d_logits, sb_row_stats *d_stats,
+                            void *d_ws, size_t ws_bytes, hipStream_t stream) {
+  if (!m || !kv || !kv->k || !kv->v || !d_tokens || !d_logits || !d_stats || !d_ws)
+    return SB_ERR_INVALID_ARG;
+  if (kv_len < 0 || !temperature_ok(temperature)) return SB_ERR_INVALID_ARG;
+  TreeArg tree;
+  sb_status st = check_tree(h_parents, n_rows, &tree);
+  if (st != SB_OK) return st;
+  if ((int64_t)kv_len + n_rows > kv->capacity) return SB_ERR_CAPACITY;
+  if (m->cfg.dtype == SB_F32 && kv_len + n_rows > kF32MaxKeys) return SB_ERR_UNSUPPORTED;
+  const Layout L = make_layout(m->cfg, n_rows, kv_len);
+  if (ws_bytes < L.total) return SB_ERR_CAPACITY;
+  if (m->cfg.dtype == SB_BF16)
+    return forward_bf16(m, kv, kv_len, d_tokens, tree, n_rows, temperature, d_logits, d_stats,
+                        (char *)d_ws, L, stream);
+  return forward_f32(m, kv, kv_len, d_tokens, tree, n_rows, temperature, d_logits, d_stats,
+                     (char *)d_ws, L, stream);
+}
+
+sb_status sb_softmax_stats(int32_t vocab, int32_t n_rows, const float *d_logits,
+                           float temperature, sb_row_stats *d_stats, hipStream_t stream) {
+  if (vocab < 1 || n_rows < 1 || !d_logits || !d_stats || !temperature_ok(temperature))
+    return SB_ERR_INVALID_ARG;
+  return hip_status(launch_softmax_stats(vocab, n_rows, d_logits, temperature, d_stats, stream));
+}
+
+size_t sb_sample_workspace_bytes(int32_t vocab) {
+  if (vocab < 1) return 0;
+  return sample_ws_bytes(vocab);
+}
+
+sb_status sb_select_branch(int32_t vocab, const float *d_logits_row,
+                           const sb_row_stats *d_stats_row, float temperature, int32_t n_cand,
+                           const int32_t *d_cand_tokens, const float *d_q, const float *d_u,
+                           int32_t *d_out, void *d_ws, size_t ws_bytes, hipStream_t stream) {
+  if (vocab < 1 || !d_logits_row || !d_stats_row || !d_cand_tokens || !d_q || !d_u || !d_out ||
+      !d_ws || !temperature_ok(temperature))
+    return SB_ERR_INVALID_ARG;
+  if (n_cand < 1 || n_cand > SB_MAX_ROWS) return SB_ERR_INVALID_ARG;
+  if (ws_bytes < sample_ws_bytes(vocab)) return SB_ERR_CAPACITY;
+  return hip_status(launch_select(vocab, d_logits_row, d_stats_row, temperature, n_cand,
+                                  d_cand_tokens, d_q, d_u, d_out, d_ws, stream));
+}
+
+sb_status sb_accept_resample(int32_t vocab, int32_t n_rows, const int32_t *d_tokens,
+                             const int32_t *h_parents, const float *d_logits,
+                             const sb_row_stats *d_stats, float temperature, const float *d_q,
+                             const float *d_u, sb_step_result *d_result, void *d_ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  if (vocab < 1 || !d_tokens || !d_logits || !d_stats || !d_q || !d_u || !d_result || !d_ws ||
+      !temperature_ok(temperature))
+    return SB_ERR_INVALID_ARG;
+  TreeArg tree;
+  sb_status st = check_tree(h_parents, n_rows, &tree);
+  if (st != SB_OK) return st;
+  if (ws_bytes < sample_ws_bytes(vocab)) return SB_ERR_CAPACITY;
+  return hip_status(launch_walk(vocab, tree, d_tokens, d_logits, d_stats, temperature, d_q, d_u,
+                                d_result, d_ws, stream));
+}
+
+sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
+                         const sb_step_result *d_result, int32_t *d_new_len,
+                         hipStream_t stream) {
+  if (!m || !kv || !kv->k || !kv->v || !d_result || !d_new_len) return SB_ERR_INVALID_ARG;
+  if (kv_len < 0 || kv_len >= kv->capacity) return SB_ERR_CAPACITY;
+  const sb_model_config &c = m->cfg;
+  const int row_bytes = c.head_dim * (int)elem_bytes(c);
+  return hip_status(launch_rollback(c.n_layers, c.n_kv_heads, kv->capacity, row_bytes, kv->k,
+                                    kv->v, kv_len, d_result, d_new_len, stream));
+}
+
+}  // extern "C"

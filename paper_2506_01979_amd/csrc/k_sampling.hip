@@ -1,0 +1,519 @@
+// Row softmax statistics, Branch Speculative Sampling at one node, and the
+// accept/resample walk over a token tree.
+//
+// What is computed (Preliminaries, "Speculative Decoding"; Appendix,
+// Algorithm 1 "Branch Speculative Sampling"):
+//   p(v)   = fl32(exp(fl32(fl32(l_v * fl32(1/T)) - zmax))) / total  (float64)
+//            or the one-hot at argmax when T = 0;
+//   accept = float64(u) < p~(x) / float64(q(x));
+//   reject : p~ <- max(0, p~ - q) / Z,  Z = sum max(0, p~ - q)   (float64),
+//            Z <= 0 keeps p~ and raises SB_FLAG_ZERO_RESIDUAL;
+//   draw   : C_v = running float64 sum of p~ in vocabulary order,
+//            y = min{v : C_v > u * C_last}; a zero-mass token is never drawn.
+// The multiply-then-subtract of the logit transform must not be contracted
+// into an FMA: every operation rounds on its own, as the definition states.
+#pragma clang fp contract(off)
+
+#include <float.h>
+#include <limits.h>
+#include <math.h>
+
+#include "sb_internal.h"
+
+namespace sb {
+namespace {
+
+constexpr int kWalkThreads = 1024;
+constexpr int kWaves = kWalkThreads / 64;
+
+__device__ __forceinline__ double wave_sum(double v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ int wave_min(int v) {
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ int wave_max(int v) {
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Block-wide reductions for blockDim.x == nthreads (multiple of 64).
+template <int NW>
+__device__ double block_sum(double v, double *red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v = wave_sum(v);
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  double t = 0.0;
+  if (w == 0) {
+    t = lane < NW ? red[lane] : 0.0;
+    t = wave_sum(t);
+    if (lane == 0) red[NW] = t;
+  }
+  __syncthreads();
+  t = red[NW];
+  __syncthreads();
+  return t;
+}
+
+template <int NW>
+__device__ int block_min(int v, int *red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v = wave_min(v);
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  if (w == 0) {
+    int t = lane < NW ? red[lane] : INT_MAX;
+    t = wave_min(t);
+    if (lane == 0) red[NW] = t;
+  }
+  __syncthreads();
+  int r = red[NW];
+  __syncthreads();
+  return r;
+}
+
+template <int NW>
+__device__ int block_max(int v, int *red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v = wave_max(v);
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  if (w == 0) {
+    int t = lane < NW ? red[lane] : INT_MIN;
+    t = wave_max(t);
+    if (lane == 0) red[NW] = t;
+  }
+  __syncthreads();
+  int r = red[NW];
+  __syncthreads();
+  return r;
+}
+
+// Exclusive prefix sum over the block (one value per thread).  Each prefix
+// is a sum of earlier values only (no subtraction of the own value).
+template <int NW>
+__device__ double block_exclusive_scan(double v, double *red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  double inc = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    double t = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += t;
+  }
+  double exc = __shfl_up(inc, 1, 64);
+  if (lane == 0) exc = 0.0;
+  if (lane == 63) red[w] = inc;
+  __syncthreads();
+  if (w == 0) {
+    double t = lane < NW ? red[lane] : 0.0;
+    double ti = t;
+    for (int o = 1; o < 64; o <<= 1) {
+      double s = __shfl_up(ti, o, 64);
+      if (lane >= o) ti += s;
+    }
+    double te = __shfl_up(ti, 1, 64);
+    if (lane == 0) te = 0.0;
+    if (lane < NW) red[lane] = te;  // each lane rewrites only its own entry
+  }
+  __syncthreads();
+  double r = (w == 0) ? exc : red[w] + exc;
+  __syncthreads();
+  return r;
+}
+
+// A target distribution p~: either a logits row with its statistics, or an
+// explicit float64 array in the workspace (after a rejection).
+struct Dist {
+  const float *l;
+  float inv_t;
+  float zmax;
+  double total;
+  int argmax;
+  int greedy;
+  const double *arr;  // non-null: explicit array
+
+  __device__ __forceinline__ double at(int v) const {
+    if (arr) return arr[v];
+    if (greedy) return v == argmax ? 1.0 : 0.0;
+    float z = l[v] * inv_t;
+    float e = expf(z - zmax);
+    return (double)e / total;
+  }
+};
+
+__device__ __forceinline__ Dist row_dist(const float *l, const sb_row_stats &st, float inv_t,
+                                         int greedy) {
+  Dist d;
+  d.l = l;
+  d.inv_t = inv_t;
+  d.zmax = st.zmax;
+  d.total = st.total;
+  d.argmax = st.argmax;
+  d.greedy = greedy;
+  d.arr = nullptr;
+  return d;
+}
+
+struct Shared {
+  double red[kWaves + 1];
+  int ired[kWaves + 1];
+  int decision;
+  double z;
+};
+
+// After candidate with draft row q is rejected: p~ <- max(0, p~ - q)/Z.
+// Writes the new array to dst; returns Z (all threads).
+__device__ double residual_pass(const Dist &cur, const float *q, int vocab, double *dst,
+                                Shared &sh) {
+  double part = 0.0;
+  for (int v = threadIdx.x; v < vocab; v += kWalkThreads) {
+    double r = cur.at(v) - (double)q[v];
+    r = r > 0.0 ? r : 0.0;
+    dst[v] = r;
+    part += r;
+  }
+  double Z = block_sum<kWaves>(part, sh.red);
+  if (Z > 0.0) {
+    for (int v = threadIdx.x; v < vocab; v += kWalkThreads) dst[v] = dst[v] / Z;
+  }
+  __syncthreads();
+  return Z;
+}
+
+// Inverse-CDF draw from p~ with uniform u (all threads return the token).
+__device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
+  const int chunk = (vocab + kWalkThreads - 1) / kWalkThreads;
+  const int lo = threadIdx.x * chunk;
+  const int hi = min(vocab, lo + chunk);
+  double s = 0.0;
+  for (int v = lo; v < hi; ++v) s += d.at(v);
+  double e = block_exclusive_scan<kWaves>(s, sh.red);
+  // the thread owning the last element publishes C_last = e + s
+  const int last_owner = (vocab - 1) / chunk;
+  if ((int)threadIdx.x == last_owner) sh.z = e + s;
+  __syncthreads();
+  const double W = sh.z;
+  const double thr = (double)u * W;
+  int cand = INT_MAX;
+  double run = 0.0;
+  for (int v = lo; v < hi; ++v) {
+    run += d.at(v);
+    if (e + run > thr) {
+      cand = v;
+      break;
+    }
+  }
+  int y = block_min<kWaves>(cand, sh.ired);
+  if (y == INT_MAX) {
+    // rounding left no crossing: the last token with positive mass
+    int lp = -1;
+    for (int v = lo; v < hi; ++v)
+      if (d.at(v) > 0.0) lp = v;
+    y = block_max<kWaves>(lp, sh.ired);
+    if (y < 0) y = vocab - 1;
+  }
+  return y;
+}
+
+// Algorithm 1 at one node.  Candidate i: token tok(i), draft row q(i),
+// uniform u(i).  Returns the accepted candidate index or -1; on -1, *cur
+// holds the final residual.  ws0/ws1 are two float64 [vocab] buffers.
+template <class Cand>
+__device__ int node_select(Dist *cur, const Cand &cand, int n_cand, int vocab, double *ws0,
+                           double *ws1, int *flags, int *nrej, Shared &sh) {
+  for (int i = 0; i < n_cand; ++i) {
+    if (threadIdx.x == 0) {
+      const int x = cand.tok(i);
+      double ratio = 0.0;  // a token id outside the vocabulary is rejected
+      if (x >= 0 && x < vocab) {
+        const double qx = (double)cand.q(i)[x];
+        if (qx == 0.0) *flags |= SB_FLAG_QZERO;
+        ratio = cur->at(x) / qx;
+      } else {
+        *flags |= SB_FLAG_QZERO;
+      }
+      sh.decision = ((double)cand.u(i) < ratio) ? 1 : 0;
+    }
+    __syncthreads();
+    const int acc = sh.decision;
+    __syncthreads();
+    if (acc) return i;
+    ++*nrej;
+    double *dst = (cur->arr == ws0) ? ws1 : ws0;
+    double Z = residual_pass(*cur, cand.q(i), vocab, dst, sh);
+    if (Z > 0.0) {
+      cur->arr = dst;
+    } else if (threadIdx.x == 0) {
+      *flags |= SB_FLAG_ZERO_RESIDUAL;
+    }
+  }
+  return -1;
+}
+
+struct ExplicitCands {
+  const int32_t *toks;
+  const float *qbase;
+  const float *ubase;
+  int vocab;
+  __device__ int tok(int i) const { return toks[i]; }
+  __device__ const float *q(int i) const { return qbase + (size_t)i * vocab; }
+  __device__ float u(int i) const { return ubase[i]; }
+};
+
+struct ChildCands {
+  const int16_t *kids;
+  const int32_t *toks;
+  const float *qbase;
+  const float *ubase;
+  int vocab;
+  __device__ int tok(int i) const { return toks[kids[i]]; }
+  __device__ const float *q(int i) const { return qbase + (size_t)kids[i] * vocab; }
+  __device__ float u(int i) const { return ubase[kids[i]]; }
+};
+
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(512) void k_softmax_stats(const float *__restrict__ logits, int vocab,
+                                                      float inv_t, int greedy,
+                                                      sb_row_stats *__restrict__ out) {
+  constexpr int NT = 512, NW = NT / 64;
+  __shared__ float smax[NW];
+  __shared__ int sarg[NW];
+  __shared__ int sbad[NW];
+  __shared__ double red[NW + 1];
+  const float *l = logits + (size_t)blockIdx.x * vocab;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // pass 1: max of l (argmax, lowest index) and max of z = fl32(l / T)
+  float best = -INFINITY;
+  int barg = INT_MAX;
+  float zbest = -INFINITY;
+  int bad = 0;
+  for (int v = threadIdx.x; v < vocab; v += NT) {
+    const float x = l[v];
+    if (isnan(x) || x == INFINITY) bad = 1;
+    if (x > best) {
+      best = x;
+      barg = v;
+    }
+    const float z = x * inv_t;
+    zbest = fmaxf(zbest, z);
+  }
+  // argmax: larger value wins, equal values -> lower index
+  for (int o = 32; o > 0; o >>= 1) {
+    float ob = __shfl_xor(best, o, 64);
+    int oa = __shfl_xor(barg, o, 64);
+    if (ob > best || (ob == best && oa < barg)) {
+      best = ob;
+      barg = oa;
+    }
+    zbest = fmaxf(zbest, __shfl_xor(zbest, o, 64));
+    bad |= __shfl_xor(bad, o, 64);
+  }
+  if (lane == 0) {
+    smax[w] = best;
+    sarg[w] = barg;
+    sbad[w] = bad;
+    red[w] = (double)zbest;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float b = smax[0];
+    int a = sarg[0];
+    float zb = (float)red[0];
+    int bd = sbad[0];
+    for (int i = 1; i < NW; ++i) {
+      if (smax[i] > b || (smax[i] == b && sarg[i] < a)) {
+        b = smax[i];
+        a = sarg[i];
+      }
+      zb = fmaxf(zb, (float)red[i]);
+      bd |= sbad[i];
+    }
+    smax[0] = greedy ? b : zb;
+    sarg[0] = (a == INT_MAX) ? 0 : a;
+    sbad[0] = bd;
+  }
+  __syncthreads();
+  const float zmax = smax[0];
+  const int arg = sarg[0];
+  const int anybad = sbad[0];
+  __syncthreads();
+  double total = 1.0;
+  if (!greedy) {
+    double part = 0.0;
+    for (int v = threadIdx.x; v < vocab; v += NT) {
+      const float z = l[v] * inv_t;
+      part += (double)expf(z - zmax);
+    }
+    part = wave_sum(part);
+    if (lane == 0) red[w] = part;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double t = 0.0;
+      for (int i = 0; i < NW; ++i) t += red[i];
+      red[NW] = t;
+    }
+    __syncthreads();
+    total = red[NW];
+  }
+  if (threadIdx.x == 0) {
+    sb_row_stats st;
+    st.zmax = zmax;
+    st.argmax = arg;
+    st.total = anybad ? (double)NAN : total;
+    out[blockIdx.x] = st;
+  }
+}
+
+__global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
+                                                       const int32_t *__restrict__ tokens,
+                                                       const float *__restrict__ logits,
+                                                       const sb_row_stats *__restrict__ stats,
+                                                       float inv_t, int greedy,
+                                                       const float *__restrict__ q,
+                                                       const float *__restrict__ u,
+                                                       sb_step_result *__restrict__ result,
+                                                       double *__restrict__ ws) {
+  __shared__ Shared sh;
+  __shared__ int16_t kids[SB_MAX_ROWS];
+  __shared__ int16_t path[SB_MAX_ROWS];
+  __shared__ int nk;
+  __shared__ int s_flags;
+  const int n = tree.n;
+  double *ws0 = ws;
+  double *ws1 = ws + vocab;
+  if (threadIdx.x == 0) s_flags = 0;
+  __syncthreads();
+  if ((int)threadIdx.x < n && isnan(stats[threadIdx.x].total)) atomicOr(&s_flags, SB_FLAG_NONFINITE);
+  __syncthreads();
+  int flags = 0;  // thread 0 accumulates
+  int nrej = 0;
+  int node = 0;
+  int plen = 1;
+  if (threadIdx.x == 0) path[0] = 0;
+  Dist cur = row_dist(logits, stats[0], inv_t, greedy);
+  int y = 0;
+  int bonus = 0;
+  for (;;) {
+    if (threadIdx.x == 0) {
+      int c = 0;
+      for (int j = node + 1; j < n; ++j)
+        if (tree.parent[j] == node) kids[c++] = (int16_t)j;
+      nk = c;
+    }
+    __syncthreads();
+    const int nkids = nk;
+    if (nkids == 0) {
+      bonus = 1;
+      y = draw_pass(cur, u[0], vocab, sh);
+      break;
+    }
+    ChildCands cc{kids, tokens, q, u, vocab};
+    const int acc = node_select(&cur, cc, nkids, vocab, ws0, ws1, &flags, &nrej, sh);
+    if (acc >= 0) {
+      node = kids[acc];
+      __syncthreads();
+      if (threadIdx.x == 0) path[plen] = (int16_t)node;
+      ++plen;
+      cur = row_dist(logits + (size_t)node * vocab, stats[node], inv_t, greedy);
+      continue;
+    }
+    y = draw_pass(cur, u[0], vocab, sh);
+    break;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int branch = -1;
+    if (plen > 1) {
+      int ord = 0;
+      for (int j = 1; j < path[1]; ++j)
+        if (tree.parent[j] == 0) ++ord;
+      branch = ord;
+    }
+    result->n_accepted = plen - 1;
+    result->branch = branch;
+    result->next_token = y;
+    result->path_len = plen;
+    result->flags = flags | s_flags;
+    result->n_rejected = nrej;
+    result->bonus = bonus;
+    result->reserved = 0;
+  }
+  for (int j = threadIdx.x; j < SB_MAX_ROWS; j += kWalkThreads)
+    result->path[j] = j < plen ? (int32_t)path[j] : -1;
+}
+
+__global__ __launch_bounds__(kWalkThreads) void k_select(int vocab, const float *__restrict__ lrow,
+                                                         const sb_row_stats *__restrict__ st,
+                                                         float inv_t, int greedy, int n_cand,
+                                                         const int32_t *__restrict__ ctoks,
+                                                         const float *__restrict__ q,
+                                                         const float *__restrict__ u,
+                                                         int32_t *__restrict__ out,
+                                                         double *__restrict__ ws) {
+  __shared__ Shared sh;
+  int flags = 0, nrej = 0;
+  const sb_row_stats s0 = st[0];
+  if (isnan(s0.total)) flags |= SB_FLAG_NONFINITE;
+  Dist cur = row_dist(lrow, s0, inv_t, greedy);
+  ExplicitCands ec{ctoks, q, u, vocab};
+  const int acc = node_select(&cur, ec, n_cand, vocab, ws, ws + vocab, &flags, &nrej, sh);
+  int tok;
+  if (acc >= 0) {
+    tok = ctoks[acc];
+  } else {
+    tok = draw_pass(cur, u[n_cand], vocab, sh);
+  }
+  if (threadIdx.x == 0) {
+    out[0] = acc;
+    out[1] = tok;
+    out[2] = flags;
+  }
+}
+
+}  // namespace
+
+size_t sample_ws_bytes(int vocab) { return (size_t)2 * (size_t)vocab * sizeof(double); }
+
+static inline void temp_args(float temperature, float *inv_t, int *greedy) {
+  *greedy = temperature <= 0.0f ? 1 : 0;
+  *inv_t = *greedy ? 1.0f : 1.0f / temperature;
+}
+
+hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, float temperature,
+                                sb_row_stats *stats, hipStream_t s) {
+  float inv_t;
+  int greedy;
+  temp_args(temperature, &inv_t, &greedy);
+  hipLaunchKernelGGL(k_softmax_stats, dim3(n_rows), dim3(512), 0, s, logits, vocab, inv_t, greedy,
+                     stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_walk(int vocab, const TreeArg &tree, const int32_t *tokens, const float *logits,
+                       const sb_row_stats *stats, float temperature, const float *q,
+                       const float *u, sb_step_result *result, void *ws, hipStream_t s) {
+  float inv_t;
+  int greedy;
+  temp_args(temperature, &inv_t, &greedy);
+  hipLaunchKernelGGL(k_walk, dim3(1), dim3(kWalkThreads), 0, s, vocab, tree, tokens, logits, stats,
+                     inv_t, greedy, q, u, result, (double *)ws);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(int vocab, const float *logits_row, const sb_row_stats *stats_row,
+                         float temperature, int n_cand, const int32_t *cand_tokens,
+                         const float *q, const float *u, int32_t *out, void *ws, hipStream_t s) {
+  float inv_t;
+  int greedy;
+  temp_args(temperature, &inv_t, &greedy);
+  hipLaunchKernelGGL(k_select, dim3(1), dim3(kWalkThreads), 0, s, vocab, logits_row, stats_row,
+                     inv_t, greedy, n_cand, cand_tokens, q, u, out, (double *)ws);
+  return hipGetLastError();
+}
+
+}  // namespace sb

@@ -1,0 +1,45 @@
+// Device helpers shared by the forward kernels (bf16 storage, MFMA types).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sb {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (data read once: weights)
+__device__ __forceinline__ uint4 load_stream(const uint4 *p) {
+  u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// float -> bfloat16 bits, round to nearest even (inputs are finite here;
+// NaN keeps a quiet NaN pattern)
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Index of element (row t, column k) in the "packed operand" layout used for
+// every bf16 matrix-core input: [t/16][k/32][lane][8] with
+// lane = (t % 16) + 16 * ((k % 32) / 8) and element k % 8.  ksteps = K/32.
+__device__ __forceinline__ size_t packed_index(int t, int k, int ksteps) {
+  const int tt = t >> 4, s = k >> 5;
+  const int lane = (t & 15) + 16 * ((k & 31) >> 3);
+  return (((size_t)tt * ksteps + s) * 64 + lane) * 8 + (k & 7);
+}
+
+}  // namespace sb

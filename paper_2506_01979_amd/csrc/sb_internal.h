@@ -1,0 +1,32 @@
+// Internal declarations shared by the HIP translation units of libsb.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sb.h"
+
+namespace sb {
+
+// Tree passed by value to kernels (parents as int16, row 0 = root).
+struct TreeArg {
+  int32_t n;
+  int16_t parent[SB_MAX_ROWS];
+};
+
+// ---- sampling (k_sampling.hip) --------------------------------------------
+hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, float temperature,
+                                sb_row_stats *stats, hipStream_t s);
+hipError_t launch_walk(int vocab, const TreeArg &tree, const int32_t *tokens, const float *logits,
+                       const sb_row_stats *stats, float temperature, const float *q,
+                       const float *u, sb_step_result *result, void *ws, hipStream_t s);
+hipError_t launch_select(int vocab, const float *logits_row, const sb_row_stats *stats_row,
+                         float temperature, int n_cand, const int32_t *cand_tokens,
+                         const float *q, const float *u, int32_t *out, void *ws, hipStream_t s);
+size_t sample_ws_bytes(int vocab);
+
+// ---- rollback (k_rollback.hip) ---------------------------------------------
+hipError_t launch_rollback(int n_layers, int n_kv, int capacity, int row_bytes, void *k, void *v,
+                           int kv_len, const sb_step_result *res, int32_t *new_len, hipStream_t s);
+
+}  // namespace sb

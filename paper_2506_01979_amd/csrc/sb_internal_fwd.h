@@ -1,0 +1,140 @@
+// Internal declarations of the forward path (host + device visible).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sb_internal.h"
+
+namespace sb {
+
+enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+
+// Per-row tree metadata kept in the workspace.
+struct Meta {
+  int32_t pos[SB_MAX_ROWS];      // kv_len + depth(i)
+  uint32_t anc[SB_MAX_ROWS][8];  // bit j: row j is on the path root..i
+};
+
+// Geometry of a packed weight kind.
+struct PackGeom {
+  int K;       // source columns
+  int ks;      // packed k-steps (bf16: K padded to 32)
+  int tiles;   // 16-row tiles (bf16)
+  int rows;    // output rows (natural-order kinds) / total rows (f32)
+  size_t bytes;
+};
+
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+inline int round_up(int a, int b) { return ceil_div(a, b) * b; }
+
+inline PackGeom pack_geom(const sb_model_config &c, int kind) {
+  PackGeom g{};
+  const int H = c.hidden, d = c.head_dim, F = c.ffn;
+  const int qd = c.n_heads * d, kvd = c.n_kv_heads * d;
+  const bool bf = c.dtype == SB_BF16;
+  switch (kind) {
+    case SB_W_QKV:
+      g.K = H;
+      g.rows = qd + 2 * kvd;
+      g.tiles = (qd + 2 * kvd) / 16;
+      break;
+    case SB_W_O:
+      g.K = qd;
+      g.rows = H;
+      g.tiles = ceil_div(H, 16);
+      break;
+    case SB_W_GATE_UP:
+      g.K = H;
+      g.rows = 2 * F;
+      g.tiles = round_up(F, 32) / 8;
+      break;
+    case SB_W_DOWN:
+      g.K = F;
+      g.rows = H;
+      g.tiles = ceil_div(H, 16);
+      break;
+    case SB_W_LM_HEAD:
+      g.K = H;
+      g.rows = c.vocab;
+      g.tiles = ceil_div(c.vocab, 16);
+      break;
+    default:
+      return g;
+  }
+  if (bf) {
+    g.ks = ceil_div(g.K, 32);
+    g.bytes = (size_t)g.tiles * g.ks * 1024;
+  } else {
+    g.ks = g.K;
+    g.bytes = (size_t)g.rows * g.K * sizeof(float);
+  }
+  return g;
+}
+
+struct EmbedArgs {
+  const int32_t *tokens;
+  const void *embed;
+  float *h;
+  int vocab, hidden, n_tok, kv_len;
+  Meta *meta;
+  float2 *rope;  // [n_tok][head_dim/2] cos, sin
+  int head_dim;
+  float rope_theta;
+};
+
+struct GemmArgs {
+  const uint16_t *W;   // packed weights
+  const uint16_t *X;   // packed activations
+  int ks;              // k-steps
+  int n_tok;           // valid activation rows
+  int out_rows;        // RESID: hidden; LOGITS: vocab
+  float *h;            // RESID output (fp32 [rows][out_rows])
+  float *logits;       // LOGITS output
+  uint16_t *act;       // SWIGLU output (packed, act_ks k-steps)
+  int act_ks;
+  uint16_t *q;         // QKV: q after RoPE, [rows][n_heads][head_dim]
+  uint16_t *kc, *vc;   // QKV: this layer's cache [n_kv][cap][head_dim]
+  int cap, kv_len;
+  int n_heads, n_kv, head_dim;
+  const float2 *rope;  // [rows][head_dim/2]
+};
+
+struct AttnArgs {
+  const void *q;        // bf16 or f32 [rows][n_heads][d]
+  const void *kc, *vc;  // this layer's cache [n_kv][cap][d]
+  int cap, kv_len, n_tok, n_heads, n_kv, head_dim;
+  int chunk, n_chunks;
+  const Meta *meta;
+  float scale;
+  float *part_o;   // [n_kv][n_chunks][R][d]
+  float *part_ml;  // [n_kv][n_chunks][R][2]
+};
+
+// k_bf16.hip
+hipError_t launch_pack_bf16(int kind, const sb_model_config &c, const void *src0, const void *src1,
+                            const void *src2, void *dst, hipStream_t s);
+hipError_t launch_embed_meta(const EmbedArgs &a, const TreeArg &tree, int blocks, int bf16,
+                             hipStream_t s);
+hipError_t launch_rmsnorm_pack(const float *h, const float *g, int hidden, int ks, int n_tok,
+                               int n_pad, float eps, uint16_t *out, hipStream_t s);
+hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int tt, hipStream_t s);
+
+// k_attn.hip
+constexpr int kAttnChunk = 128;
+hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s);
+hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,
+                                  hipStream_t s);
+
+// k_f32.hip
+hipError_t launch_f32_rmsnorm(const float *h, const float *g, int hidden, int n_tok, float eps,
+                              float *out, hipStream_t s);
+hipError_t launch_f32_gemm(const float *X, const float *W, float *Y, int n_tok, int M, int K,
+                           int ldy, int accumulate, hipStream_t s);
+hipError_t launch_f32_rope_qkv(const float *qkv, const sb_model_config &c, int n_tok,
+                               const float2 *rope, float *q, float *kc, float *vc, int cap,
+                               int kv_len, hipStream_t s);
+hipError_t launch_f32_attn(const AttnArgs &a, float *out, hipStream_t s);
+hipError_t launch_f32_swiglu(const float *gu, int n_tok, int ffn, float *act, hipStream_t s);
+
+}  // namespace sb

@@ -1,0 +1,89 @@
+"""CPU checks of the C ABI: the library loads, exports every entry point
+that include/sb.h declares, and rejects bad arguments on the host before
+anything reaches a device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sb.h")
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sb_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2506_01979_amd import api as A
+    return A
+
+
+def test_exports_every_declared_symbol(api):
+    names = declared()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(api.lib, n), n
+    assert set(api.EXPORTS) == set(names)
+
+
+def test_version_and_strings(api):
+    assert api.lib.sb_version() == 1
+    for code in range(7):
+        assert api.lib.sb_status_string(code)
+
+
+def cfg(api, **kw):
+    from paper_2506_01979_amd import synth
+    c = api.make_config(synth.SHAPES["llama7b"])
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def test_packed_bytes(api):
+    c = cfg(api)
+    # 7B shape: QKV 12288 x 4096, O 4096 x 4096, gate/up 2 x 11008 x 4096,
+    # down 4096 x 11008, LM head 32000 x 4096 -- bf16, no padding needed
+    assert api.sb_packed_bytes(c, api.SB_W_QKV) == 12288 * 4096 * 2
+    assert api.sb_packed_bytes(c, api.SB_W_O) == 4096 * 4096 * 2
+    assert api.sb_packed_bytes(c, api.SB_W_GATE_UP) == 2 * 11008 * 4096 * 2
+    assert api.sb_packed_bytes(c, api.SB_W_DOWN) == 4096 * 11008 * 2
+    assert api.sb_packed_bytes(c, api.SB_W_LM_HEAD) == 32000 * 4096 * 2
+    assert api.sb_packed_bytes(c, 9) == 0
+    bad = cfg(api, n_kv_heads=5)
+    assert api.sb_packed_bytes(bad, api.SB_W_QKV) == 0
+    # ragged ffn (688) and vocab (1000) are padded to whole tiles
+    from paper_2506_01979_amd import synth
+    s = api.make_config(synth.SHAPES["small_bf16"])
+    assert api.sb_packed_bytes(s, api.SB_W_DOWN) == 256 * 704 * 2
+    assert api.sb_packed_bytes(s, api.SB_W_LM_HEAD) == 1008 * 256 * 2
+
+
+def test_host_validation_without_device(api):
+    lib = api.lib
+    c = cfg(api)
+    h = C.c_void_p()
+    assert lib.sb_model_create(C.byref(c), None, C.byref(h)) == 1
+    assert lib.sb_model_create(None, None, C.byref(h)) == 1
+    bad = cfg(api, head_dim=96)
+    w = api.ModelWeights(1, 1, 1, (api.LayerWeights * 32)())
+    assert lib.sb_model_create(C.byref(bad), C.byref(w), C.byref(h)) == 6
+    assert lib.sb_workspace_bytes(None, 4, 10) == 0
+    kv = api.KVCache(1, 1, 100)
+    par = (C.c_int32 * 3)(-1, 0, 1)
+    assert lib.sb_verify_forward(None, C.byref(kv), 10, 1, par, 3, 1.0, 1, 1, 1, 10, None) == 1
+    assert lib.sb_softmax_stats(0, 1, 1, 1.0, 1, None) == 1
+    assert lib.sb_softmax_stats(10, 1, 1, -1.0, 1, None) == 1
+    bad_par = (C.c_int32 * 3)(-1, 0, 2)
+    assert lib.sb_accept_resample(10, 3, 1, bad_par, 1, 1, 1.0, 1, 1, 1, 1, 1 << 20, None) == 2
+    root_par = (C.c_int32 * 2)(0, 0)
+    assert lib.sb_accept_resample(10, 2, 1, root_par, 1, 1, 1.0, 1, 1, 1, 1, 1 << 20, None) == 2
+    assert lib.sb_accept_resample(10, 3, 1, par, 1, 1, 1.0, 1, 1, 1, 1, 8, None) == 3
+    assert lib.sb_select_branch(10, 1, 1, 1.0, 0, 1, 1, 1, 1, 1, 1 << 20, None) == 1
+    assert lib.sb_kv_rollback(None, C.byref(kv), 3, 1, 1, None) == 1
+    assert lib.sb_sample_workspace_bytes(1000) == 16000

@@ -1,0 +1,186 @@
+"""GPU parity of sb_verify_forward against the oracle decoder.
+
+Logits must match per row within 1e-4 (float32 models, against the float64
+oracle) or 2e-2 (bfloat16 models, against the oracle's bfloat16 emulation)
+relative to the row's largest logit; the K/V the step writes for the tree
+rows must match to the same bound.  Shapes span several GEMM tiles, ragged K
+(ffn 688), ragged vocabularies (1000), ragged attention chunks, GQA, both
+head widths and 5..129-row trees.  Invariant (a) -- branch-masked rows equal
+each branch run alone -- is checked on the GPU path too.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import row_relerr, say
+from oracle import decoder
+from paper_2506_01979_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+_WEIGHTS = {}
+_MODELS = {}
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2506_01979_amd import api as A
+    assert torch.cuda.is_available()
+    return A
+
+
+def weights(shape):
+    if shape.name not in _WEIGHTS:
+        _WEIGHTS[shape.name] = synth.model_weights(shape)
+    return _WEIGHTS[shape.name]
+
+
+def model(api, shape):
+    if shape.name not in _MODELS:
+        _MODELS[shape.name] = api.Model(shape, api.dict_tensors(weights(shape)))
+    return _MODELS[shape.name]
+
+
+def tol(shape):
+    return 2e-2 if shape.dtype == "bf16" else 1e-4
+
+
+def mode(shape):
+    return "bf16" if shape.dtype == "bf16" else "f64"
+
+
+def gpu_forward(api, m, Kp, Vp, kv_len, tokens, parents, T=1.0, cap=None):
+    n = len(parents)
+    cap = cap or kv_len + n + 8
+    k, v = m.new_kv(cap)
+    if kv_len:
+        k[:, :, :kv_len] = torch.from_numpy(np.ascontiguousarray(Kp[:, :, :kv_len], np.float32)).to(m.wdtype)
+        v[:, :, :kv_len] = torch.from_numpy(np.ascontiguousarray(Vp[:, :, :kv_len], np.float32)).to(m.wdtype)
+    logits = torch.empty((n, m.shape.vocab), dtype=torch.float32, device="cuda")
+    stats = api.new_stats(n)
+    ws = m.workspace(n, kv_len)
+    toks = torch.from_numpy(np.asarray(tokens, np.int32)).cuda()
+    m.sb_verify_forward(k, v, kv_len, toks, parents, T, logits, stats, ws)
+    torch.cuda.synchronize()
+    return logits.cpu().numpy(), k, v
+
+
+CASES = [
+    # shape, prefix P, tree
+    ("tiny", 128, ("branch", 2, 4)),
+    ("exact", 8, ("branch", 3, 3)),
+    ("tiny", 40, ("chain", 30)),
+    ("small_bf16", 128, ("branch", 2, 4)),
+    ("small_bf16", 300, ("branch", 4, 8)),
+    ("small_gqa_bf16", 300, ("branch", 4, 8)),
+    ("small_h128_bf16", 200, ("branch", 8, 16)),
+    ("small_bf16", 1, ("chain", 40)),
+]
+
+
+def tree_of(spec):
+    if spec[0] == "branch":
+        return synth.branch_parents(spec[1], spec[2])
+    return synth.chain_parents(spec[1])
+
+
+@pytest.mark.parametrize("sname,P,spec", CASES, ids=[f"{c[0]}-P{c[1]}-{c[2]}" for c in CASES])
+def test_verify_forward_parity(api, sname, P, spec):
+    shape = synth.SHAPES[sname]
+    say(f"forward parity {sname} P={P} tree={spec}")
+    W = weights(shape)
+    parents = tree_of(spec)
+    n = len(parents)
+    ptoks = synth.prefix_tokens(shape.vocab, P)
+    kv_len = P - 1
+    if kv_len:
+        _, Kp, Vp = decoder.prefill(shape, W, ptoks[:-1], mode(shape))
+    else:
+        Kp = Vp = np.zeros((shape.n_layers, shape.n_kv_heads, 0, shape.head_dim))
+    g = np.random.default_rng(P + n)
+    toks = g.integers(0, shape.vocab, n).astype(np.int32)
+    toks[0] = ptoks[-1]
+    ref, kt, vt = decoder.tree_forward(shape, W, Kp, Vp, kv_len, toks, parents, mode(shape))
+    m = model(api, shape)
+    got, k, v = gpu_forward(api, m, Kp, Vp, kv_len, toks, parents)
+    err = row_relerr(got, ref)
+    say(f"  logits row-relative error {err:.3e}")
+    assert err < tol(shape)
+    kg = k[:, :, kv_len:kv_len + n].float().cpu().numpy()
+    vg = v[:, :, kv_len:kv_len + n].float().cpu().numpy()
+    assert row_relerr(kg.reshape(-1, shape.head_dim), kt.reshape(-1, shape.head_dim)) < tol(shape) * 5
+    assert row_relerr(vg.reshape(-1, shape.head_dim), vt.reshape(-1, shape.head_dim)) < tol(shape) * 5
+    # the prefix slots are untouched
+    if kv_len:
+        kp = k[:, :, :kv_len].float().cpu().numpy()
+        assert np.array_equal(kp, np.asarray(Kp[:, :, :kv_len], np.float32))
+
+
+@pytest.mark.parametrize("sname", ["tiny", "small_bf16", "small_gqa_bf16"])
+def test_branch_mask_gpu(api, sname):
+    """Invariant (a) on the HIP path: each branch's rows in the tree forward
+    equal a forward of [root, that branch] alone on the same prefix."""
+    shape = synth.SHAPES[sname]
+    say(f"branch mask {sname}")
+    W = weights(shape)
+    B, k = 3, 5
+    parents = synth.branch_parents(B, k)
+    P = 100
+    ptoks = synth.prefix_tokens(shape.vocab, P)
+    _, Kp, Vp = decoder.prefill(shape, W, ptoks[:-1], mode(shape))
+    g = np.random.default_rng(5)
+    toks = g.integers(0, shape.vocab, len(parents)).astype(np.int32)
+    toks[0] = ptoks[-1]
+    m = model(api, shape)
+    lt, _, _ = gpu_forward(api, m, Kp, Vp, P - 1, toks, parents)
+    for b in range(B):
+        rows = [0] + [1 + b * k + j for j in range(k)]
+        lc, _, _ = gpu_forward(api, m, Kp, Vp, P - 1, toks[rows], synth.chain_parents(len(rows)))
+        assert row_relerr(lt[rows], lc) < tol(shape) / 4
+
+
+@pytest.mark.parametrize("sname", ["tiny", "small_bf16"])
+def test_gpu_chunked_prefill(api, sname):
+    """A prefix built on the GPU by chained verify steps (chain trees of at
+    most 64 rows) matches the oracle's prefill."""
+    shape = synth.SHAPES[sname]
+    say(f"chunked prefill {sname}")
+    W = weights(shape)
+    P = 150
+    ptoks = synth.prefix_tokens(shape.vocab, P)
+    _, Kr, Vr = decoder.prefill(shape, W, ptoks, mode(shape))
+    m = model(api, shape)
+    k, v = m.new_kv(P + 8)
+    done = 0
+    while done < P:
+        n = min(64, P - done)
+        logits = torch.empty((n, shape.vocab), dtype=torch.float32, device="cuda")
+        stats = api.new_stats(n)
+        ws = m.workspace(n, done)
+        toks = torch.from_numpy(ptoks[done:done + n].astype(np.int32)).cuda()
+        m.sb_verify_forward(k, v, done, toks, synth.chain_parents(n), 1.0, logits, stats, ws)
+        done += n
+    torch.cuda.synchronize()
+    kg = k[:, :, :P].float().cpu().numpy()
+    vg = v[:, :, :P].float().cpu().numpy()
+    assert row_relerr(kg.reshape(-1, shape.head_dim), Kr.reshape(-1, shape.head_dim)) < tol(shape) * 5
+    assert row_relerr(vg.reshape(-1, shape.head_dim), Vr.reshape(-1, shape.head_dim)) < tol(shape) * 5
+
+
+def test_verify_forward_host_errors(api):
+    shape = synth.SHAPES["tiny"]
+    m = model(api, shape)
+    k, v = m.new_kv(20)
+    logits = torch.empty((4, shape.vocab), dtype=torch.float32, device="cuda")
+    stats = api.new_stats(4)
+    ws = m.workspace(4, 16)
+    toks = torch.zeros(4, dtype=torch.int32, device="cuda")
+    with pytest.raises(api.SBError) as e:
+        m.sb_verify_forward(k, v, 16, toks, [-1, 0, 1, 2], 1.0, logits, stats, ws[:10])
+    assert e.value.code == 3           # workspace too small
+    with pytest.raises(api.SBError) as e:
+        m.sb_verify_forward(k, v, 17, toks, [-1, 0, 1, 2], 1.0, logits, stats, ws)
+    assert e.value.code == 3           # kv_len + n_rows > capacity
+    with pytest.raises(api.SBError) as e:
+        m.sb_verify_forward(k, v, 4, toks, [-1, 0, 3, 1], 1.0, logits, stats, ws)
+    assert e.value.code == 2           # parent after child
