@@ -231,6 +231,31 @@ sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_le
                          const sb_step_result *d_result, int32_t *d_new_len,
                          hipStream_t stream);
 
+/* ---- measurement ---------------------------------------------------- */
+
+/* Kernel classes of the verify step, for sb_timer_start. */
+typedef enum {
+  SB_KC_QKV = 0,        /* QKV GEMM + RoPE + KV write */
+  SB_KC_O = 1,          /* O GEMM + residual */
+  SB_KC_GATE_UP = 2,    /* gate/up GEMM + SwiGLU */
+  SB_KC_DOWN = 3,       /* down GEMM + residual */
+  SB_KC_LM_HEAD = 4,    /* LM head GEMM */
+  SB_KC_ATTN = 5,       /* branch-masked attention */
+  SB_KC_ATTN_MERGE = 6, /* attention chunk merge */
+  SB_KC_NORM = 7,       /* RMSNorm */
+  SB_KC_STATS = 8       /* softmax statistics */
+} sb_kernel_class;
+
+/* Starts timing one kernel class of this model: every later launch of that
+ * class by sb_verify_forward is bracketed by a pair of HIP events recorded on
+ * the call's stream (at most `capacity` launches).  The events are created
+ * here (host runtime objects, no device memory). */
+sb_status sb_timer_start(sb_model *m, int32_t kernel_class, int32_t capacity);
+
+/* Waits for the recorded events, returns the summed kernel time in
+ * milliseconds and the number of timed launches, and releases the events. */
+sb_status sb_timer_stop(sb_model *m, double *total_ms, int32_t *launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -29,7 +29,10 @@ STATUS = {0: "SB_OK", 1: "SB_ERR_INVALID_ARG", 2: "SB_ERR_TREE", 3: "SB_ERR_CAPA
 EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight",
            "sb_model_create", "sb_model_destroy", "sb_workspace_bytes", "sb_verify_forward",
            "sb_softmax_stats", "sb_sample_workspace_bytes", "sb_select_branch",
-           "sb_accept_resample", "sb_kv_rollback")
+           "sb_accept_resample", "sb_kv_rollback", "sb_timer_start", "sb_timer_stop")
+
+KERNEL_CLASSES = {"qkv": 0, "o": 1, "gate_up": 2, "down": 3, "lm_head": 4, "attn": 5,
+                  "attn_merge": 6, "norm": 7, "stats": 8}
 
 
 class SBError(RuntimeError):
@@ -89,6 +92,10 @@ lib.sb_select_branch.argtypes = [_i32, _vp, _vp, _f, _i32, _vp, _vp, _vp, _vp, _
 lib.sb_accept_resample.restype = _i32
 lib.sb_accept_resample.argtypes = [_i32, _i32, _vp, C.POINTER(_i32), _vp, _vp, _f, _vp, _vp, _vp,
                                    _vp, _sz, _vp]
+lib.sb_timer_start.restype = _i32
+lib.sb_timer_start.argtypes = [_vp, _i32, _i32]
+lib.sb_timer_stop.restype = _i32
+lib.sb_timer_stop.argtypes = [_vp, C.POINTER(C.c_double), C.POINTER(_i32)]
 lib.sb_kv_rollback.restype = _i32
 lib.sb_kv_rollback.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, _vp, _vp]
 
@@ -342,6 +349,16 @@ class Model:
                                      len(par), temperature, logits.data_ptr(), stats.data_ptr(),
                                      ws.data_ptr(), ws.numel() * ws.element_size(),
                                      _stream(stream)), "sb_verify_forward")
+
+    def sb_timer_start(self, kernel_class: str, capacity: int) -> None:
+        _check(lib.sb_timer_start(self.handle, KERNEL_CLASSES[kernel_class], capacity),
+               "sb_timer_start")
+
+    def sb_timer_stop(self) -> tuple[float, int]:
+        ms = C.c_double()
+        n = C.c_int32()
+        _check(lib.sb_timer_stop(self.handle, C.byref(ms), C.byref(n)), "sb_timer_stop")
+        return ms.value, n.value
 
     def sb_kv_rollback(self, k: torch.Tensor, v: torch.Tensor, kv_len: int,
                        result: torch.Tensor, new_len: torch.Tensor, stream=None) -> None:

@@ -9,12 +9,20 @@
 
 #include "sb_internal_fwd.h"
 
+struct sb_timer {
+  int active = 0;
+  int kernel_class = -1;
+  int used = 0;
+  std::vector<hipEvent_t> start, stop;
+};
+
 struct sb_model {
   sb_model_config cfg;
   std::vector<sb_layer_weights> layers;
   const void *embed;
   const float *final_norm;
   const void *lm_head;
+  sb_timer timer;
 };
 
 namespace sb {
@@ -120,6 +128,30 @@ inline sb_status hip_status(hipError_t e) { return e == hipSuccess ? SB_OK : SB_
 
 size_t elem_bytes(const sb_model_config &c) { return c.dtype == SB_BF16 ? 2 : 4; }
 
+// Brackets one launch of kernel class kc with the model's timer events.
+struct TimedLaunch {
+  sb_timer &t;
+  hipStream_t s;
+  bool on;
+  TimedLaunch(sb_model *m, int kc, hipStream_t st)
+      : t(m->timer), s(st), on(m->timer.active && m->timer.kernel_class == kc &&
+                               m->timer.used < (int)m->timer.start.size()) {
+    if (on) hipEventRecord(t.start[t.used], s);
+  }
+  ~TimedLaunch() {
+    if (on) {
+      hipEventRecord(t.stop[t.used], s);
+      ++t.used;
+    }
+  }
+};
+
+#define SB_TIMED(kc, expr)          \
+  do {                              \
+    TimedLaunch _tl(m, (kc), s);    \
+    SB_TRY(expr);                   \
+  } while (0)
+
 sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int32_t *tokens,
                        const TreeArg &tree, int n, float temperature, float *logits,
                        sb_row_stats *stats, char *ws, const Layout &L, hipStream_t s) {
@@ -174,40 +206,40 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
     const sb_layer_weights &lw = m->layers[l];
     uint16_t *kc = (uint16_t *)kv->k + l * layer_kv;
     uint16_t *vc = (uint16_t *)kv->v + l * layer_kv;
-    SB_TRY(launch_rmsnorm_pack(h, lw.attn_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+    SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, lw.attn_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
     ga.W = (const uint16_t *)lw.qkv;
     ga.X = xa;
     ga.ks = gq.ks;
     ga.kc = kc;
     ga.vc = vc;
-    SB_TRY(launch_gemm(EPI_QKV, ga, gq.tiles, tt, s));
+    SB_TIMED(SB_KC_QKV, launch_gemm(EPI_QKV, ga, gq.tiles, tt, s));
     aa.kc = kc;
     aa.vc = vc;
-    SB_TRY(launch_attn_bf16(aa, s));
-    SB_TRY(launch_attn_merge_bf16(aa, xa, L.ks_o, s));
+    SB_TIMED(SB_KC_ATTN, launch_attn_bf16(aa, s));
+    SB_TIMED(SB_KC_ATTN_MERGE, launch_attn_merge_bf16(aa, xa, L.ks_o, s));
     ga.W = (const uint16_t *)lw.o;
     ga.X = xa;
     ga.ks = go.ks;
     ga.out_rows = H;
-    SB_TRY(launch_gemm(EPI_RESID, ga, go.tiles, tt, s));
-    SB_TRY(launch_rmsnorm_pack(h, lw.mlp_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+    SB_TIMED(SB_KC_O, launch_gemm(EPI_RESID, ga, go.tiles, tt, s));
+    SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, lw.mlp_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
     ga.W = (const uint16_t *)lw.gate_up;
     ga.X = xa;
     ga.ks = gg.ks;
-    SB_TRY(launch_gemm(EPI_SWIGLU, ga, gg.tiles, tt, s));
+    SB_TIMED(SB_KC_GATE_UP, launch_gemm(EPI_SWIGLU, ga, gg.tiles, tt, s));
     ga.W = (const uint16_t *)lw.down;
     ga.X = act;
     ga.ks = gd.ks;
     ga.out_rows = H;
-    SB_TRY(launch_gemm(EPI_RESID, ga, gd.tiles, tt, s));
+    SB_TIMED(SB_KC_DOWN, launch_gemm(EPI_RESID, ga, gd.tiles, tt, s));
   }
-  SB_TRY(launch_rmsnorm_pack(h, m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+  SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
   ga.W = (const uint16_t *)m->lm_head;
   ga.X = xa;
   ga.ks = gl.ks;
   ga.out_rows = c.vocab;
-  SB_TRY(launch_gemm(EPI_LOGITS, ga, gl.tiles, tt, s));
-  SB_TRY(launch_softmax_stats(c.vocab, n, logits, temperature, stats, s));
+  SB_TIMED(SB_KC_LM_HEAD, launch_gemm(EPI_LOGITS, ga, gl.tiles, tt, s));
+  SB_TIMED(SB_KC_STATS, launch_softmax_stats(c.vocab, n, logits, temperature, stats, s));
   return SB_OK;
 }
 
@@ -367,7 +399,62 @@ sb_status sb_model_create(const sb_model_config *cfg, const sb_model_weights *w,
   return SB_OK;
 }
 
-void sb_model_destroy(sb_model *m) { delete m; }
+static void timer_release(sb_timer &t) {
+  for (hipEvent_t e : t.start) hipEventDestroy(e);
+  for (hipEvent_t e : t.stop) hipEventDestroy(e);
+  t.start.clear();
+  t.stop.clear();
+  t.active = 0;
+  t.used = 0;
+}
+
+void sb_model_destroy(sb_model *m) {
+  if (!m) return;
+  timer_release(m->timer);
+  delete m;
+}
+
+sb_status sb_timer_start(sb_model *m, int32_t kernel_class, int32_t capacity) {
+  if (!m || kernel_class < SB_KC_QKV || kernel_class > SB_KC_STATS || capacity < 1 ||
+      capacity > (1 << 20))
+    return SB_ERR_INVALID_ARG;
+  timer_release(m->timer);
+  sb_timer &t = m->timer;
+  t.start.resize(capacity);
+  t.stop.resize(capacity);
+  for (int i = 0; i < capacity; ++i) {
+    if (hipEventCreate(&t.start[i]) != hipSuccess || hipEventCreate(&t.stop[i]) != hipSuccess) {
+      t.start.resize(i);
+      t.stop.resize(i);
+      timer_release(t);
+      return SB_ERR_HIP;
+    }
+  }
+  t.kernel_class = kernel_class;
+  t.used = 0;
+  t.active = 1;
+  return SB_OK;
+}
+
+sb_status sb_timer_stop(sb_model *m, double *total_ms, int32_t *launches) {
+  if (!m || !total_ms || !launches) return SB_ERR_INVALID_ARG;
+  sb_timer &t = m->timer;
+  double sum = 0.0;
+  sb_status st = SB_OK;
+  for (int i = 0; i < t.used; ++i) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(t.stop[i]) != hipSuccess ||
+        hipEventElapsedTime(&ms, t.start[i], t.stop[i]) != hipSuccess) {
+      st = SB_ERR_HIP;
+      break;
+    }
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = t.used;
+  timer_release(t);
+  return st;
+}
 
 size_t sb_workspace_bytes(const sb_model *m, int32_t max_rows, int32_t max_kv_len) {
   if (!m || max_rows < 1 || max_rows > SB_MAX_ROWS || max_kv_len < 0) return 0;
