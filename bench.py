@@ -195,7 +195,7 @@ def main():
         kb = synth.synthetic_kv(shape, l, kv_len, kv_len, 0, as_bits=True)
         vb = synth.synthetic_kv(shape, l, kv_len, kv_len, 1, as_bits=True)
         k_[l, :, :kv_len] = torch.from_numpy(kb.view(np.int16)).view(torch.bfloat16).to(dev)
-        v_[l, :, :kv_len] = torch.from_numpy(vb.view(np.int16)).view(torch.bfloat16).to(dev)
+        v_[l, :, :, :kv_len] = torch.from_numpy(vb.view(np.int16)).view(torch.bfloat16).to(dev).transpose(1, 2)
         if l < args.cpu_layers:
             kv_host[l] = (kb, vb)
     log(f"prefix KV ready ({kv_len} slots) at {time.time() - t0:.1f}s")

@@ -313,20 +313,45 @@ class Model:
 
     def _check_kv(self, k: torch.Tensor, v: torch.Tensor) -> None:
         s = self.shape
+        if k.dim() != 4 or tuple(k.shape[:2]) != (s.n_layers, s.n_kv_heads) \
+                or k.shape[3] != s.head_dim:
+            raise ValueError("k cache must be [n_layers][n_kv][capacity][head_dim]")
+        if v.dim() != 4 or tuple(v.shape) != (s.n_layers, s.n_kv_heads, s.head_dim, k.shape[2]):
+            raise ValueError("v cache must be [n_layers][n_kv][head_dim][capacity]")
+        if k.shape[2] % 8:
+            raise ValueError("cache capacity must be a multiple of 8")
         for t, nm in ((k, "k"), (v, "v")):
-            if t.dim() != 4 or tuple(t.shape[:2]) != (s.n_layers, s.n_kv_heads) \
-                    or t.shape[3] != s.head_dim:
-                raise ValueError(f"{nm} cache must be [n_layers][n_kv][capacity][head_dim]")
             _need(t, t.numel() * t.element_size(), nm, self.wdtype)
-        if k.shape != v.shape:
-            raise ValueError("k and v caches differ in shape")
 
     def new_kv(self, capacity: int):
+        """Zeroed caches: K [n_layers][n_kv][capacity][head_dim] and V stored
+        transposed, [n_layers][n_kv][head_dim][capacity] (capacity is rounded
+        up to a multiple of 8)."""
         s = self.shape
-        shp = (s.n_layers, s.n_kv_heads, capacity, s.head_dim)
-        k = torch.zeros(shp, dtype=self.wdtype, device=self.device)
-        v = torch.zeros(shp, dtype=self.wdtype, device=self.device)
+        capacity = (capacity + 7) // 8 * 8
+        k = torch.zeros((s.n_layers, s.n_kv_heads, capacity, s.head_dim), dtype=self.wdtype,
+                        device=self.device)
+        v = torch.zeros((s.n_layers, s.n_kv_heads, s.head_dim, capacity), dtype=self.wdtype,
+                        device=self.device)
         return k, v
+
+    def load_kv(self, k: torch.Tensor, v: torch.Tensor, K, V, n: int, start: int = 0) -> None:
+        """Writes host K/V rows given as [n_layers][n_kv][n][head_dim] (float32
+        values or bf16 bit patterns) into slots start..start+n-1."""
+        def dev(a):
+            a = np.ascontiguousarray(a)
+            if a.dtype == np.uint16:
+                return torch.from_numpy(a.view(np.int16)).to(self.device).view(torch.bfloat16)
+            return torch.from_numpy(np.asarray(a, np.float32)).to(self.device).to(self.wdtype)
+        k[:, :, start:start + n] = dev(np.asarray(K)[:, :, :n])
+        v[:, :, :, start:start + n] = dev(np.asarray(V)[:, :, :n]).transpose(2, 3)
+
+    @staticmethod
+    def read_kv(k: torch.Tensor, v: torch.Tensor, start: int, n: int):
+        """Slots start..start+n-1 as float32 arrays [n_layers][n_kv][n][head_dim]."""
+        K = k[:, :, start:start + n].float().cpu().numpy()
+        V = v[:, :, :, start:start + n].float().transpose(2, 3).cpu().numpy()
+        return K, V
 
     def workspace(self, max_rows: int, max_kv_len: int) -> torch.Tensor:
         n = int(lib.sb_workspace_bytes(self.handle, max_rows, max_kv_len))

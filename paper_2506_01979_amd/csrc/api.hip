@@ -30,6 +30,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kF32MaxKeys = 15360;  // scores of one row in 60 KB of LDS
+constexpr int kBf16MaxKeys = 512 * kAttnChunk;  // chunks one merge workgroup combines
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -97,6 +98,7 @@ bool config_ok(const sb_model_config *c) {
 sb_status shape_supported(const sb_model_config *c) {
   if (c->dtype == SB_BF16) {
     if (c->head_dim != 64 && c->head_dim != 128) return SB_ERR_UNSUPPORTED;
+    if (c->hidden % 8 != 0 || c->hidden > 16384) return SB_ERR_UNSUPPORTED;
   } else {
     if (c->head_dim > 256) return SB_ERR_UNSUPPORTED;
   }
@@ -127,6 +129,27 @@ inline sb_status hip_status(hipError_t e) { return e == hipSuccess ? SB_OK : SB_
   } while (0)
 
 size_t elem_bytes(const sb_model_config &c) { return c.dtype == SB_BF16 ? 2 : 4; }
+
+// Embedding / metadata arguments, with the RoPE frequencies theta_j =
+// base^(-2j/d) evaluated once on the host in float64.
+EmbedArgs embed_args(const sb_model *m, const int32_t *tokens, float *h, int n, int kv_len,
+                     Meta *meta, float2 *rope) {
+  const sb_model_config &c = m->cfg;
+  EmbedArgs ea{};
+  ea.tokens = tokens;
+  ea.embed = m->embed;
+  ea.h = h;
+  ea.vocab = c.vocab;
+  ea.hidden = c.hidden;
+  ea.n_tok = n;
+  ea.kv_len = kv_len;
+  ea.meta = meta;
+  ea.rope = rope;
+  ea.head_dim = c.head_dim;
+  for (int j = 0; j < c.head_dim / 2 && j < 128; ++j)
+    ea.theta[j] = pow((double)c.rope_theta, -2.0 * (double)j / (double)c.head_dim);
+  return ea;
+}
 
 // Brackets one launch of kernel class kc with the model's timer events.
 struct TimedLaunch {
@@ -165,7 +188,7 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   uint16_t *act = (uint16_t *)(ws + L.act);
   uint16_t *q = (uint16_t *)(ws + L.q);
 
-  EmbedArgs ea{tokens, m->embed, h, c.vocab, H, n, kv_len, meta, rope, d, c.rope_theta};
+  EmbedArgs ea = embed_args(m, tokens, h, n, kv_len, meta, rope);
   SB_TRY(launch_embed_meta(ea, tree, L.np, 1, s));
 
   const PackGeom gq = pack_geom(c, SB_W_QKV), go = pack_geom(c, SB_W_O),
@@ -259,7 +282,7 @@ sb_status forward_f32(sb_model *m, const sb_kv_cache *kv, int kv_len, const int3
   float *gu = (float *)(ws + L.gu);
   float *act = (float *)(ws + L.fact);
 
-  EmbedArgs ea{tokens, m->embed, h, c.vocab, H, n, kv_len, meta, rope, d, c.rope_theta};
+  EmbedArgs ea = embed_args(m, tokens, h, n, kv_len, meta, rope);
   SB_TRY(launch_embed_meta(ea, tree, n, 0, s));
   const size_t layer_kv = (size_t)c.n_kv_heads * kv->capacity * d;
 
@@ -471,7 +494,8 @@ sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
   TreeArg tree;
   sb_status st = check_tree(h_parents, n_rows, &tree);
   if (st != SB_OK) return st;
-  if ((int64_t)kv_len + n_rows > kv->capacity) return SB_ERR_CAPACITY;
+  if ((int64_t)kv_len + n_rows > kv->capacity || kv->capacity % 8 != 0) return SB_ERR_CAPACITY;
+  if (m->cfg.dtype == SB_BF16 && (int64_t)kv_len + n_rows > kBf16MaxKeys) return SB_ERR_UNSUPPORTED;
   if (m->cfg.dtype == SB_F32 && kv_len + n_rows > kF32MaxKeys) return SB_ERR_UNSUPPORTED;
   const Layout L = make_layout(m->cfg, n_rows, kv_len);
   if (ws_bytes < L.total) return SB_ERR_CAPACITY;
@@ -528,10 +552,11 @@ sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_le
                          hipStream_t stream) {
   if (!m || !kv || !kv->k || !kv->v || !d_result || !d_new_len) return SB_ERR_INVALID_ARG;
   if (kv_len < 0 || kv_len >= kv->capacity) return SB_ERR_CAPACITY;
+  if (kv->capacity % 8 != 0) return SB_ERR_CAPACITY;
   const sb_model_config &c = m->cfg;
-  const int row_bytes = c.head_dim * (int)elem_bytes(c);
-  return hip_status(launch_rollback(c.n_layers, c.n_kv_heads, kv->capacity, row_bytes, kv->k,
-                                    kv->v, kv_len, d_result, d_new_len, stream));
+  return hip_status(launch_rollback(c.n_layers, c.n_kv_heads, kv->capacity, c.head_dim,
+                                    (int)elem_bytes(c), kv->k, kv->v, kv_len, d_result, d_new_len,
+                                    stream));
 }
 
 }  // extern "C"

@@ -7,12 +7,16 @@
 // causal forward of that branch would see (Section "Branch Resampling").
 //
 // Work split: one workgroup per (KV head, chunk of 128 key slots) over the
-// combined key range [0, kv_len + n_tok).  The chunk's V is staged in LDS
-// once (transposed for the P.V operand) and its K is read once per
-// 64-query-row block, so a prefix tile is fetched from HBM once and reused by
-// every branch and every query head of the KV group (GQA).  The workgroup
-// writes an unnormalised partial (row max m, row sum l, sum p v) per query
-// row; a merge kernel combines the chunks with the usual log-sum-exp rule.
+// combined key range [0, kv_len + n_tok).  The V cache is stored transposed
+// ([d][slot]), so both matrix-core operands that come from the cache -- K
+// rows for S^T = K Q^T and V^T rows for O^T = V^T P^T -- are 16-byte runs of
+// consecutive elements read straight from HBM.  Every cache load of the
+// chunk is issued before the first wait, so a workgroup pays one memory
+// latency; a prefix tile is fetched once and reused by every branch and
+// every query head of the KV group (GQA).  Queries and probabilities go
+// through LDS.  The workgroup writes an unnormalised partial (row max m, row
+// sum l, sum p v) per query row; the merge kernel combines the chunks with
+// the log-sum-exp rule.
 #include <math.h>
 
 #include "sb_device.h"
@@ -23,15 +27,35 @@ namespace {
 
 constexpr int CH = kAttnChunk;  // keys per workgroup
 constexpr int RB = 64;          // query rows per block (4 row tiles)
-constexpr int VPAD = 8;         // LDS row padding (bf16 elements)
+constexpr int PAD = 8;          // LDS row padding (bf16 elements)
+
+// 8 consecutive bf16 of a V^T row starting at slot `key`; slots >= nkeys
+// (never written for this step) read as zero, and nothing past the cache
+// capacity is touched.
+__device__ __forceinline__ uint4 load_vt8(const uint16_t *row, int key, int nkeys, int cap) {
+  if (key + 8 <= nkeys) return *(const uint4 *)(row + key);
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (key < nkeys && key + 8 <= cap) {
+    v = *(const uint4 *)(row + key);
+    const int keep = nkeys - key;  // 1..7 valid elements
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (e >= keep) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+    v = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  return v;
+}
 
 template <int D>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  constexpr int KSD = D / 32;           // k-steps over head_dim
-  constexpr int DT = D / 16;            // d tiles
-  constexpr int DTW = DT / 4;           // d tiles per wave (4 waves)
-  __shared__ uint16_t Vt[D][CH + VPAD];  // V chunk, transposed
-  __shared__ uint16_t P[RB][CH + VPAD];  // probabilities (bf16)
+  constexpr int KSD = D / 32;    // k-steps over head_dim
+  constexpr int DT = D / 16;     // d tiles
+  constexpr int DTW = DT / 4;    // d tiles per wave (4 waves)
+  constexpr int VV = D / 8;      // 16-byte vectors per query row
+  constexpr int KK = CH / 32;    // k-steps over the chunk's keys
+  __shared__ uint16_t P[RB][CH + PAD];  // probabilities (bf16), row-major
+  __shared__ uint16_t Qs[RB][D + PAD];  // query rows of this block
   __shared__ float redm[4][RB];
   __shared__ float redl[4][RB];
 
@@ -43,26 +67,40 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int key0 = c * CH;
   const int nkeys = a.kv_len + a.n_tok;
   const uint16_t *__restrict__ kc = (const uint16_t *)a.kc + (size_t)g * a.cap * D;
-  const uint16_t *__restrict__ vc = (const uint16_t *)a.vc + (size_t)g * a.cap * D;
+  const uint16_t *__restrict__ vt = (const uint16_t *)a.vc + (size_t)g * D * a.cap;
   const uint16_t *__restrict__ q = (const uint16_t *)a.q;
 
-  // stage V^T for this chunk
-  for (int idx = threadIdx.x; idx < CH * (D / 8); idx += 256) {
-    const int key = idx / (D / 8);
-    const int dv = (idx % (D / 8)) * 8;
-    const int slot = key0 + key;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (slot < nkeys) v = *(const uint4 *)(vc + (size_t)slot * D + dv);
-    const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+  // ---- every cache load of the chunk, issued up front
+  uint4 ka[2][KSD];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      Vt[dv + 2 * e][key] = (uint16_t)(wv[e] & 0xffff);
-      Vt[dv + 2 * e + 1][key] = (uint16_t)(wv[e] >> 16);
-    }
+  for (int i = 0; i < 2; ++i) {
+    const int slot = key0 + (2 * w + i) * 16 + lr;
+#pragma unroll
+    for (int s = 0; s < KSD; ++s)
+      ka[i][s] = slot < nkeys ? *(const uint4 *)(kc + (size_t)slot * D + 32 * s + 8 * lg)
+                              : make_uint4(0, 0, 0, 0);
+  }
+  uint4 va[DTW][KK];
+#pragma unroll
+  for (int i = 0; i < DTW; ++i) {
+    const uint16_t *row = vt + (size_t)((w * DTW + i) * 16 + lr) * a.cap;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) va[i][kk] = load_vt8(row, key0 + kk * 32 + 8 * lg, nkeys, a.cap);
   }
 
   for (int r0 = 0; r0 < R; r0 += RB) {
-    __syncthreads();  // Vt ready / P free
+    // stage the query rows of this block
+    for (int idx = threadIdx.x; idx < RB * VV; idx += 256) {
+      const int rr = idx / VV, dv = (idx % VV) * 8;
+      const int r = r0 + rr;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (r < R) {
+        const int t = r / G, hl = r - t * G;
+        v = *(const uint4 *)(q + ((size_t)t * a.n_heads + g * G + hl) * D + dv);
+      }
+      *(uint4 *)&Qs[rr][dv] = v;
+    }
+    __syncthreads();
     // ---- S^T = K Q^T for this wave's 2 key tiles x 4 row tiles
     f32x4 sacc[2][4];
 #pragma unroll
@@ -71,30 +109,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       for (int rt = 0; rt < 4; ++rt) sacc[i][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < KSD; ++s) {
-      uint4 ka[2], qb[4];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int slot = key0 + (2 * w + i) * 16 + lr;
-        ka[i] = slot < nkeys ? *(const uint4 *)(kc + (size_t)slot * D + 32 * s + 8 * lg)
-                             : make_uint4(0, 0, 0, 0);
-      }
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) {
-        const int r = r0 + rt * 16 + lr;
-        if (r < R) {
-          const int t = r / G, hl = r - t * G;
-          qb[rt] = *(const uint4 *)(q + ((size_t)t * a.n_heads + g * G + hl) * D + 32 * s + 8 * lg);
-        } else {
-          qb[rt] = make_uint4(0, 0, 0, 0);
-        }
+        const uint4 qb = *(const uint4 *)&Qs[rt * 16 + lr][32 * s + 8 * lg];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          sacc[i][rt] = mfma16(as_bf16x8(ka[i][s]), as_bf16x8(qb), sacc[i][rt]);
       }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int rt = 0; rt < 4; ++rt) sacc[i][rt] = mfma16(as_bf16x8(ka[i]), as_bf16x8(qb[rt]), sacc[i][rt]);
     }
     // ---- scale, mask, row max over this wave's 32 keys
-    float mrow[4];
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
       const int r = r0 + rt * 16 + lr;
@@ -117,7 +140,6 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       }
       m = fmaxf(m, __shfl_xor(m, 16, 64));
       m = fmaxf(m, __shfl_xor(m, 32, 64));
-      mrow[rt] = m;
       if (lg == 0) redm[w][rt * 16 + lr] = m;
     }
     __syncthreads();
@@ -125,7 +147,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
       const int rr = rt * 16 + lr;
-      float m = fmaxf(fmaxf(redm[0][rr], redm[1][rr]), fmaxf(redm[2][rr], redm[3][rr]));
+      const float m = fmaxf(fmaxf(redm[0][rr], redm[1][rr]), fmaxf(redm[2][rr], redm[3][rr]));
       const float mref = (m == -INFINITY) ? 0.0f : m;
       float l = 0.0f;
 #pragma unroll
@@ -145,12 +167,11 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       l += __shfl_xor(l, 16, 64);
       l += __shfl_xor(l, 32, 64);
       lsum[rt] = l;
-      mrow[rt] = m;
     }
-    __syncthreads();  // all of P written, redm read
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt)
       if (lg == 0) redl[w][rt * 16 + lr] = lsum[rt];
+    __syncthreads();  // P and redl complete
     // ---- O^T = V^T P^T for this wave's d tiles
     f32x4 oacc[DTW][4];
 #pragma unroll
@@ -158,16 +179,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) oacc[i][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kk = 0; kk < CH / 32; ++kk) {
-      uint4 va[DTW], pbv[4];
-#pragma unroll
-      for (int i = 0; i < DTW; ++i) va[i] = *(const uint4 *)&Vt[(w * DTW + i) * 16 + lr][kk * 32 + 8 * lg];
+    for (int kk = 0; kk < KK; ++kk) {
+      uint4 pbv[4];
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) pbv[rt] = *(const uint4 *)&P[rt * 16 + lr][kk * 32 + 8 * lg];
 #pragma unroll
       for (int i = 0; i < DTW; ++i)
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) oacc[i][rt] = mfma16(as_bf16x8(va[i]), as_bf16x8(pbv[rt]), oacc[i][rt]);
+        for (int rt = 0; rt < 4; ++rt)
+          oacc[i][rt] = mfma16(as_bf16x8(va[i][kk]), as_bf16x8(pbv[rt]), oacc[i][rt]);
     }
     const size_t base = ((size_t)g * a.n_chunks + c) * R;
 #pragma unroll
@@ -181,43 +201,97 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         }
       }
     }
-    __syncthreads();  // redl written
     if (threadIdx.x < RB) {
       const int rr = threadIdx.x;
       const int r = r0 + rr;
       if (r < R) {
         const float m = fmaxf(fmaxf(redm[0][rr], redm[1][rr]), fmaxf(redm[2][rr], redm[3][rr]));
         const float l = redl[0][rr] + redl[1][rr] + redl[2][rr] + redl[3][rr];
-        a.part_ml[(base + r) * 2 + 0] = m;
-        a.part_ml[(base + r) * 2 + 1] = l;
+        *(float2 *)&a.part_ml[(base + r) * 2] = make_float2(m, l);
       }
     }
+    __syncthreads();  // Qs, P, redm, redl free for the next row block
   }
 }
 
-// Combines the chunks of one (row, head) and writes the attention output in
-// the packed operand layout of the O projection.
+// Combines the chunks of one (row t, query head) and writes the attention
+// output in the packed operand layout of the O projection.  The 256 threads
+// form 4 chunk groups x 64 column lanes: the chunk weights exp(m_c - M) are
+// computed once into LDS, each group sums its chunks with independent loads,
+// and the groups are added in LDS.
 template <int D>
-__global__ __launch_bounds__(D) void k_attn_merge(AttnArgs a, uint16_t *__restrict__ out, int ks) {
+__global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, uint16_t *__restrict__ out, int ks) {
+  constexpr int DPT = D / 64;  // columns per lane
+  constexpr int MAXC = 512;
+  __shared__ float sw[MAXC];
+  __shared__ float red[8];
+  __shared__ float acc[4][D];
   const int t = blockIdx.x, head = blockIdx.y;
   const int G = a.n_heads / a.n_kv;
   const int g = head / G;
   const int R = a.n_tok * G;
   const int r = t * G + (head - g * G);
-  const int dd = threadIdx.x;
-  float M = -INFINITY;
-  for (int c = 0; c < a.n_chunks; ++c)
-    M = fmaxf(M, a.part_ml[(((size_t)g * a.n_chunks + c) * R + r) * 2]);
-  float L = 0.0f, o = 0.0f;
-  for (int c = 0; c < a.n_chunks; ++c) {
-    const size_t b = ((size_t)g * a.n_chunks + c) * R + r;
-    const float m = a.part_ml[b * 2];
-    if (m == -INFINITY) continue;
-    const float wgt = expf(m - M);
-    L += a.part_ml[b * 2 + 1] * wgt;
-    o += a.part_o[b * D + dd] * wgt;
+  const int nc = a.n_chunks;
+  const float2 *ml = (const float2 *)a.part_ml + (size_t)g * nc * R + r;
+  float m = -INFINITY;
+  for (int cc = threadIdx.x; cc < nc; cc += 256) {
+    const float mv = ml[(size_t)cc * R].x;
+    sw[cc] = mv;
+    m = fmaxf(m, mv);
   }
-  out[packed_index(t, head * D + dd, ks)] = f2bf(o / L);
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float l = 0.0f;
+  for (int cc = threadIdx.x; cc < nc; cc += 256) {
+    const float mv = sw[cc];
+    const float wgt = mv == -INFINITY ? 0.0f : expf(mv - M);
+    sw[cc] = wgt;
+    l += wgt * ml[(size_t)cc * R].y;
+  }
+  for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
+  if ((threadIdx.x & 63) == 0) red[4 + (threadIdx.x >> 6)] = l;
+  __syncthreads();
+  const float L = red[4] + red[5] + red[6] + red[7];
+  const int cg = threadIdx.x >> 6, lt = threadIdx.x & 63;
+  float o[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) o[e] = 0.0f;
+  const float *po = a.part_o + ((size_t)g * nc * R + r) * D + lt * DPT;
+  const size_t cstride = (size_t)R * D;
+  int cc = cg;
+  for (; cc + 12 < nc; cc += 16) {  // four chunks of this group per batch
+    float v[4][DPT];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) v[j][e] = po[(size_t)(cc + 4 * j) * cstride + e];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) o[e] += sw[cc + 4 * j] * v[j][e];
+  }
+  for (; cc < nc; cc += 4)
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) o[e] += sw[cc] * po[(size_t)cc * cstride + e];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) acc[cg][lt * DPT + e] = o[e];
+  __syncthreads();
+  if (threadIdx.x < D / 8) {
+    const int d0 = threadIdx.x * 8;
+    const float inv = 1.0f / L;
+    uint16_t b[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      b[e] = f2bf((acc[0][d0 + e] + acc[1][d0 + e] + acc[2][d0 + e] + acc[3][d0 + e]) * inv);
+    uint4 pk;
+    pk.x = b[0] | ((uint32_t)b[1] << 16);
+    pk.y = b[2] | ((uint32_t)b[3] << 16);
+    pk.z = b[4] | ((uint32_t)b[5] << 16);
+    pk.w = b[6] | ((uint32_t)b[7] << 16);
+    *(uint4 *)(out + packed_index(t, head * D + d0, ks)) = pk;
+  }
 }
 
 }  // namespace
@@ -235,11 +309,12 @@ hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s) {
 
 hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,
                                   hipStream_t s) {
+  if (a.n_chunks > 512) return hipErrorInvalidValue;
   dim3 grid(a.n_tok, a.n_heads);
   if (a.head_dim == 128)
-    hipLaunchKernelGGL(k_attn_merge<128>, grid, dim3(128), 0, s, a, out_packed, out_ks);
+    hipLaunchKernelGGL(k_attn_merge<128>, grid, dim3(256), 0, s, a, out_packed, out_ks);
   else if (a.head_dim == 64)
-    hipLaunchKernelGGL(k_attn_merge<64>, grid, dim3(64), 0, s, a, out_packed, out_ks);
+    hipLaunchKernelGGL(k_attn_merge<64>, grid, dim3(256), 0, s, a, out_packed, out_ks);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

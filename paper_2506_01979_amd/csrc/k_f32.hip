@@ -75,7 +75,7 @@ __global__ __launch_bounds__(128) void k_f32_rope_qkv(const float *__restrict__ 
       dst[j + half] = o2;
     } else {
       const int g = hh - n_heads - n_kv;
-      vc[((size_t)g * cap + kv_len + t) * d + j] = row[j];
+      vc[((size_t)g * d + j) * cap + kv_len + t] = row[j];  // V cached transposed
     }
   }
 }
@@ -92,7 +92,7 @@ __global__ __launch_bounds__(256) void k_f32_attn(AttnArgs a, float *__restrict_
   const int nkeys = a.kv_len + a.n_tok;
   const float *qr = (const float *)a.q + ((size_t)t * a.n_heads + head) * d;
   const float *kc = (const float *)a.kc + (size_t)g * a.cap * d;
-  const float *vc = (const float *)a.vc + (size_t)g * a.cap * d;
+  const float *vt = (const float *)a.vc + (size_t)g * d * a.cap;  // [d][slot]
   float m = -INFINITY;
   for (int j = threadIdx.x; j < nkeys; j += 256) {
     bool ok = j < a.kv_len;
@@ -126,7 +126,8 @@ __global__ __launch_bounds__(256) void k_f32_attn(AttnArgs a, float *__restrict_
   l = red[4] + red[5] + red[6] + red[7];
   for (int dd = threadIdx.x; dd < d; dd += 256) {
     float o = 0.0f;
-    for (int j = 0; j < nkeys; ++j) o += sc[j] * vc[(size_t)j * d + dd];
+    const float *vrow = vt + (size_t)dd * a.cap;
+    for (int j = 0; j < nkeys; ++j) o += sc[j] * vrow[j];
     out[(size_t)t * a.n_heads * d + (size_t)head * d + dd] = o / l;
   }
 }

@@ -9,7 +9,8 @@
 //   reject : p~ <- max(0, p~ - q) / Z,  Z = sum max(0, p~ - q)   (float64),
 //            Z <= 0 keeps p~ and raises SB_FLAG_ZERO_RESIDUAL;
 //   draw   : C_v = running float64 sum of p~ in vocabulary order,
-//            y = min{v : C_v > u * C_last}; a zero-mass token is never drawn.
+//            y = min{v : C_v > u * W}, W the float64 total; a zero-mass
+//            token is never drawn.
 // The multiply-then-subtract of the logit transform must not be contracted
 // into an FMA: every operation rounds on its own, as the definition states.
 #pragma clang fp contract(off)
@@ -94,39 +95,9 @@ __device__ int block_max(int v, int *red) {
   return r;
 }
 
-// Exclusive prefix sum over the block (one value per thread).  Each prefix
-// is a sum of earlier values only (no subtraction of the own value).
-template <int NW>
-__device__ double block_exclusive_scan(double v, double *red) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  double inc = v;
-  for (int o = 1; o < 64; o <<= 1) {
-    double t = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += t;
-  }
-  double exc = __shfl_up(inc, 1, 64);
-  if (lane == 0) exc = 0.0;
-  if (lane == 63) red[w] = inc;
-  __syncthreads();
-  if (w == 0) {
-    double t = lane < NW ? red[lane] : 0.0;
-    double ti = t;
-    for (int o = 1; o < 64; o <<= 1) {
-      double s = __shfl_up(ti, o, 64);
-      if (lane >= o) ti += s;
-    }
-    double te = __shfl_up(ti, 1, 64);
-    if (lane == 0) te = 0.0;
-    if (lane < NW) red[lane] = te;  // each lane rewrites only its own entry
-  }
-  __syncthreads();
-  double r = (w == 0) ? exc : red[w] + exc;
-  __syncthreads();
-  return r;
-}
-
-// A target distribution p~: either a logits row with its statistics, or an
-// explicit float64 array in the workspace (after a rejection).
+// A target distribution p~: either a logits row with its statistics, or a
+// residual r in the workspace with its mass Z (p~(v) = r_v / Z, the
+// normalisation done element by element as it is read).
 struct Dist {
   const float *l;
   float inv_t;
@@ -134,10 +105,11 @@ struct Dist {
   double total;
   int argmax;
   int greedy;
-  const double *arr;  // non-null: explicit array
+  const double *arr;  // non-null: residual array
+  double zdiv;
 
   __device__ __forceinline__ double at(int v) const {
-    if (arr) return arr[v];
+    if (arr) return arr[v] / zdiv;
     if (greedy) return v == argmax ? 1.0 : 0.0;
     float z = l[v] * inv_t;
     float e = expf(z - zmax);
@@ -155,6 +127,7 @@ __device__ __forceinline__ Dist row_dist(const float *l, const sb_row_stats &st,
   d.argmax = st.argmax;
   d.greedy = greedy;
   d.arr = nullptr;
+  d.zdiv = 1.0;
   return d;
 }
 
@@ -165,53 +138,101 @@ struct Shared {
   double z;
 };
 
-// After candidate with draft row q is rejected: p~ <- max(0, p~ - q)/Z.
-// Writes the new array to dst; returns Z (all threads).
+// Elements of a vocabulary pass handled per thread per batch: their loads are
+// issued together so a batch costs one memory latency.
+constexpr int kBatch = 8;
+
+// After candidate with draft row q is rejected: r = max(0, p~ - q) into
+// dst; returns Z = sum r (all threads).  The new p~ is r / Z.
 __device__ double residual_pass(const Dist &cur, const float *q, int vocab, double *dst,
                                 Shared &sh) {
   double part = 0.0;
-  for (int v = threadIdx.x; v < vocab; v += kWalkThreads) {
-    double r = cur.at(v) - (double)q[v];
-    r = r > 0.0 ? r : 0.0;
-    dst[v] = r;
-    part += r;
+  for (int v0 = threadIdx.x; v0 < vocab; v0 += kBatch * kWalkThreads) {
+    float qv[kBatch];
+    double pv[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int v = v0 + j * kWalkThreads;
+      qv[j] = v < vocab ? q[v] : 0.0f;
+      pv[j] = v < vocab ? cur.at(v) : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int v = v0 + j * kWalkThreads;
+      double r = pv[j] - (double)qv[j];
+      r = r > 0.0 ? r : 0.0;
+      if (v < vocab) {
+        dst[v] = r;
+        part += r;
+      }
+    }
   }
-  double Z = block_sum<kWaves>(part, sh.red);
-  if (Z > 0.0) {
-    for (int v = threadIdx.x; v < vocab; v += kWalkThreads) dst[v] = dst[v] / Z;
-  }
-  __syncthreads();
-  return Z;
+  return block_sum<kWaves>(part, sh.red);
 }
 
 // Inverse-CDF draw from p~ with uniform u (all threads return the token).
+// Each wave owns a contiguous segment of the vocabulary: pass 1 sums the
+// segments, pass 2 rescans its segment 64 elements at a time (a lane-parallel
+// inclusive scan on top of the running prefix) and stops at the first
+// C_v > u * W.  Both passes read kBatch blocks of 64 per batch.
 __device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
-  const int chunk = (vocab + kWalkThreads - 1) / kWalkThreads;
-  const int lo = threadIdx.x * chunk;
-  const int hi = min(vocab, lo + chunk);
-  double s = 0.0;
-  for (int v = lo; v < hi; ++v) s += d.at(v);
-  double e = block_exclusive_scan<kWaves>(s, sh.red);
-  // the thread owning the last element publishes C_last = e + s
-  const int last_owner = (vocab - 1) / chunk;
-  if ((int)threadIdx.x == last_owner) sh.z = e + s;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int seg = ((vocab + kWaves - 1) / kWaves + 63) & ~63;
+  const int lo = w * seg;
+  const int hi = min(vocab, lo + seg);
+  double part = 0.0;
+  for (int v0 = lo + lane; v0 < hi; v0 += 64 * kBatch) {
+    double x[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) x[j] = (v0 + 64 * j < hi) ? d.at(v0 + 64 * j) : 0.0;
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) part += x[j];
+  }
+  part = wave_sum(part);
+  if (lane == 0) sh.red[w] = part;
   __syncthreads();
-  const double W = sh.z;
+  if (threadIdx.x == 0) {
+    double run = 0.0;
+    for (int i = 0; i < kWaves; ++i) {
+      const double t = sh.red[i];
+      sh.red[i] = run;  // exclusive prefix of wave i
+      run += t;
+    }
+    sh.red[kWaves] = run;  // W
+  }
+  __syncthreads();
+  const double base = sh.red[w];
+  const double W = sh.red[kWaves];
   const double thr = (double)u * W;
   int cand = INT_MAX;
-  double run = 0.0;
-  for (int v = lo; v < hi; ++v) {
-    run += d.at(v);
-    if (e + run > thr) {
-      cand = v;
-      break;
+  double run = base;
+  for (int v0 = lo; v0 < hi && cand == INT_MAX; v0 += 64 * kBatch) {
+    double x[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int v = v0 + 64 * j + lane;
+      x[j] = v < hi ? d.at(v) : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (cand != INT_MAX) break;
+      const int v = v0 + 64 * j + lane;
+      double inc = x[j];
+      for (int o = 1; o < 64; o <<= 1) {
+        const double y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+      }
+      const double C = run + inc;
+      const unsigned long long hit = __ballot(v < hi && C > thr);
+      if (hit) cand = v0 + 64 * j + __ffsll((long long)hit) - 1;
+      run += __shfl(inc, 63, 64);
     }
   }
   int y = block_min<kWaves>(cand, sh.ired);
   if (y == INT_MAX) {
     // rounding left no crossing: the last token with positive mass
     int lp = -1;
-    for (int v = lo; v < hi; ++v)
+    for (int v = threadIdx.x; v < vocab; v += kWalkThreads)
       if (d.at(v) > 0.0) lp = v;
     y = block_max<kWaves>(lp, sh.ired);
     if (y < 0) y = vocab - 1;
@@ -247,6 +268,7 @@ __device__ int node_select(Dist *cur, const Cand &cand, int n_cand, int vocab, d
     double Z = residual_pass(*cur, cand.q(i), vocab, dst, sh);
     if (Z > 0.0) {
       cur->arr = dst;
+      cur->zdiv = Z;
     } else if (threadIdx.x == 0) {
       *flags |= SB_FLAG_ZERO_RESIDUAL;
     }
@@ -277,35 +299,58 @@ struct ChildCands {
 
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(512) void k_softmax_stats(const float *__restrict__ logits, int vocab,
-                                                      float inv_t, int greedy,
-                                                      sb_row_stats *__restrict__ out) {
-  constexpr int NT = 512, NW = NT / 64;
-  __shared__ float smax[NW];
+// One workgroup per row.  Pass 1: max of l (lowest-index argmax), max of
+// z = fl32(l / T) and a NaN/+inf scan; pass 2: float64 sum of
+// fl32(exp(z - zmax)).  Loads are 16-byte and independent across a thread's
+// items so a pass costs about one memory latency.
+__global__ __launch_bounds__(1024) void k_softmax_stats(const float *__restrict__ logits,
+                                                        int vocab, float inv_t, int greedy,
+                                                        sb_row_stats *__restrict__ out) {
+  constexpr int NT = 1024, NW = NT / 64;
+  __shared__ float smax[NW], szmax[NW];
   __shared__ int sarg[NW];
   __shared__ int sbad[NW];
-  __shared__ double red[NW + 1];
+  __shared__ double red[NW];
   const float *l = logits + (size_t)blockIdx.x * vocab;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  // pass 1: max of l (argmax, lowest index) and max of z = fl32(l / T)
+  const bool vec = (vocab & 3) == 0;
   float best = -INFINITY;
   int barg = INT_MAX;
   float zbest = -INFINITY;
   int bad = 0;
-  for (int v = threadIdx.x; v < vocab; v += NT) {
-    const float x = l[v];
+  auto visit = [&](float x, int v) {
     if (isnan(x) || x == INFINITY) bad = 1;
     if (x > best) {
       best = x;
       barg = v;
     }
-    const float z = x * inv_t;
-    zbest = fmaxf(zbest, z);
+    zbest = fmaxf(zbest, x * inv_t);
+  };
+  if (vec) {
+    const float4 *l4 = (const float4 *)l;
+    const int n4 = vocab >> 2;
+    for (int i0 = threadIdx.x; i0 < n4; i0 += 4 * NT) {
+      float4 x[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        x[j] = (i0 + j * NT < n4) ? l4[i0 + j * NT] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = i0 + j * NT;
+        if (i < n4) {
+          visit(x[j].x, 4 * i);
+          visit(x[j].y, 4 * i + 1);
+          visit(x[j].z, 4 * i + 2);
+          visit(x[j].w, 4 * i + 3);
+        }
+      }
+    }
+  } else {
+    for (int v = threadIdx.x; v < vocab; v += NT) visit(l[v], v);
   }
-  // argmax: larger value wins, equal values -> lower index
   for (int o = 32; o > 0; o >>= 1) {
-    float ob = __shfl_xor(best, o, 64);
-    int oa = __shfl_xor(barg, o, 64);
+    const float ob = __shfl_xor(best, o, 64);
+    const int oa = __shfl_xor(barg, o, 64);
     if (ob > best || (ob == best && oa < barg)) {
       best = ob;
       barg = oa;
@@ -317,20 +362,18 @@ __global__ __launch_bounds__(512) void k_softmax_stats(const float *__restrict__
     smax[w] = best;
     sarg[w] = barg;
     sbad[w] = bad;
-    red[w] = (double)zbest;
+    szmax[w] = zbest;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    float b = smax[0];
-    int a = sarg[0];
-    float zb = (float)red[0];
-    int bd = sbad[0];
+    float b = smax[0], zb = szmax[0];
+    int a = sarg[0], bd = sbad[0];
     for (int i = 1; i < NW; ++i) {
       if (smax[i] > b || (smax[i] == b && sarg[i] < a)) {
         b = smax[i];
         a = sarg[i];
       }
-      zb = fmaxf(zb, (float)red[i]);
+      zb = fmaxf(zb, szmax[i]);
       bd |= sbad[i];
     }
     smax[0] = greedy ? b : zb;
@@ -341,13 +384,27 @@ __global__ __launch_bounds__(512) void k_softmax_stats(const float *__restrict__
   const float zmax = smax[0];
   const int arg = sarg[0];
   const int anybad = sbad[0];
-  __syncthreads();
   double total = 1.0;
   if (!greedy) {
     double part = 0.0;
-    for (int v = threadIdx.x; v < vocab; v += NT) {
-      const float z = l[v] * inv_t;
-      part += (double)expf(z - zmax);
+    if (vec) {
+      const float4 *l4 = (const float4 *)l;
+      const int n4 = vocab >> 2;
+      for (int i0 = threadIdx.x; i0 < n4; i0 += 4 * NT) {
+        float4 x[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          x[j] = (i0 + j * NT < n4) ? l4[i0 + j * NT] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          part += (double)expf(x[j].x * inv_t - zmax);
+          part += (double)expf(x[j].y * inv_t - zmax);
+          part += (double)expf(x[j].z * inv_t - zmax);
+          part += (double)expf(x[j].w * inv_t - zmax);
+        }
+      }
+    } else {
+      for (int v = threadIdx.x; v < vocab; v += NT) part += (double)expf(l[v] * inv_t - zmax);
     }
     part = wave_sum(part);
     if (lane == 0) red[w] = part;
@@ -355,10 +412,10 @@ __global__ __launch_bounds__(512) void k_softmax_stats(const float *__restrict__
     if (threadIdx.x == 0) {
       double t = 0.0;
       for (int i = 0; i < NW; ++i) t += red[i];
-      red[NW] = t;
+      red[0] = t;
     }
     __syncthreads();
-    total = red[NW];
+    total = red[0];
   }
   if (threadIdx.x == 0) {
     sb_row_stats st;
@@ -489,7 +546,7 @@ hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, floa
   float inv_t;
   int greedy;
   temp_args(temperature, &inv_t, &greedy);
-  hipLaunchKernelGGL(k_softmax_stats, dim3(n_rows), dim3(512), 0, s, logits, vocab, inv_t, greedy,
+  hipLaunchKernelGGL(k_softmax_stats, dim3(n_rows), dim3(1024), 0, s, logits, vocab, inv_t, greedy,
                      stats);
   return hipGetLastError();
 }

@@ -26,7 +26,8 @@ hipError_t launch_select(int vocab, const float *logits_row, const sb_row_stats 
 size_t sample_ws_bytes(int vocab);
 
 // ---- rollback (k_rollback.hip) ---------------------------------------------
-hipError_t launch_rollback(int n_layers, int n_kv, int capacity, int row_bytes, void *k, void *v,
-                           int kv_len, const sb_step_result *res, int32_t *new_len, hipStream_t s);
+hipError_t launch_rollback(int n_layers, int n_kv, int capacity, int head_dim, int elem_bytes,
+                           void *k, void *v, int kv_len, const sb_step_result *res,
+                           int32_t *new_len, hipStream_t s);
 
 }  // namespace sb

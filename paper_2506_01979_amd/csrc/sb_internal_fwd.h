@@ -80,13 +80,14 @@ struct EmbedArgs {
   Meta *meta;
   float2 *rope;  // [n_tok][head_dim/2] cos, sin
   int head_dim;
-  float rope_theta;
+  double theta[128];  // RoPE frequencies base^(-2j/d), j < head_dim/2
 };
 
 struct GemmArgs {
   const uint16_t *W;   // packed weights
   const uint16_t *X;   // packed activations
   int ks;              // k-steps
+  int tiles;           // 16-row weight tiles
   int n_tok;           // valid activation rows
   int out_rows;        // RESID: hidden; LOGITS: vocab
   float *h;            // RESID output (fp32 [rows][out_rows])

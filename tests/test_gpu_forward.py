@@ -54,8 +54,7 @@ def gpu_forward(api, m, Kp, Vp, kv_len, tokens, parents, T=1.0, cap=None):
     cap = cap or kv_len + n + 8
     k, v = m.new_kv(cap)
     if kv_len:
-        k[:, :, :kv_len] = torch.from_numpy(np.ascontiguousarray(Kp[:, :, :kv_len], np.float32)).to(m.wdtype)
-        v[:, :, :kv_len] = torch.from_numpy(np.ascontiguousarray(Vp[:, :, :kv_len], np.float32)).to(m.wdtype)
+        m.load_kv(k, v, Kp, Vp, kv_len)
     logits = torch.empty((n, m.shape.vocab), dtype=torch.float32, device="cuda")
     stats = api.new_stats(n)
     ws = m.workspace(n, kv_len)
@@ -106,14 +105,14 @@ def test_verify_forward_parity(api, sname, P, spec):
     err = row_relerr(got, ref)
     say(f"  logits row-relative error {err:.3e}")
     assert err < tol(shape)
-    kg = k[:, :, kv_len:kv_len + n].float().cpu().numpy()
-    vg = v[:, :, kv_len:kv_len + n].float().cpu().numpy()
+    kg, vg = m.read_kv(k, v, kv_len, n)
     assert row_relerr(kg.reshape(-1, shape.head_dim), kt.reshape(-1, shape.head_dim)) < tol(shape) * 5
     assert row_relerr(vg.reshape(-1, shape.head_dim), vt.reshape(-1, shape.head_dim)) < tol(shape) * 5
     # the prefix slots are untouched
     if kv_len:
-        kp = k[:, :, :kv_len].float().cpu().numpy()
+        kp, vp = m.read_kv(k, v, 0, kv_len)
         assert np.array_equal(kp, np.asarray(Kp[:, :, :kv_len], np.float32))
+        assert np.array_equal(vp, np.asarray(Vp[:, :, :kv_len], np.float32))
 
 
 @pytest.mark.parametrize("sname", ["tiny", "small_bf16", "small_gqa_bf16"])
@@ -161,8 +160,7 @@ def test_gpu_chunked_prefill(api, sname):
         m.sb_verify_forward(k, v, done, toks, synth.chain_parents(n), 1.0, logits, stats, ws)
         done += n
     torch.cuda.synchronize()
-    kg = k[:, :, :P].float().cpu().numpy()
-    vg = v[:, :, :P].float().cpu().numpy()
+    kg, vg = m.read_kv(k, v, 0, P)
     assert row_relerr(kg.reshape(-1, shape.head_dim), Kr.reshape(-1, shape.head_dim)) < tol(shape) * 5
     assert row_relerr(vg.reshape(-1, shape.head_dim), Vr.reshape(-1, shape.head_dim)) < tol(shape) * 5
 
@@ -170,7 +168,7 @@ def test_gpu_chunked_prefill(api, sname):
 def test_verify_forward_host_errors(api):
     shape = synth.SHAPES["tiny"]
     m = model(api, shape)
-    k, v = m.new_kv(20)
+    k, v = m.new_kv(24)
     logits = torch.empty((4, shape.vocab), dtype=torch.float32, device="cuda")
     stats = api.new_stats(4)
     ws = m.workspace(4, 16)
@@ -179,7 +177,7 @@ def test_verify_forward_host_errors(api):
         m.sb_verify_forward(k, v, 16, toks, [-1, 0, 1, 2], 1.0, logits, stats, ws[:10])
     assert e.value.code == 3           # workspace too small
     with pytest.raises(api.SBError) as e:
-        m.sb_verify_forward(k, v, 17, toks, [-1, 0, 1, 2], 1.0, logits, stats, ws)
+        m.sb_verify_forward(k, v, 21, toks, [-1, 0, 1, 2], 1.0, logits, stats, ws)
     assert e.value.code == 3           # kv_len + n_rows > capacity
     with pytest.raises(api.SBError) as e:
         m.sb_verify_forward(k, v, 4, toks, [-1, 0, 3, 1], 1.0, logits, stats, ws)

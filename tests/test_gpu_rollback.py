@@ -36,7 +36,7 @@ def test_rollback_bytes(api, sname, path):
     shape = synth.SHAPES[sname]
     say(f"rollback bytes {sname} path={path}")
     m = api.Model(shape.with_layers(2), api.synth_tensors(shape.with_layers(2)))
-    kv_len, cap = 37, 37 + 40
+    kv_len, cap = 37, 80
     g = np.random.default_rng(len(path))
     L = 2
     K = g.standard_normal((L, shape.n_kv_heads, cap, shape.head_dim)).astype(np.float32)
@@ -44,15 +44,16 @@ def test_rollback_bytes(api, sname, path):
     if shape.dtype == "bf16":
         K = decoder.round_bf16(K)
         V = decoder.round_bf16(V)
-    k = torch.from_numpy(K).to(m.wdtype).cuda()
-    v = torch.from_numpy(V).to(m.wdtype).cuda()
+    k, v = m.new_kv(cap)
+    m.load_kv(k, v, K, V, cap)
     new_len = torch.zeros(1, dtype=torch.int32, device="cuda")
     m.sb_kv_rollback(k, v, kv_len, result_tensor(api, path), new_len)
     torch.cuda.synchronize()
     K2, V2, n2 = rollback.kv_rollback(K, V, kv_len, path)
     assert int(new_len.item()) == n2
-    assert np.array_equal(k.float().cpu().numpy(), K2)
-    assert np.array_equal(v.float().cpu().numpy(), V2)
+    kg, vg = m.read_kv(k, v, 0, cap)
+    assert np.array_equal(kg, K2)
+    assert np.array_equal(vg, V2)
 
 
 @pytest.mark.parametrize("sname,seed_u", [("tiny", 1), ("tiny", 4), ("small_bf16", 2),
@@ -72,8 +73,7 @@ def test_rollback_equals_fresh_prefill(api, sname, seed_u):
     m = api.Model(shape, api.dict_tensors(W))
     cap = kv_len + n + 4
     k, v = m.new_kv(cap)
-    k[:, :, :kv_len] = torch.from_numpy(np.asarray(Kp, np.float32)).to(m.wdtype)
-    v[:, :, :kv_len] = torch.from_numpy(np.asarray(Vp, np.float32)).to(m.wdtype)
+    m.load_kv(k, v, Kp, Vp, kv_len)
     g = np.random.default_rng(seed_u)
     toks = g.integers(0, shape.vocab, n).astype(np.int32)
     toks[0] = ptoks[-1]
@@ -105,20 +105,19 @@ def test_rollback_equals_fresh_prefill(api, sname, seed_u):
     acc = [int(toks[i]) for i in path[1:]]
     seq = np.concatenate([ptoks, np.asarray(acc, np.int32)])
     _, Kf, Vf = decoder.prefill(shape, W, seq, md)
-    kg = k[:, :, :nl].float().cpu().numpy()
-    vg = v[:, :, :nl].float().cpu().numpy()
+    kg, vg = m.read_kv(k, v, 0, nl)
     assert row_relerr(kg.reshape(-1, shape.head_dim), Kf.reshape(-1, shape.head_dim)) < 5 * tol
     assert row_relerr(vg.reshape(-1, shape.head_dim), Vf.reshape(-1, shape.head_dim)) < 5 * tol
     # the same rows from a fresh GPU forward of root + accepted tokens
     k2, v2 = m.new_kv(cap)
     k2[:, :, :kv_len] = k[:, :, :kv_len]
-    v2[:, :, :kv_len] = v[:, :, :kv_len]
+    v2[:, :, :, :kv_len] = v[:, :, :, :kv_len]
     nn = 1 + len(acc)
     l2 = torch.empty((nn, shape.vocab), dtype=torch.float32, device="cuda")
     m.sb_verify_forward(k2, v2, kv_len, torch.from_numpy(seq[kv_len:].astype(np.int32)).cuda(),
                         synth.chain_parents(nn), 1.0, l2, api.new_stats(nn), m.workspace(nn, kv_len))
     torch.cuda.synchronize()
-    k2g = k2[:, :, :nl].float().cpu().numpy()
+    k2g, _ = m.read_kv(k2, v2, 0, nl)
     assert row_relerr(k2g.reshape(-1, shape.head_dim), kg.reshape(-1, shape.head_dim)) < tol
 
 
