@@ -94,8 +94,11 @@ typedef struct {
   const sb_layer_weights *layers;  /* host array of n_layers entries */
 } sb_model_weights;
 
-/* KV cache: k and v are [n_layers][n_kv_heads][capacity][head_dim] in the
- * model dtype; slots [0, kv_len) hold the committed prefix. */
+/* KV cache in the model dtype: k is [n_layers][n_kv_heads][capacity][head_dim]
+ * (one key per row) and v is stored transposed, [n_layers][n_kv_heads]
+ * [head_dim][capacity] (one value dimension per row), so attention reads both
+ * with unit-stride vector loads along its own contraction.  capacity must be
+ * a multiple of 8; slots [0, kv_len) hold the committed prefix. */
 typedef struct {
   void *k;
   void *v;
@@ -145,7 +148,8 @@ size_t sb_packed_bytes(const sb_model_config *cfg, int32_t kind);
 
 /* Re-lays one weight kind into the kernels' layout: for SB_BF16, 16-row x
  * 32-column tiles in the operand order of the gfx950 bf16 matrix-core
- * instruction (rows padded to 16 and columns to 32 with zeros; Q/K rows of
+ * instruction (rows padded to 16 and columns to a multiple of 256 -- whole
+ * chunks of 8 k-steps -- with zeros; Q/K rows of
  * every head reordered so a tile holds RoPE pairs (j, j + d/2); gate and up
  * rows interleaved 8 by 8); for SB_F32, the source rows concatenated
  * (Wq;Wk;Wv and Wgate;Wup).  src* and dst are device pointers, dst holds

@@ -35,7 +35,7 @@ constexpr int kBf16MaxKeys = 512 * kAttnChunk;  // chunks one merge workgroup co
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  size_t meta, rope, h;
+  size_t meta, rope, h, delta;
   // bf16
   size_t xa, act, q, part_o, part_ml;
   // f32
@@ -61,9 +61,11 @@ Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
   L.rope = take((size_t)np * (d / 2) * sizeof(float2));
   L.h = take((size_t)np * H * sizeof(float));
   if (c.dtype == SB_BF16) {
-    L.ks_h = ceil_div(H, 32);
-    L.ks_o = ceil_div(qd, 32);
-    L.ks_f = round_up(F, 32) / 32;
+    L.delta = take((size_t)kMaxSplit * np * H * sizeof(float));
+    // packed activations use the k-steps of the weights they multiply
+    L.ks_h = pack_geom(c, SB_W_QKV).ks;
+    L.ks_o = pack_geom(c, SB_W_O).ks;
+    L.ks_f = pack_geom(c, SB_W_DOWN).ks;
     const int ksx = L.ks_h > L.ks_o ? L.ks_h : L.ks_o;
     L.n_chunks = ceil_div(kv_len + n_rows, kAttnChunk);
     L.xa = take((size_t)np * ksx * 32 * 2);
@@ -180,10 +182,10 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
                        sb_row_stats *stats, char *ws, const Layout &L, hipStream_t s) {
   const sb_model_config &c = m->cfg;
   const int H = c.hidden, d = c.head_dim;
-  const int tt = L.np / 16;
   Meta *meta = (Meta *)(ws + L.meta);
   float2 *rope = (float2 *)(ws + L.rope);
   float *h = (float *)(ws + L.h);
+  float *delta = (float *)(ws + L.delta);
   uint16_t *xa = (uint16_t *)(ws + L.xa);
   uint16_t *act = (uint16_t *)(ws + L.act);
   uint16_t *q = (uint16_t *)(ws + L.q);
@@ -205,7 +207,7 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   ga.n_kv = c.n_kv_heads;
   ga.head_dim = d;
   ga.rope = rope;
-  ga.h = h;
+  ga.h = delta;
   ga.act = act;
   ga.act_ks = L.ks_f;
   ga.logits = logits;
@@ -225,17 +227,20 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   aa.part_o = (float *)(ws + L.part_o);
   aa.part_ml = (float *)(ws + L.part_ml);
 
+  int split = 0;  // delta slices left by the last residual projection
   for (int l = 0; l < c.n_layers; ++l) {
     const sb_layer_weights &lw = m->layers[l];
     uint16_t *kc = (uint16_t *)kv->k + l * layer_kv;
     uint16_t *vc = (uint16_t *)kv->v + l * layer_kv;
-    SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, lw.attn_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+    SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, split ? delta : nullptr, split ? split : 1,
+                                             lw.attn_norm, H, L.ks_h, n, L.np, c.rms_eps, xa,
+                                             s));
     ga.W = (const uint16_t *)lw.qkv;
     ga.X = xa;
     ga.ks = gq.ks;
     ga.kc = kc;
     ga.vc = vc;
-    SB_TIMED(SB_KC_QKV, launch_gemm(EPI_QKV, ga, gq.tiles, tt, s));
+    SB_TIMED(SB_KC_QKV, launch_gemm(EPI_QKV, ga, gq.tiles, nullptr, s));
     aa.kc = kc;
     aa.vc = vc;
     SB_TIMED(SB_KC_ATTN, launch_attn_bf16(aa, s));
@@ -244,24 +249,26 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
     ga.X = xa;
     ga.ks = go.ks;
     ga.out_rows = H;
-    SB_TIMED(SB_KC_O, launch_gemm(EPI_RESID, ga, go.tiles, tt, s));
-    SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, lw.mlp_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+    SB_TIMED(SB_KC_O, launch_gemm(EPI_RESID, ga, go.tiles, &split, s));
+    SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, delta, split, lw.mlp_norm, H, L.ks_h, n, L.np,
+                                             c.rms_eps, xa, s));
     ga.W = (const uint16_t *)lw.gate_up;
     ga.X = xa;
     ga.ks = gg.ks;
-    SB_TIMED(SB_KC_GATE_UP, launch_gemm(EPI_SWIGLU, ga, gg.tiles, tt, s));
+    SB_TIMED(SB_KC_GATE_UP, launch_gemm(EPI_SWIGLU, ga, gg.tiles, nullptr, s));
     ga.W = (const uint16_t *)lw.down;
     ga.X = act;
     ga.ks = gd.ks;
     ga.out_rows = H;
-    SB_TIMED(SB_KC_DOWN, launch_gemm(EPI_RESID, ga, gd.tiles, tt, s));
+    SB_TIMED(SB_KC_DOWN, launch_gemm(EPI_RESID, ga, gd.tiles, &split, s));
   }
-  SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+  SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, split ? delta : nullptr, split ? split : 1,
+                                           m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
   ga.W = (const uint16_t *)m->lm_head;
   ga.X = xa;
   ga.ks = gl.ks;
   ga.out_rows = c.vocab;
-  SB_TIMED(SB_KC_LM_HEAD, launch_gemm(EPI_LOGITS, ga, gl.tiles, tt, s));
+  SB_TIMED(SB_KC_LM_HEAD, launch_gemm(EPI_LOGITS, ga, gl.tiles, nullptr, s));
   SB_TIMED(SB_KC_STATS, launch_softmax_stats(c.vocab, n, logits, temperature, stats, s));
   return SB_OK;
 }

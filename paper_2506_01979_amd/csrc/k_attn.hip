@@ -292,6 +292,13 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, uint16_t *__rest
     pk.w = b[6] | ((uint32_t)b[7] << 16);
     *(uint4 *)(out + packed_index(t, head * D + d0, ks)) = pk;
   }
+  // the last head also clears the padding columns of the packed row (the
+  // GEMM reads K in whole chunks)
+  const int width = a.n_heads * D;
+  if (head == a.n_heads - 1) {
+    for (int k0 = width + (int)threadIdx.x * 8; k0 < ks * 32; k0 += 256 * 8)
+      *(uint4 *)(out + packed_index(t, k0, ks)) = make_uint4(0, 0, 0, 0);
+  }
 }
 
 }  // namespace

@@ -1,16 +1,16 @@
 // bf16 forward kernels for gfx950: weight packing, embedding + tree
 // metadata, RMSNorm into the packed operand layout, and the skinny
-// matrix-core GEMM with fused epilogues (RoPE + KV write, residual add,
+// matrix-core GEMM with fused epilogues (RoPE + KV write, residual delta,
 // SwiGLU, logits).
 //
 // The verify forward multiplies n_rows (5..256) activation rows by every
 // weight matrix once; the weights (13-140 GB) dominate the bytes, so the
 // GEMM streams each weight tile from HBM exactly once with 16-byte loads in
 // the operand order of v_mfma_f32_16x16x32_bf16 (the layout sb_pack_weight
-// writes), keeps all activation rows of the step resident as B operands, and
-// splits K across the 8 waves of a workgroup, reducing in LDS.  A workgroup
-// owns one 16-row output tile, so every output element is finished inside one
-// workgroup and its epilogue runs there.
+// writes).  One workgroup per compute unit owns a range of weight tiles and
+// walks K in chunks, reusing each activation fragment across all of its
+// tiles; the residual projections, about one tile per compute unit, also
+// split K across workgroups and leave partial deltas for the next RMSNorm.
 #include <math.h>
 
 #include "sb_device.h"
@@ -31,7 +31,7 @@ struct PackArgs {
   uint16_t *dst;
   int kind;
   int K;        // source columns
-  int ks;       // packed k-steps (K padded to 32)
+  int ks;       // packed k-steps (K padded to whole 8-k-step chunks)
   int tiles;
   int n_heads, n_kv, head_dim, ffn, rows0;  // rows0: rows of src0 for O/DOWN/LM
 };
@@ -154,8 +154,13 @@ __global__ __launch_bounds__(256) void k_embed_meta(EmbedArgs a, TreeArg tree) {
 // One workgroup per row; a thread holds IPT groups of 8 columns in registers
 // (one read of the row), the sum of squares is reduced across the block, and
 // each group is written as one 16-byte store.
+// With delta set, the n_delta slices of the previous projection (one per K
+// range of a split-K GEMM, [n_delta][n_tok][hidden]) are first summed in
+// slice order and added to the residual row, which is written back.
 template <int IPT>
-__global__ __launch_bounds__(256) void k_rmsnorm_pack(const float *__restrict__ h,
+__global__ __launch_bounds__(256) void k_rmsnorm_pack(float *__restrict__ h,
+                                                      const float *__restrict__ delta,
+                                                      int n_delta,
                                                       const float *__restrict__ g, int hidden,
                                                       int ks, int n_tok, float eps,
                                                       uint16_t *__restrict__ out) {
@@ -170,8 +175,22 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(const float *__restrict__ 
     const int it = threadIdx.x + j * 256;
     const int k0 = it * 8;
     if (live && it < items && k0 < hidden) {
-      const float4 *src = (const float4 *)(h + (size_t)t * hidden + k0);
-      const float4 p0 = src[0], p1 = src[1];
+      float4 *src = (float4 *)(h + (size_t)t * hidden + k0);
+      float4 p0 = src[0], p1 = src[1];
+      if (delta) {  // residual add of the previous projection
+        const float4 *dd = (const float4 *)(delta + (size_t)t * hidden + k0);
+        float4 d0 = dd[0], d1 = dd[1];
+        const size_t stride = (size_t)n_tok * hidden / 4;
+        for (int sl = 1; sl < n_delta; ++sl) {
+          const float4 e0 = dd[sl * stride], e1 = dd[sl * stride + 1];
+          d0.x += e0.x; d0.y += e0.y; d0.z += e0.z; d0.w += e0.w;
+          d1.x += e1.x; d1.y += e1.y; d1.z += e1.z; d1.w += e1.w;
+        }
+        p0.x += d0.x; p0.y += d0.y; p0.z += d0.z; p0.w += d0.w;
+        p1.x += d1.x; p1.y += d1.y; p1.z += d1.z; p1.w += d1.w;
+        src[0] = p0;
+        src[1] = p1;
+      }
       x[j][0] = p0.x; x[j][1] = p0.y; x[j][2] = p0.z; x[j][3] = p0.w;
       x[j][4] = p1.x; x[j][5] = p1.y; x[j][6] = p1.z; x[j][7] = p1.w;
     } else {
@@ -220,12 +239,11 @@ __device__ __forceinline__ void rope_pair(float x1, float x2, float2 cs, float *
 }
 
 // Epilogue of one finished output pair: rows p and p + 8 of tile `tile`,
-// activation row t, values v1 / v2.
-template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs &a, int tile, int p, int t, float v1,
-                                         float v2) {
-  if constexpr (EPI == EPI_QKV) {
-    if (t >= a.n_tok) return;
+// activation row t < n_tok, values v1 / v2 (K range `split` of a split-K
+// launch).
+__device__ __forceinline__ void epilogue(const GemmArgs &a, int split, int tile, int p, int t,
+                                         float v1, float v2) {
+  if (a.epi == EPI_QKV) {
     const int d = a.head_dim, ht = d / 16;
     const int qt = a.n_heads * ht, kt = a.n_kv * ht;
     if (tile < qt + kt) {
@@ -247,18 +265,18 @@ __device__ __forceinline__ void epilogue(const GemmArgs &a, int tile, int p, int
       col[0] = f2bf(v1);
       col[(size_t)8 * a.cap] = f2bf(v2);
     }
-  } else if constexpr (EPI == EPI_RESID) {
-    if (t >= a.n_tok) return;
+  } else if (a.epi == EPI_RESID) {
+    // the projection is stored as a delta (one slice per K range); the next
+    // RMSNorm adds the slices to the residual stream
     const int d1 = tile * 16 + p, d2 = d1 + 8;
-    float *hrow = a.h + (size_t)t * a.out_rows;
-    if (d1 < a.out_rows) hrow[d1] += v1;
-    if (d2 < a.out_rows) hrow[d2] += v2;
-  } else if constexpr (EPI == EPI_SWIGLU) {
+    float *drow = a.h + ((size_t)split * a.n_tok + t) * a.out_rows;
+    if (d1 < a.out_rows) drow[d1] = v1;
+    if (d2 < a.out_rows) drow[d2] = v2;
+  } else if (a.epi == EPI_SWIGLU) {
     const int f = tile * 8 + p;
     const float gsil = v1 / (1.0f + expf(-v1));
     a.act[packed_index(t, f, a.act_ks)] = f2bf(gsil * v2);
   } else {  // EPI_LOGITS
-    if (t >= a.n_tok) return;
     const int v1i = tile * 16 + p, v2i = v1i + 8;
     float *lrow = a.logits + (size_t)t * a.out_rows;
     if (v1i < a.out_rows) lrow[v1i] = v1;
@@ -266,143 +284,205 @@ __device__ __forceinline__ void epilogue(const GemmArgs &a, int tile, int p, int
   }
 }
 
-// A workgroup owns RT consecutive 16-row tiles; its 8 waves split K.  Each
-// wave streams its weight fragments with a two-deep software pipeline
-// (batch i+1 in flight while batch i feeds the matrix cores).
-template <int TT, int EPI, int RT>
-__global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs a) {
-  extern __shared__ float red[];  // [waves][RT][TT][64 lanes][4]
-  constexpr int U = TT <= 4 ? 2 : 1;
-  const int tile0 = blockIdx.x * RT;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+// Chunk-major weight-streaming GEMM.
+//
+// K is cut into chunks of 8 k-steps; wave w of a workgroup owns k-step
+// 8c + w of every chunk c.  A workgroup owns a range of 16-row weight tiles
+// (and, for split-K launches, one K range), and a wave walks its chunks in
+// order: per chunk it loads its TT activation fragments once and the NT
+// weight fragments of that k-step (one per tile), so each activation
+// fragment feeds NT matrix-core products.  Activation re-reads from L2 are
+// what limits a skinny GEMM whose waves stream one tile at a time; reusing
+// them across the workgroup's tiles cuts that traffic NT-fold.  Loads run R
+// chunks ahead in a register ring.  At the end the 8 waves' partial sums of
+// every tile are reduced in LDS and the epilogue runs.
+//
+// Ring depth per (TT, NT): as deep as the 256-register budget of two waves
+// per SIMD allows (ring 4R(NT+TT), accumulators 4*NT*TT, lane offsets NT+TT,
+// about 48 for the rest).
+template <int TT, int NT>
+struct Ring {
+  static constexpr int free_regs = 208 - TT - NT - 4 * NT * TT;
+  static constexpr int r = free_regs / (4 * (NT + TT));
+  static constexpr int R = r > 4 ? 4 : (r < 1 ? 1 : r);
+};
+
+// token tiles reduced per LDS round
+constexpr int kRedTT = 4;
+
+// Workgroup barrier for LDS traffic only (does not wait for global loads).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int TT, int NT>
+__global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
+  __shared__ f32x4 red[kGemmWaves][kRedTT][64];
+  constexpr int R = Ring<TT, NT>::R;
+  constexpr int RT = TT < kRedTT ? TT : kRedTT;
+  // wave-uniform quantities live in scalar registers
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int ks = a.ks;
-  const int s0 = (ks * w) / kGemmWaves, s1 = (ks * (w + 1)) / kGemmWaves;
-  const uint4 *Wt[RT];
+  const int S = a.split;
+  const int split = blockIdx.x % S, grp = blockIdx.x / S;
+  const int t_lo = (int)(((long long)a.tiles * grp) / a.groups);
+  const int t_hi = (int)(((long long)a.tiles * (grp + 1)) / a.groups);
+  const int nc = ks >> 3;
+  const int c_begin = (nc * split) / S;
+  const int n_ch = (nc * (split + 1)) / S - c_begin;
+  // Activation lanes of rows >= n_tok point past the end of the buffer and
+  // read as zero; weight lanes of tiles past the group's end likewise.
+  const int xbytes = ((a.n_tok + 15) >> 4) * ks * 1024;
+  const __amdgpu_buffer_rsrc_t xrs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.X, 0, xbytes, kBufferDword3);
+  int xvo[TT];
 #pragma unroll
-  for (int r = 0; r < RT; ++r)
-    Wt[r] = (const uint4 *)a.W + (size_t)min(tile0 + r, a.tiles - 1) * ks * 64 + lane;
-  const uint4 *__restrict__ Xp = (const uint4 *)a.X + lane;
+  for (int tt = 0; tt < TT; ++tt)
+    xvo[tt] = (tt * 16 + (lane & 15)) < a.n_tok ? tt * ks * 1024 + lane * 16 : xbytes;
 
-  bool tv[TT];
+  for (int gb = t_lo; gb < t_hi; gb += NT) {
+    const int n_here = t_hi - gb < NT ? t_hi - gb : NT;
+    const int wbytes = n_here * ks * 1024;
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)a.W + (size_t)gb * ks * 1024), 0, wbytes, kBufferDword3);
+    int wvo[NT];
 #pragma unroll
-  for (int tt = 0; tt < TT; ++tt) tv[tt] = (tt * 16 + (lane & 15)) < a.n_tok;
+    for (int t = 0; t < NT; ++t) wvo[t] = t < n_here ? t * ks * 1024 + lane * 16 : wbytes;
 
-  f32x4 acc[RT][TT];
+    i32x4 wr[R][NT], xr[R][TT];
+    f32x4 acc[NT][TT];
 #pragma unroll
-  for (int r = 0; r < RT; ++r)
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) acc[r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  auto load = [&](int s, uint4(&av)[U][RT], uint4(&bv)[U][TT]) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-#pragma unroll
-      for (int r = 0; r < RT; ++r)
-        av[u][r] = (s + u < s1) ? load_stream(Wt[r] + (size_t)(s + u) * 64) : make_uint4(0, 0, 0, 0);
+      for (int tt = 0; tt < TT; ++tt) acc[t][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // loads of this wave's k-step of chunk c (relative to the K range)
+    auto issue = [&](int r, int c) {
+      const int koff = ((c_begin + c) * 8 + w) * 1024;
 #pragma unroll
       for (int tt = 0; tt < TT; ++tt)
-        bv[u][tt] = (s + u < s1 && tv[tt]) ? Xp[((size_t)tt * ks + s + u) * 64]
-                                            : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto compute = [&](uint4(&av)[U][RT], uint4(&bv)[U][TT]) {
+        xr[r][tt] = __builtin_amdgcn_raw_buffer_load_b128(xrs, xvo[tt], koff, 0);
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+      for (int t = 0; t < NT; ++t)
+        wr[r][t] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo[t], koff, kNonTemporal);
+    };
+    auto mac = [&](int r) {
 #pragma unroll
-      for (int r = 0; r < RT; ++r)
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt)
-          acc[r][tt] = mfma16(as_bf16x8(av[u][r]), as_bf16x8(bv[u][tt]), acc[r][tt]);
-  };
-  if constexpr (TT <= 8) {
-    uint4 a0[U][RT], b0[U][TT], a1[U][RT], b1[U][TT];
-    int s = s0;
-    if (s < s1) load(s, a0, b0);
-    while (s < s1) {
-      if (s + U < s1) load(s + U, a1, b1);
-      compute(a0, b0);
-      s += U;
-      if (s >= s1) break;
-      if (s + U < s1) load(s + U, a0, b0);
-      compute(a1, b1);
-      s += U;
+          acc[t][tt] = mfma16(__builtin_bit_cast(bf16x8, wr[r][t]),
+                              __builtin_bit_cast(bf16x8, xr[r][tt]), acc[t][tt]);
+    };
+    int c = 0;
+    if (n_ch >= R) {
+      // fill the ring in slot order (the oldest loads are consumed first)
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        issue(r, r);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // steady state: every consumed slot is refilled R chunks ahead
+      for (; c + 2 * R <= n_ch; c += R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          mac(r);
+          issue(r, c + R + r);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      // the last one or two rings: refill only while chunks remain
+      for (; c < n_ch; c += R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if (c + r < n_ch) {
+            mac(r);
+            if (c + r + R < n_ch) issue(r, c + r + R);
+          }
+        }
+      }
+    } else {
+      for (; c < n_ch; ++c) {
+        issue(0, c);
+        mac(0);
+      }
     }
-  } else {  // very wide trees: one batch at a time keeps the registers in budget
-    for (int s = s0; s < s1; s += U) {
-      uint4 a0[U][RT], b0[U][TT];
-      load(s, a0, b0);
-      compute(a0, b0);
-    }
-  }
 
+    // reduce the 8 waves' partial sums tile by tile, kRedTT token tiles at
+    // a time, and run the epilogue on each finished (row pair, token)
 #pragma unroll
-  for (int r = 0; r < RT; ++r)
+    for (int t = 0; t < NT; ++t) {
+      if (t < n_here) {
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt)
-      *(f32x4 *)&red[((((size_t)w * RT + r) * TT + tt) * 64 + lane) * 4] = acc[r][tt];
-  __syncthreads();
-
-  // item = (tile r, pair p of rows p / p+8, token t)
-  const int items = RT * 8 * 16 * TT;
-  for (int it = threadIdx.x; it < items; it += kGemmThreads) {
-    const int r = it / (128 * TT);
-    const int rem = it - r * 128 * TT;
-    const int p = rem & 7;
-    const int t = rem >> 3;
-    const int tt = t >> 4;
-    const int l1 = (t & 15) + 16 * (p >> 2), e1 = p & 3;
-    const int l2 = (t & 15) + 16 * ((p + 8) >> 2), e2 = (p + 8) & 3;
-    float v1 = 0.f, v2 = 0.f;
+        for (int t0 = 0; t0 < TT; t0 += RT) {
+          if (t0 * 16 < a.n_tok) {
 #pragma unroll
-    for (int ww = 0; ww < kGemmWaves; ++ww) {
-      v1 += red[((((size_t)ww * RT + r) * TT + tt) * 64 + l1) * 4 + e1];
-      v2 += red[((((size_t)ww * RT + r) * TT + tt) * 64 + l2) * 4 + e2];
+            for (int j = 0; j < RT; ++j)
+              if (t0 + j < TT) red[w][j][lane] = acc[t][t0 + j];
+            lds_barrier();
+            for (int it = threadIdx.x; it < 128 * RT; it += kGemmThreads) {
+              const int p = it & 7;
+              const int tl = it >> 3;  // token within this round
+              const int j = tl >> 4;
+              const int tok = t0 * 16 + tl;
+              const int l1 = (tl & 15) + 16 * (p >> 2), e1 = p & 3;
+              const int l2 = (tl & 15) + 16 * ((p + 8) >> 2), e2 = (p + 8) & 3;
+              if (t0 + j < TT && tok < a.n_tok) {
+                float v1 = 0.f, v2 = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < kGemmWaves; ++ww) {
+                  v1 += red[ww][j][l1][e1];
+                  v2 += red[ww][j][l2][e2];
+                }
+                epilogue(a, split, gb + t, p, tok, v1, v2);
+              }
+            }
+            lds_barrier();
+          }
+        }
+      }
     }
-    if (tile0 + r < a.tiles) epilogue<EPI>(a, tile0 + r, p, t, v1, v2);
   }
 }
 
-template <int TT, int EPI, int RT>
-hipError_t launch_gemm_rt(const GemmArgs &a, hipStream_t s) {
-  const size_t lds = (size_t)kGemmWaves * RT * TT * 64 * 4 * sizeof(float);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)k_gemm<TT, EPI, RT>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
+int device_cus() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
   }
-  const int grid = (a.tiles + RT - 1) / RT;
-  hipLaunchKernelGGL((k_gemm<TT, EPI, RT>), dim3(grid), dim3(kGemmThreads), lds, s, a);
-  return hipGetLastError();
+  return cus;
 }
 
-// Row tiles per workgroup: more tiles share the activation fragments (fewer
-// bytes from L2 per weight byte) but leave fewer workgroups; measured best
-// on MI355X for 33-row steps: 4 for >= 768 tiles (QKV, LM head), 2 for the
-// gate/up GEMM, 1 for the 256-tile O and down GEMMs.
-template <int TT, int EPI>
-hipError_t launch_gemm_tt(const GemmArgs &a, hipStream_t s) {
-  if constexpr (TT <= 3) {
-    if (a.tiles >= 1700 || (a.tiles >= 700 && a.tiles < 1000)) return launch_gemm_rt<TT, EPI, 4>(a, s);
+// Token-tile counts with a kernel (rounded up; padded rows read as zero) and
+// the largest tile count per pass each supports.
+constexpr int kTTs[] = {1, 2, 3, 4, 6, 8, 12, 16};
+constexpr int kNTs[] = {1, 2, 3, 4, 6, 8};
+constexpr int nt_cap(int tt) { return tt <= 4 ? 8 : tt <= 6 ? 6 : tt <= 8 ? 4 : tt <= 12 ? 2 : 1; }
+
+template <int TT, int NT>
+hipError_t launch_tt_nt(const GemmArgs &a, int grid, hipStream_t s) {
+  if constexpr (NT > nt_cap(TT)) {
+    return hipErrorInvalidValue;
+  } else {
+    hipLaunchKernelGGL((k_gemm<TT, NT>), dim3(grid), dim3(kGemmThreads), 0, s, a);
+    return hipGetLastError();
   }
-  if constexpr (TT <= 4) {
-    if (a.tiles >= 700) return launch_gemm_rt<TT, EPI, 2>(a, s);
-  }
-  return launch_gemm_rt<TT, EPI, 1>(a, s);
 }
 
-template <int EPI>
-hipError_t launch_gemm_epi(const GemmArgs &a, int tt, hipStream_t s) {
-  switch (tt) {
-#define SB_TT(n) \
-  case n:        \
-    return launch_gemm_tt<n, EPI>(a, s);
-    SB_TT(1) SB_TT(2) SB_TT(3) SB_TT(4) SB_TT(5) SB_TT(6) SB_TT(7) SB_TT(8)
-    SB_TT(9) SB_TT(10) SB_TT(11) SB_TT(12) SB_TT(13) SB_TT(14) SB_TT(15) SB_TT(16)
-#undef SB_TT
-    default:
-      return hipErrorInvalidValue;
+template <int TT>
+hipError_t launch_tt(const GemmArgs &a, int nt, int grid, hipStream_t s) {
+  switch (nt) {
+    case 1: return launch_tt_nt<TT, 1>(a, grid, s);
+    case 2: return launch_tt_nt<TT, 2>(a, grid, s);
+    case 3: return launch_tt_nt<TT, 3>(a, grid, s);
+    case 4: return launch_tt_nt<TT, 4>(a, grid, s);
+    case 6: return launch_tt_nt<TT, 6>(a, grid, s);
+    case 8: return launch_tt_nt<TT, 8>(a, grid, s);
+    default: return hipErrorInvalidValue;
   }
 }
 
@@ -441,14 +521,16 @@ hipError_t launch_embed_meta(const EmbedArgs &a, const TreeArg &tree, int blocks
   return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm_pack(const float *h, const float *g, int hidden, int ks, int n_tok,
-                               int n_pad, float eps, uint16_t *out, hipStream_t s) {
+hipError_t launch_rmsnorm_pack(float *h, const float *delta, int n_delta, const float *g,
+                               int hidden, int ks, int n_tok, int n_pad, float eps, uint16_t *out,
+                               hipStream_t s) {
+  if (hidden % 8 != 0 || n_delta < 1 || n_delta > kMaxSplit) return hipErrorInvalidValue;
   const int ipt = (ks * 4 + 255) / 256;
   switch (ipt) {
 #define SB_IPT(n)                                                                              \
   case n:                                                                                      \
-    hipLaunchKernelGGL(k_rmsnorm_pack<n>, dim3(n_pad), dim3(256), 0, s, h, g, hidden, ks, n_tok, \
-                       eps, out);                                                              \
+    hipLaunchKernelGGL(k_rmsnorm_pack<n>, dim3(n_pad), dim3(256), 0, s, h, delta, n_delta, g,    \
+                       hidden, ks, n_tok, eps, out);                                           \
     break;
     SB_IPT(1) SB_IPT(2) SB_IPT(3) SB_IPT(4) SB_IPT(5) SB_IPT(6) SB_IPT(7) SB_IPT(8)
 #undef SB_IPT
@@ -458,20 +540,60 @@ hipError_t launch_rmsnorm_pack(const float *h, const float *g, int hidden, int k
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int tt, hipStream_t s) {
+GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
+  GemmPlan p{};
+  const int cus = device_cus();
+  const int nc = ks / 8;
+  const int tt = (n_tok + 15) / 16;
+  for (int v : kTTs)
+    if (v >= tt) {
+      p.tt = v;
+      break;
+    }
+  // Projections that add into the residual stream have as many tiles as the
+  // model is wide, about one per compute unit: they split K so that each
+  // workgroup owns several tiles; the next RMSNorm sums the partial deltas.
+  const int per_cu = (tiles + cus - 1) / cus;
+  int S = 1;
+  if (epi == EPI_RESID) S = per_cu == 1 ? kMaxSplit : per_cu == 2 ? 2 : 1;
+  if (S > nc) S = nc;
+  if (S < 1) S = 1;
+  int groups = cus / S;
+  if (groups > tiles) groups = tiles;
+  const int per_wg = (tiles + groups - 1) / groups;
+  const int cap = nt_cap(p.tt);
+  const int passes = (per_wg + cap - 1) / cap;
+  const int need = (per_wg + passes - 1) / passes;
+  for (int v : kNTs)
+    if (v >= need) {
+      p.nt = v;
+      break;
+    }
+  p.split = S;
+  p.groups = groups;
+  p.grid = groups * S;
+  return p;
+}
+
+hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int *split, hipStream_t s) {
+  if (a.ks % 8 != 0 || a.n_tok <= 0 || a.n_tok > SB_MAX_ROWS) return hipErrorInvalidValue;
+  const GemmPlan p = plan_gemm(epi, tiles, a.ks, a.n_tok);
   GemmArgs b = a;
+  b.epi = epi;
   b.tiles = tiles;
-  switch (epi) {
-    case EPI_QKV:
-      return launch_gemm_epi<EPI_QKV>(b, tt, s);
-    case EPI_RESID:
-      return launch_gemm_epi<EPI_RESID>(b, tt, s);
-    case EPI_SWIGLU:
-      return launch_gemm_epi<EPI_SWIGLU>(b, tt, s);
-    case EPI_LOGITS:
-      return launch_gemm_epi<EPI_LOGITS>(b, tt, s);
-    default:
-      return hipErrorInvalidValue;
+  b.split = p.split;
+  b.groups = p.groups;
+  if (split) *split = p.split;
+  switch (p.tt) {
+    case 1: return launch_tt<1>(b, p.nt, p.grid, s);
+    case 2: return launch_tt<2>(b, p.nt, p.grid, s);
+    case 3: return launch_tt<3>(b, p.nt, p.grid, s);
+    case 4: return launch_tt<4>(b, p.nt, p.grid, s);
+    case 6: return launch_tt<6>(b, p.nt, p.grid, s);
+    case 8: return launch_tt<8>(b, p.nt, p.grid, s);
+    case 12: return launch_tt<12>(b, p.nt, p.grid, s);
+    case 16: return launch_tt<16>(b, p.nt, p.grid, s);
+    default: return hipErrorInvalidValue;
   }
 }
 

@@ -9,6 +9,12 @@ namespace sb {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource word 3 for gfx9-family raw buffers, and the cache-policy
+// bit that marks a load non-temporal on gfx94x/gfx950.
+constexpr int kBufferDword3 = 0x00020000;
+constexpr int kNonTemporal = 2;
 
 // 16-byte streaming load (data read once: weights)
 __device__ __forceinline__ uint4 load_stream(const uint4 *p) {

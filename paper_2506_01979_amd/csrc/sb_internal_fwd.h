@@ -19,7 +19,7 @@ struct Meta {
 // Geometry of a packed weight kind.
 struct PackGeom {
   int K;       // source columns
-  int ks;      // packed k-steps (bf16: K padded to 32)
+  int ks;      // packed k-steps (bf16: K padded to a multiple of 256)
   int tiles;   // 16-row tiles (bf16)
   int rows;    // output rows (natural-order kinds) / total rows (f32)
   size_t bytes;
@@ -47,7 +47,7 @@ inline PackGeom pack_geom(const sb_model_config &c, int kind) {
     case SB_W_GATE_UP:
       g.K = H;
       g.rows = 2 * F;
-      g.tiles = round_up(F, 32) / 8;
+      g.tiles = round_up(F, 256) / 8;  // covers every column of the padded activation
       break;
     case SB_W_DOWN:
       g.K = F;
@@ -63,7 +63,7 @@ inline PackGeom pack_geom(const sb_model_config &c, int kind) {
       return g;
   }
   if (bf) {
-    g.ks = ceil_div(g.K, 32);
+    g.ks = round_up(ceil_div(g.K, 32), 8);  // whole 8-k-step chunks
     g.bytes = (size_t)g.tiles * g.ks * 1024;
   } else {
     g.ks = g.K;
@@ -83,14 +83,19 @@ struct EmbedArgs {
   double theta[128];  // RoPE frequencies base^(-2j/d), j < head_dim/2
 };
 
+// Largest K split of a residual projection (slices of the delta buffer).
+constexpr int kMaxSplit = 4;
+
 struct GemmArgs {
   const uint16_t *W;   // packed weights
   const uint16_t *X;   // packed activations
-  int ks;              // k-steps
+  int ks;              // k-steps (a multiple of 8)
   int tiles;           // 16-row weight tiles
   int n_tok;           // valid activation rows
   int out_rows;        // RESID: hidden; LOGITS: vocab
-  float *h;            // RESID output (fp32 [rows][out_rows])
+  int epi;             // EPI_*
+  int split, groups;   // K ranges, tile groups (grid = split * groups)
+  float *h;            // RESID output: projection delta slices, fp32 [split][n_tok][out_rows]
   float *logits;       // LOGITS output
   uint16_t *act;       // SWIGLU output (packed, act_ks k-steps)
   int act_ks;
@@ -117,9 +122,17 @@ hipError_t launch_pack_bf16(int kind, const sb_model_config &c, const void *src0
                             const void *src2, void *dst, hipStream_t s);
 hipError_t launch_embed_meta(const EmbedArgs &a, const TreeArg &tree, int blocks, int bf16,
                              hipStream_t s);
-hipError_t launch_rmsnorm_pack(const float *h, const float *g, int hidden, int ks, int n_tok,
-                               int n_pad, float eps, uint16_t *out, hipStream_t s);
-hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int tt, hipStream_t s);
+hipError_t launch_rmsnorm_pack(float *h, const float *delta, int n_delta, const float *g,
+                               int hidden, int ks, int n_tok, int n_pad, float eps, uint16_t *out,
+                               hipStream_t s);
+// Launch geometry of a GEMM: token tiles (rounded up to a kernel's), tiles per
+// pass, K split, tile groups and grid.
+struct GemmPlan {
+  int tt, nt, split, groups, grid;
+};
+GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok);
+// *split receives the K split used (the number of delta slices for RESID).
+hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int *split, hipStream_t s);
 
 // k_attn.hip
 constexpr int kAttnChunk = 128;

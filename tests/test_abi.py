@@ -57,10 +57,12 @@ def test_packed_bytes(api):
     assert api.sb_packed_bytes(c, 9) == 0
     bad = cfg(api, n_kv_heads=5)
     assert api.sb_packed_bytes(bad, api.SB_W_QKV) == 0
-    # ragged ffn (688) and vocab (1000) are padded to whole tiles
+    # ragged ffn (688) is padded to whole 256-column chunks, vocab (1000)
+    # to whole 16-row tiles; gate/up rows cover the padded ffn columns
     from paper_2506_01979_amd import synth
     s = api.make_config(synth.SHAPES["small_bf16"])
-    assert api.sb_packed_bytes(s, api.SB_W_DOWN) == 256 * 704 * 2
+    assert api.sb_packed_bytes(s, api.SB_W_DOWN) == 256 * 768 * 2
+    assert api.sb_packed_bytes(s, api.SB_W_GATE_UP) == 2 * 768 * 256 * 2
     assert api.sb_packed_bytes(s, api.SB_W_LM_HEAD) == 1008 * 256 * 2
 
 
