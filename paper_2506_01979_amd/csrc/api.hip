@@ -30,7 +30,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kF32MaxKeys = 15360;  // scores of one row in 60 KB of LDS
-constexpr int kBf16MaxKeys = 512 * kAttnChunk;  // chunks one merge workgroup combines
+constexpr int kBf16MaxKeys = 65536;  // cache slots a bf16 step may attend to
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -67,7 +67,7 @@ Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
     L.ks_o = pack_geom(c, SB_W_O).ks;
     L.ks_f = pack_geom(c, SB_W_DOWN).ks;
     const int ksx = L.ks_h > L.ks_o ? L.ks_h : L.ks_o;
-    L.n_chunks = ceil_div(kv_len + n_rows, kAttnChunk);
+    L.n_chunks = attn_splits(c.n_kv_heads, c.head_dim, kv_len + n_rows);
     L.xa = take((size_t)np * ksx * 32 * 2);
     L.act = take((size_t)np * L.ks_f * 32 * 2);
     L.q = take((size_t)np * qd * 2);
@@ -220,7 +220,6 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   aa.n_heads = c.n_heads;
   aa.n_kv = c.n_kv_heads;
   aa.head_dim = d;
-  aa.chunk = kAttnChunk;
   aa.n_chunks = L.n_chunks;
   aa.meta = meta;
   aa.scale = 1.0f / sqrtf((float)d);

@@ -6,17 +6,25 @@
 // scores all branches at once while each branch sees exactly what a separate
 // causal forward of that branch would see (Section "Branch Resampling").
 //
-// Work split: one workgroup per (KV head, chunk of 128 key slots) over the
-// combined key range [0, kv_len + n_tok).  The V cache is stored transposed
-// ([d][slot]), so both matrix-core operands that come from the cache -- K
-// rows for S^T = K Q^T and V^T rows for O^T = V^T P^T -- are 16-byte runs of
-// consecutive elements read straight from HBM.  Every cache load of the
-// chunk is issued before the first wait, so a workgroup pays one memory
-// latency; a prefix tile is fetched once and reused by every branch and
-// every query head of the KV group (GQA).  Queries and probabilities go
-// through LDS.  The workgroup writes an unnormalised partial (row max m, row
-// sum l, sum p v) per query row; the merge kernel combines the chunks with
-// the log-sum-exp rule.
+// Flash-decoding split: the key range [0, kv_len + n_tok) of each KV head is
+// cut into n_chunks ranges of at most 2 NW 32-key steps (NW = head_dim / 16
+// waves per workgroup), one workgroup each, about one per compute unit.
+// The workgroup reads its K rows and rows of the transposed V cache once,
+// straight from HBM into registers, and keeps them for every block of query
+// rows of the KV group (GQA):
+//   1. wave w scores steps w and w + NW: S^T = K Q^T, masked, row max into
+//      LDS;
+//   2. after a barrier, the block max M of each row gives p = exp(s - M);
+//      the wave writes its probabilities (bf16) and their row sums to LDS;
+//   3. after a barrier, wave w computes the 16 dimensions 16 w .. 16 w + 15
+//      of O^T = V^T P^T over all of the workgroup's keys, reading P from LDS,
+//      and writes them: every output element is finished by one wave, so
+//      the waves never merge accumulators.
+// K rows are fetched in a permuted order so that lane group lg of S^T holds
+// keys 8 lg .. 8 lg + 7, the layout P is stored and read back in.  The
+// workgroup writes an unnormalised partial (row max m, row sum l, sum p v)
+// per query row; the merge kernel combines the ranges with the log-sum-exp
+// rule.
 #include <math.h>
 
 #include "sb_device.h"
@@ -25,192 +33,279 @@
 namespace sb {
 namespace {
 
-constexpr int CH = kAttnChunk;  // keys per workgroup
-constexpr int RB = 64;          // query rows per block (4 row tiles)
-constexpr int PAD = 8;          // LDS row padding (bf16 elements)
-
-// 8 consecutive bf16 of a V^T row starting at slot `key`; slots >= nkeys
-// (never written for this step) read as zero, and nothing past the cache
-// capacity is touched.
-__device__ __forceinline__ uint4 load_vt8(const uint16_t *row, int key, int nkeys, int cap) {
-  if (key + 8 <= nkeys) return *(const uint4 *)(row + key);
-  uint4 v = make_uint4(0, 0, 0, 0);
-  if (key < nkeys && key + 8 <= cap) {
-    v = *(const uint4 *)(row + key);
-    const int keep = nkeys - key;  // 1..7 valid elements
-    uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (e >= keep) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-    v = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-  return v;
+// Workgroup barrier for LDS traffic only (does not wait for global loads).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int D>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  constexpr int KSD = D / 32;    // k-steps over head_dim
-  constexpr int DT = D / 16;     // d tiles
-  constexpr int DTW = DT / 4;    // d tiles per wave (4 waves)
-  constexpr int VV = D / 8;      // 16-byte vectors per query row
-  constexpr int KK = CH / 32;    // k-steps over the chunk's keys
-  __shared__ uint16_t P[RB][CH + PAD];  // probabilities (bf16), row-major
-  __shared__ uint16_t Qs[RB][D + PAD];  // query rows of this block
-  __shared__ float redm[4][RB];
-  __shared__ float redl[4][RB];
+// Two floats to packed bf16 (round to nearest even), one instruction.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
 
-  const int g = blockIdx.x, c = blockIdx.y;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+// Max / sum over the lane pairs (l, l ^ 16) and (l, l ^ 32) with the gfx950
+// lane-swap instructions: swapping a value with itself yields, in every lane,
+// the pair's even-row and odd-row values.
+__device__ __forceinline__ float max_x16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, v),
+                                                  __builtin_bit_cast(uint32_t, v), false, false);
+  return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
+}
+__device__ __forceinline__ float max_x32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v),
+                                                  __builtin_bit_cast(uint32_t, v), false, false);
+  return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
+}
+__device__ __forceinline__ float sum_x16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, v),
+                                                  __builtin_bit_cast(uint32_t, v), false, false);
+  return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
+}
+__device__ __forceinline__ float sum_x32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v),
+                                                  __builtin_bit_cast(uint32_t, v), false, false);
+  return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
+}
+
+// Visibility of the 8 keys k0 .. k0 + 7 (k0 a multiple of 8) for a row with
+// ancestor mask anc (LDS): prefix slots are visible, tree slot kv_len + j is
+// visible when bit j is set, slots >= nkeys are not.
+__device__ __forceinline__ uint32_t visible8(const uint32_t *anc, int k0, int kv_len, int nkeys) {
+  uint32_t vis;
+  const int jt = k0 - kv_len;
+  if (jt + 8 <= 0) {
+    vis = 0xffu;
+  } else if (jt >= 0) {
+    const int wi = jt >> 5, sh = jt & 31;  // bits jt .. jt + 7 of the 256-bit mask
+    const uint64_t win = (uint64_t)anc[wi] | ((uint64_t)(wi < 7 ? anc[wi + 1] : 0u) << 32);
+    vis = (uint32_t)(win >> sh) & 0xffu;
+  } else {
+    const int pre = -jt;  // 1..7 prefix keys, then tree bits 0 ..
+    vis = ((anc[0] << pre) | ((1u << pre) - 1u)) & 0xffu;
+  }
+  const int valid = nkeys - k0;
+  if (valid < 8) vis &= valid > 0 ? (1u << valid) - 1u : 0u;
+  return vis;
+}
+
+// D: head_dim; RT: 16-row query tiles per row block.
+template <int D, int RT>
+__global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
+  constexpr int NW = D / 16;   // waves: one per 16 output dimensions
+  constexpr int NT = NW * 64;
+  constexpr int KSD = D / 32;  // k-steps over head_dim (S)
+  constexpr int RB = 16 * RT;  // rows per block
+  constexpr int SW = 2;        // steps per wave (at most)
+  constexpr int MS = SW * NW;  // steps of a workgroup (at most)
+  constexpr int KW = 32 * MS;  // keys of a workgroup (at most)
+  __shared__ uint16_t sp[RB][KW + 8];  // probabilities (bf16), row-major
+  __shared__ uint16_t sq[RB][D + 8];   // query rows of the block (bf16)
+  __shared__ uint32_t sanc[RB][8];
+  __shared__ float smax[NW][RB];
+  __shared__ float ssum[NW][RB];
+
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int lr = lane & 15, lg = lane >> 4;
+  const int g = blockIdx.x / a.n_chunks, split = blockIdx.x % a.n_chunks;
   const int G = a.n_heads / a.n_kv;
+  const float inv_g = 1.0f / (float)G;  // r / G = floor((r + 0.5) / G) for r < 2^20
   const int R = a.n_tok * G;
-  const int key0 = c * CH;
   const int nkeys = a.kv_len + a.n_tok;
-  const uint16_t *__restrict__ kc = (const uint16_t *)a.kc + (size_t)g * a.cap * D;
-  const uint16_t *__restrict__ vt = (const uint16_t *)a.vc + (size_t)g * D * a.cap;
-  const uint16_t *__restrict__ q = (const uint16_t *)a.q;
+  const int n_steps = (nkeys + 31) >> 5;
+  const int st0 = (n_steps * split) / a.n_chunks, st1 = (n_steps * (split + 1)) / a.n_chunks;
+  const int nst = st1 - st0;  // 1 .. MS
+  const int kbytes = a.cap * D * 2, vbytes = kbytes;  // one head's K (or V^T) block
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const uint16_t *)a.kc + (size_t)g * a.cap * D), 0, kbytes, kBufferDword3);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const uint16_t *)a.vc + (size_t)g * D * a.cap), 0, vbytes, kBufferDword3);
+  const int qbytes = a.n_tok * a.n_heads * D * 2;
+  const __amdgpu_buffer_rsrc_t qrs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.q, 0, qbytes, kBufferDword3);
+  const int abytes = a.n_tok * 8 * 4;  // ancestor words of the step's rows
+  const __amdgpu_buffer_rsrc_t ars =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.meta->anc, 0, abytes, kBufferDword3);
+  // exp(x * scale) = exp2(x * c): one FMA per score before the exp2
+  const float c = a.scale * 1.44269504088896340736f;
 
-  // ---- every cache load of the chunk, issued up front
-  uint4 ka[2][KSD];
+  // ---- the workgroup's cache reads, once, into registers.  Lanes whose
+  // slot is >= nkeys (or past the workgroup's steps) get an offset past the
+  // end of the head's buffer and read zero.
+  // K: the wave's steps w + NW u; row rho of key tile i is key
+  // 8 (rho / 4) + 4 i + rho % 4
+  i32x4 kf[SW][2][KSD];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int slot = key0 + (2 * w + i) * 16 + lr;
+  for (int u = 0; u < SW; ++u) {
+    const int sl = w + NW * u;
 #pragma unroll
-    for (int s = 0; s < KSD; ++s)
-      ka[i][s] = slot < nkeys ? *(const uint4 *)(kc + (size_t)slot * D + 32 * s + 8 * lg)
-                              : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < 2; ++i) {
+      const int slot = (st0 + sl) * 32 + 8 * (lr >> 2) + 4 * i + (lr & 3);
+      const int vo = (sl < nst && slot < nkeys) ? (slot * D + 8 * lg) * 2 : kbytes;
+#pragma unroll
+      for (int ks = 0; ks < KSD; ++ks)
+        kf[u][i][ks] = __builtin_amdgcn_raw_buffer_load_b128(krs, vo, ks * 64, 0);
+    }
   }
-  uint4 va[DTW][KK];
+  // V^T: dimensions 16 w + lr, keys 8 lg .. 8 lg + 7 of every step j
+  i32x4 vf[MS];
 #pragma unroll
-  for (int i = 0; i < DTW; ++i) {
-    const uint16_t *row = vt + (size_t)((w * DTW + i) * 16 + lr) * a.cap;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) va[i][kk] = load_vt8(row, key0 + kk * 32 + 8 * lg, nkeys, a.cap);
+  for (int j = 0; j < MS; ++j) {
+    const int key = (st0 + j) * 32 + 8 * lg;
+    const int vo = (j < nst && key < nkeys) ? ((16 * w + lr) * a.cap + key) * 2 : vbytes;
+    vf[j] = __builtin_amdgcn_raw_buffer_load_b128(vrs, vo, 0, 0);
   }
 
-  for (int r0 = 0; r0 < R; r0 += RB) {
-    // stage the query rows of this block
-    for (int idx = threadIdx.x; idx < RB * VV; idx += 256) {
-      const int rr = idx / VV, dv = (idx % VV) * 8;
-      const int r = r0 + rr;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (r < R) {
-        const int t = r / G, hl = r - t * G;
-        v = *(const uint4 *)(q + ((size_t)t * a.n_heads + g * G + hl) * D + dv);
-      }
-      *(uint4 *)&Qs[rr][dv] = v;
+  for (int rb = 0; rb < R; rb += RB) {
+    // ---- stage the block's query rows and ancestor masks
+    constexpr int QPT = (RB * (D / 8) + NT - 1) / NT;
+    constexpr int APT = (RB * 8 + NT - 1) / NT;
+    i32x4 qst[QPT];
+    int ast[APT];
+#pragma unroll
+    for (int j = 0; j < QPT; ++j) {
+      const int idx = threadIdx.x + j * NT;
+      const int rr = idx / (D / 8), d0 = (idx % (D / 8)) * 8;
+      const int r = rb + rr;
+      const int t = (int)(((float)r + 0.5f) * inv_g), hl = r - t * G;
+      const int vo = (rr < RB && r < R) ? ((t * a.n_heads + g * G + hl) * D + d0) * 2 : qbytes;
+      qst[j] = __builtin_amdgcn_raw_buffer_load_b128(qrs, vo, 0, 0);
     }
-    __syncthreads();
-    // ---- S^T = K Q^T for this wave's 2 key tiles x 4 row tiles
-    f32x4 sacc[2][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) sacc[i][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < KSD; ++s) {
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        const uint4 qb = *(const uint4 *)&Qs[rt * 16 + lr][32 * s + 8 * lg];
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-          sacc[i][rt] = mfma16(as_bf16x8(ka[i][s]), as_bf16x8(qb), sacc[i][rt]);
-      }
+    for (int j = 0; j < APT; ++j) {
+      const int idx = threadIdx.x + j * NT;
+      const int rr = idx >> 3, wd = idx & 7;
+      const int r = rb + rr;
+      const int t = (int)(((float)r + 0.5f) * inv_g);
+      const int vo = (rr < RB && r < R) ? (t * 8 + wd) * 4 : abytes;
+      ast[j] = __builtin_amdgcn_raw_buffer_load_b32(ars, vo, 0, 0);
     }
-    // ---- scale, mask, row max over this wave's 32 keys
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
-      const int r = r0 + rt * 16 + lr;
-      const int t = r < R ? r / G : 0;
-      float m = -INFINITY;
+    for (int j = 0; j < QPT; ++j) {
+      const int idx = threadIdx.x + j * NT;
+      const int rr = idx / (D / 8), d0 = (idx % (D / 8)) * 8;
+      if (rr < RB) *(i32x4 *)&sq[rr][d0] = qst[j];
+    }
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+    for (int j = 0; j < APT; ++j) {
+      const int idx = threadIdx.x + j * NT;
+      if ((idx >> 3) < RB) sanc[idx >> 3][idx & 7] = (uint32_t)ast[j];
+    }
+    lds_barrier();
+
+    // ---- 1. scores of the wave's steps, row max
+    float sv[SW][RT][8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int slot = key0 + (2 * w + i) * 16 + 4 * lg + e;
-          bool ok = slot < a.kv_len;
-          if (!ok && slot < nkeys) {
-            const int j = slot - a.kv_len;
-            ok = (a.meta->anc[t][j >> 5] >> (j & 31)) & 1u;
-          }
-          const float sv = ok ? sacc[i][rt][e] * a.scale : -INFINITY;
-          sacc[i][rt][e] = sv;
-          m = fmaxf(m, sv);
+    for (int rt = 0; rt < RT; ++rt) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < SW; ++u) {
+        const int sl = w + NW * u;
+        const int k0 = (st0 + sl) * 32 + 8 * lg;  // this lane's 8 keys of the step
+        f32x4 sacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+        for (int ks = 0; ks < KSD; ++ks) {
+          const uint4 qv = *(const uint4 *)&sq[rt * 16 + lr][32 * ks + 8 * lg];
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            sacc[i] = mfma16(__builtin_bit_cast(bf16x8, kf[u][i][ks]), as_bf16x8(qv), sacc[i]);
         }
-      }
-      m = fmaxf(m, __shfl_xor(m, 16, 64));
-      m = fmaxf(m, __shfl_xor(m, 32, 64));
-      if (lg == 0) redm[w][rt * 16 + lr] = m;
-    }
-    __syncthreads();
-    float lsum[4];
+        // element e of sacc[i]: key k0 + 4 i + e, row rb + 16 rt + lr
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
+        for (int j = 0; j < 8; ++j) sv[u][rt][j] = sacc[j >> 2][j & 3];
+        if (sl >= nst) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) sv[u][rt][j] = -INFINITY;
+        } else if ((st0 + sl + 1) * 32 > a.kv_len) {  // the step reaches past the prefix
+          const uint32_t vis = visible8(sanc[rt * 16 + lr], k0, a.kv_len, nkeys);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) sv[u][rt][j] = (vis >> j) & 1u ? sv[u][rt][j] : -INFINITY;
+        }
+        mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sv[u][rt][0], sv[u][rt][1]), fmaxf(sv[u][rt][2], sv[u][rt][3])),
+                             fmaxf(fmaxf(sv[u][rt][4], sv[u][rt][5]), fmaxf(sv[u][rt][6], sv[u][rt][7]))));
+      }
+      mx = max_x32(max_x16(mx));
+      if (lg == 0) smax[w][rt * 16 + lr] = mx;
+    }
+    lds_barrier();
+
+    // ---- 2. probabilities against the block max, row sums
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
       const int rr = rt * 16 + lr;
-      const float m = fmaxf(fmaxf(redm[0][rr], redm[1][rr]), fmaxf(redm[2][rr], redm[3][rr]));
-      const float mref = (m == -INFINITY) ? 0.0f : m;
-      float l = 0.0f;
+      float M = smax[0][rr];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        uint16_t pb[4];
+      for (int ww = 1; ww < NW; ++ww) M = fmaxf(M, smax[ww][rr]);
+      const float mc = (M == -INFINITY ? 0.0f : M) * c;
+      float ps = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float pv = expf(sacc[i][rt][e] - mref);  // exp(-inf) = 0 for masked keys
-          l += pv;
-          pb[e] = f2bf(pv);
+      for (int u = 0; u < SW; ++u) {
+        const int sl = w + NW * u;
+        float pv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          pv[j] = __builtin_amdgcn_exp2f(fmaf(sv[u][rt][j], c, -mc));  // exp2(-inf) = 0 when masked
+          ps += pv[j];
         }
-        uint2 st;
-        st.x = pb[0] | ((uint32_t)pb[1] << 16);
-        st.y = pb[2] | ((uint32_t)pb[3] << 16);
-        *(uint2 *)&P[rr][(2 * w + i) * 16 + 4 * lg] = st;
+        *(uint4 *)&sp[rr][32 * sl + 8 * lg] =
+            make_uint4(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                       pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7]));
       }
-      l += __shfl_xor(l, 16, 64);
-      l += __shfl_xor(l, 32, 64);
-      lsum[rt] = l;
+      ps = sum_x32(sum_x16(ps));
+      if (lg == 0) ssum[w][rr] = ps;
     }
+    lds_barrier();
+
+    // ---- 3. O^T for dimensions 16 w .. 16 w + 15 over all of the keys
+    f32x4 oacc[RT];
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
-      if (lg == 0) redl[w][rt * 16 + lr] = lsum[rt];
-    __syncthreads();  // P and redl complete
-    // ---- O^T = V^T P^T for this wave's d tiles
-    f32x4 oacc[DTW][4];
+    for (int rt = 0; rt < RT; ++rt) oacc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < DTW; ++i)
+    for (int j = 0; j < MS; ++j) {
+      if (j < nst) {
+        i32x4 vv = vf[j];
+        const int key = (st0 + j) * 32 + 8 * lg;
+        if (key + 8 > nkeys) {  // slots never written for this step: zero
+          const int valid = nkeys - key;
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt) oacc[i][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t lo = 2 * e < valid ? 0x0000ffffu : 0u;
+            const uint32_t hi = 2 * e + 1 < valid ? 0xffff0000u : 0u;
+            vv[e] &= (int)(lo | hi);
+          }
+        }
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      uint4 pbv[4];
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) pbv[rt] = *(const uint4 *)&P[rt * 16 + lr][kk * 32 + 8 * lg];
-#pragma unroll
-      for (int i = 0; i < DTW; ++i)
-#pragma unroll
-        for (int rt = 0; rt < 4; ++rt)
-          oacc[i][rt] = mfma16(as_bf16x8(va[i][kk]), as_bf16x8(pbv[rt]), oacc[i][rt]);
-    }
-    const size_t base = ((size_t)g * a.n_chunks + c) * R;
-#pragma unroll
-    for (int i = 0; i < DTW; ++i) {
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        const int r = r0 + rt * 16 + lr;
-        if (r < R) {
-          const int d0 = (w * DTW + i) * 16 + 4 * lg;
-          *(f32x4 *)&a.part_o[(base + r) * D + d0] = oacc[i][rt];
+        for (int rt = 0; rt < RT; ++rt) {
+          const uint4 pf = *(const uint4 *)&sp[rt * 16 + lr][32 * j + 8 * lg];
+          oacc[rt] = mfma16(__builtin_bit_cast(bf16x8, vv), as_bf16x8(pf), oacc[rt]);
         }
       }
+    }
+    // lane holds dimensions 16 w + 4 lg .. + 3 of row rb + 16 rt + lr
+    const size_t base = ((size_t)g * a.n_chunks + split) * R;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int r = rb + rt * 16 + lr;
+      if (r < R) *(f32x4 *)&a.part_o[(base + r) * D + 16 * w + 4 * lg] = oacc[rt];
     }
     if (threadIdx.x < RB) {
       const int rr = threadIdx.x;
-      const int r = r0 + rr;
+      const int r = rb + rr;
       if (r < R) {
-        const float m = fmaxf(fmaxf(redm[0][rr], redm[1][rr]), fmaxf(redm[2][rr], redm[3][rr]));
-        const float l = redl[0][rr] + redl[1][rr] + redl[2][rr] + redl[3][rr];
-        *(float2 *)&a.part_ml[(base + r) * 2] = make_float2(m, l);
+        float M = smax[0][rr], L = ssum[0][rr];
+#pragma unroll
+        for (int ww = 1; ww < NW; ++ww) {
+          M = fmaxf(M, smax[ww][rr]);
+          L += ssum[ww][rr];
+        }
+        // row max in units of the scaled score (s * scale)
+        *(float2 *)&a.part_ml[(base + r) * 2] = make_float2(M == -INFINITY ? M : M * a.scale, L);
       }
     }
-    __syncthreads();  // Qs, P, redm, redl free for the next row block
+    lds_barrier();  // sp, sq, sanc, smax, ssum free for the next row block
   }
 }
 
@@ -303,15 +398,39 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, uint16_t *__rest
 
 }  // namespace
 
-hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s) {
-  dim3 grid(a.n_kv, a.n_chunks);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL(k_attn<128>, grid, dim3(256), 0, s, a);
-  else if (a.head_dim == 64)
-    hipLaunchKernelGGL(k_attn<64>, grid, dim3(256), 0, s, a);
-  else
-    return hipErrorInvalidValue;
+int attn_splits(int n_kv, int head_dim, int nkeys) {
+  // at most 2 head_dim / 16 steps of 32 keys per workgroup, and about
+  // kAttnTargetGroups workgroups in all while every one has a step
+  const int steps = (nkeys + 31) / 32;
+  const int ms = 2 * (head_dim / 16);
+  int sp = (steps + ms - 1) / ms;
+  const int fill = (kAttnTargetGroups + n_kv - 1) / n_kv;
+  if (sp < fill) sp = fill < steps ? fill : steps;
+  return sp < 1 ? 1 : sp;
+}
+
+template <int D>
+hipError_t launch_attn_d(const AttnArgs &a, hipStream_t s) {
+  // row tiles per block
+  constexpr int max_rt = 4;
+  const int rows = a.n_tok * (a.n_heads / a.n_kv);
+  const int rt = rows >= 16 * max_rt ? max_rt : (rows + 15) / 16;
+  const dim3 grid(a.n_kv * a.n_chunks);
+  const dim3 block(D * 4);
+  switch (rt) {
+    case 1: hipLaunchKernelGGL((k_attn<D, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_attn<D, 2>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_attn<D, 3>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_attn<D, 4>), grid, block, 0, s, a); break;
+  }
   return hipGetLastError();
+}
+
+hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s) {
+  if (a.n_chunks != attn_splits(a.n_kv, a.head_dim, a.kv_len + a.n_tok)) return hipErrorInvalidValue;
+  if (a.head_dim == 128) return launch_attn_d<128>(a, s);
+  if (a.head_dim == 64) return launch_attn_d<64>(a, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,

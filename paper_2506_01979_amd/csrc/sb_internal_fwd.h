@@ -110,7 +110,7 @@ struct AttnArgs {
   const void *q;        // bf16 or f32 [rows][n_heads][d]
   const void *kc, *vc;  // this layer's cache [n_kv][cap][d]
   int cap, kv_len, n_tok, n_heads, n_kv, head_dim;
-  int chunk, n_chunks;
+  int n_chunks;     // key ranges per KV head (attn_splits)
   const Meta *meta;
   float scale;
   float *part_o;   // [n_kv][n_chunks][R][d]
@@ -135,7 +135,9 @@ GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok);
 hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int *split, hipStream_t s);
 
 // k_attn.hip
-constexpr int kAttnChunk = 128;
+// Key ranges per KV head: about kAttnTargetGroups workgroups in all.
+constexpr int kAttnTargetGroups = 256;
+int attn_splits(int n_kv, int head_dim, int nkeys);
 hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s);
 hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,
                                   hipStream_t s);
