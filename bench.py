@@ -31,8 +31,191 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, vendor figure
 DOMINANT = "gate_up"    # kernel class holding the most bytes per step
 
 
+COPY_BYTES = 1 << 29     # plain device copy used to scale the HBM byte counters
+PMC_STEPS = 3            # timed steps of a counter run (--steps 3)
+CPU_REPEATS = 2          # whole CPU oracle steps timed (about 15 s on 16 cores)
+WORKLOAD = "llama7b_b4k8_p2048"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", f"traffic_gate_up_{WORKLOAD}.md")
+# sources the dominant GEMM kernel is built from (its byte counters are
+# stale once any of them changes)
+GEMM_SOURCES = ("paper_2506_01979_amd/csrc/k_gemm.hip", "paper_2506_01979_amd/csrc/sb_device.h",
+                "paper_2506_01979_amd/csrc/sb_internal_fwd.h")
+# kernels of one verify step, in launch order: embed, 8 per layer, final
+# norm, LM head, stats; the gate/up GEMM is the 7th kernel of a layer
+PER_LAYER = ("norm", "qkv", "attn", "attn_merge", "o", "norm", "gate_up", "down")
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def gemm_source_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {d}")
+    per = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            key = int(r["Dispatch_Id"])
+            e = per.setdefault(key, {"name": r["Kernel_Name"], "values": {}})
+            e["values"][r["Counter_Name"]] = e["values"].get(r["Counter_Name"], 0.0) + \
+                float(r["Counter_Value"])
+    return [per[k] for k in sorted(per)]
+
+
+def _gate_up_dispatches(rows, n_layers, last):
+    """Dispatch records of the gate/up GEMM in the last `last` complete verify
+    steps (the timed ones; earlier steps generate the drafts on partial
+    trees)."""
+    out = []
+    for i, r in enumerate(rows):
+        if "k_embed_meta" not in r["name"]:
+            continue
+        step = rows[i:i + 1 + len(PER_LAYER) * n_layers + 3]
+        if len(step) < 1 + len(PER_LAYER) * n_layers + 3 or "k_softmax_stats" not in step[-1]["name"]:
+            continue
+        for l in range(n_layers):
+            g = step[1 + len(PER_LAYER) * l + PER_LAYER.index("gate_up")]
+            if "k_gemm" not in g["name"]:
+                raise RuntimeError(f"unexpected kernel order: {g['name']}")
+            out.append(g)
+    return out[-last * n_layers:]
+
+
+def pmc_summary(fetch_dir: str, write_dir: str) -> str:
+    """Markdown summary of two rocprofv3 --pmc runs of
+    `bench.py --copy-calibration` (FETCH_SIZE, then WRITE_SIZE): HBM bytes
+    per gate/up launch, each counter scaled by what it reads for the final
+    device copy of COPY_BYTES bytes."""
+    from paper_2506_01979_amd import synth
+    shape = synth.WORKLOADS[WORKLOAD].shape
+    res = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _counter_rows(d)
+        gu = _gate_up_dispatches(rows, shape.n_layers, PMC_STEPS)
+        copy = rows[-1]
+        kib = sum(g["values"][counter] for g in gu) / len(gu)
+        copy_kib = copy["values"][counter]
+        res[counter] = {"kib_per_launch": kib, "launches": len(gu), "copy_kernel": copy["name"],
+                        "copy_kib": copy_kib, "scale": COPY_BYTES / (copy_kib * 1024.0),
+                        "kernel": gu[0]["name"]}
+    f, w = res["FETCH_SIZE"], res["WRITE_SIZE"]
+    fetch_b = f["kib_per_launch"] * 1024.0 * f["scale"]
+    write_b = w["kib_per_launch"] * 1024.0 * w["scale"]
+    nb = algorithmic_bytes(shape, synth.WORKLOADS[WORKLOAD].kv_len, synth.WORKLOADS[WORKLOAD].n_rows)
+    rec = {"workload": WORKLOAD, "kernel": f["kernel"], "launches": f["launches"],
+           "fetch_kib_per_launch": round(f["kib_per_launch"], 1),
+           "write_kib_per_launch": round(w["kib_per_launch"], 1),
+           "copy_bytes": COPY_BYTES, "copy_kernel": f["copy_kernel"],
+           "copy_fetch_kib": round(f["copy_kib"], 1), "copy_write_kib": round(w["copy_kib"], 1),
+           "fetch_scale": round(f["scale"], 4), "write_scale": round(w["scale"], 4),
+           "traffic_bytes": int(fetch_b + write_b),
+           "algorithmic_bytes": nb["gate_up_launch"],
+           "gemm_source_sha256": gemm_source_sha()}
+    cmd = ("cd /tmp && export TMPDIR=/tmp && "
+           "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <repo>/gpurun_out/pmc_fetch -o run -- "
+           "python3 <repo>/bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-alpha-sweep "
+           "--copy-calibration; the same with --pmc WRITE_SIZE into gpurun_out/pmc_write; then "
+           "python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write")
+    return "\n".join([
+        f"# HBM traffic of the gate/up GEMM launch, {WORKLOAD}",
+        "",
+        f"Command: `{cmd}`",
+        "",
+        f"- kernel: `{f['kernel']}`, {f['launches']} launches (every layer of the last {PMC_STEPS} "
+        f"timed steps)",
+        f"- FETCH_SIZE {f['kib_per_launch']:.1f} KiB/launch, scale {f['scale']:.4f} "
+        f"(copy of {COPY_BYTES} B reads {f['copy_kib']:.1f} KiB, `{f['copy_kernel']}`)",
+        f"- WRITE_SIZE {w['kib_per_launch']:.1f} KiB/launch, scale {w['scale']:.4f} "
+        f"(same copy writes {w['copy_kib']:.1f} KiB)",
+        f"- traffic {(fetch_b + write_b) / 1e6:.2f} MB/launch vs algorithmic "
+        f"{nb['gate_up_launch'] / 1e6:.2f} MB/launch",
+        "",
+        json.dumps(rec),
+        ""])
+
+
+def measured_traffic():
+    """HBM bytes per dominant launch from the committed counter summary, or
+    None when there is none or the kernel sources changed since."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            line = [l for l in fh if l.startswith("{")][-1]
+        rec = json.loads(line)
+    except (OSError, IndexError, ValueError):
+        return None
+    if rec.get("gemm_source_sha256") != gemm_source_sha():
+        return None
+    return rec["traffic_bytes"]
+
+
+def trace_summary(trace_dir: str) -> str:
+    """Markdown per-kernel summary of a rocprofv3 --kernel-trace --stats run
+    of bench.py: the whole-run stats table, then the kernels of the last 5
+    complete verify steps in launch order."""
+    import csv
+    import glob
+    from paper_2506_01979_amd import synth
+    shape = synth.WORKLOADS[WORKLOAD].shape
+    stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)[0]
+    trace = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
+    rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
+    starts = [i for i, r in enumerate(rows) if "k_embed_meta" in r["Kernel_Name"]]
+    n_k = 1 + len(PER_LAYER) * shape.n_layers + 3
+    steps = [i for i in starts if i + n_k <= len(rows) and
+             "k_softmax_stats" in rows[i + n_k - 1]["Kernel_Name"]][-5:]
+    cls = ["embed"] + list(PER_LAYER) * shape.n_layers + ["norm", "lm_head", "stats"]
+    # the bench step goes on with the accept walk and the rollback
+    tail = [c for c in ("k_walk", "k_rollback")]
+    n_s = n_k
+    if steps and all(steps[-1] + n_k + j < len(rows) and tail[j] in rows[steps[-1] + n_k + j]["Kernel_Name"]
+                     for j in range(len(tail))):
+        n_s = n_k + len(tail)
+        cls = cls + ["accept_walk", "rollback"]
+    agg, span = {}, []
+    for i in steps:
+        span.append((int(rows[i + n_s - 1]["End_Timestamp"]) - int(rows[i]["Start_Timestamp"])) / 1e3)
+        for j in range(n_s):
+            r = rows[i + j]
+            d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            a = agg.setdefault(cls[j], {"name": set(), "us": []})
+            a["name"].add(r["Kernel_Name"].replace("sb::(anonymous namespace)::", ""))
+            a["us"].append(d)
+    out = [f"# Kernel trace of the verify step, {WORKLOAD}", "",
+           "Command: `cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
+           "--output-format csv -d <repo>/gpurun_out/prof_step -o run -- python3 <repo>/bench.py "
+           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep`, then "
+           "`python3 bench.py --trace-summary gpurun_out/prof_step`", "",
+           f"Last {len(steps)} complete steps (embed .. stats, then the accept walk and the rollback "
+           f"when traced): span "
+           + ", ".join(f"{x:.1f}" for x in span) + " us", "",
+           "| class | kernel | launches/step | avg us | min us | us/step |",
+           "|---|---|---|---|---|---|"]
+    tot = 0.0
+    for c, a in sorted(agg.items(), key=lambda kv: -sum(kv[1]["us"])):
+        per = sum(a["us"]) / len(steps)
+        tot += per
+        out.append(f"| {c} | `{', '.join(sorted(a['name']))}` | {len(a['us']) // len(steps)} | "
+                   f"{sum(a['us']) / len(a['us']):.2f} | {min(a['us']):.2f} | {per:.1f} |")
+    out += [f"| total | | | | | {tot:.1f} |", "", "Whole-run `--stats` (all launches, incl. "
+            "draft generation and warmup):", "", "| kernel | calls | avg us | min us | max us | % |",
+            "|---|---|---|---|---|---|"]
+    for r in list(csv.DictReader(open(stats)))[:16]:
+        out.append(f"| `{r['Name'].replace('sb::(anonymous namespace)::', '')[:70]}` | {r['Calls']} | "
+                   f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                   f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    return "\n".join(out) + "\n"
 
 
 def algorithmic_bytes(shape, P_kv: int, n: int) -> dict:
@@ -95,10 +278,28 @@ def make_drafts(api, synth, m, k_, v_, kv_len, root_tok, B, kd, alpha, q_temp, s
     return tokens, q
 
 
+class _PerLayer:
+    """Read-only sequence whose items are built when indexed (the oracle walks
+    the layers in order, so one layer's float32 copy is alive at a time)."""
+
+    def __init__(self, n, make):
+        self.n, self.make = n, make
+
+    def __len__(self):
+        return self.n
+
+    def __getitem__(self, i):
+        if not 0 <= i < self.n:
+            raise IndexError(i)
+        return self.make(i)
+
+
 def cpu_baseline(shape, host_bits, kv_host, kv_len, inp, n_layers_sample: int) -> dict:
-    """The oracle as it stands, on the host cores: a bf16-emulation forward of
-    the first layers of the same model (plus embedding, final norm and LM
-    head) and the accept walk, extrapolated to the full depth per layer."""
+    """The oracle as it stands, on the host cores: its bf16-emulation forward
+    of the same model on the same inputs (embedding, n_layers_sample decoder
+    layers, final norm, LM head) and its accept walk.  With every layer
+    sampled (the default) this is one whole verify step; with fewer, the
+    per-layer time is extrapolated to the full depth."""
     from oracle import decoder, sampling
     from paper_2506_01979_amd import synth
 
@@ -108,43 +309,56 @@ def cpu_baseline(shape, host_bits, kv_host, kv_len, inp, n_layers_sample: int) -
     except Exception:  # pragma: no cover
         cores = len(os.sched_getaffinity(0))
 
-    def weights(nl):
-        d = {"embed": synth.bits_to_f32(host_bits[("embed", None)]),
-             "lm_head": synth.bits_to_f32(host_bits[("lm_head", None)]),
-             "final_norm": synth.norm_gain(shape), "layers": []}
-        for l in range(nl):
-            lw = {n: synth.bits_to_f32(host_bits[(n, l)]) for n in synth.LAYER_MATS}
-            lw["attn_norm"] = synth.norm_gain(shape)
-            lw["mlp_norm"] = synth.norm_gain(shape)
-            d["layers"].append(lw)
-        return d
+    def layer(l):
+        lw = {n: synth.bits_to_f32(host_bits[(n, l)]) for n in synth.LAYER_MATS}
+        lw["attn_norm"] = synth.norm_gain(shape)
+        lw["mlp_norm"] = synth.norm_gain(shape)
+        return lw
 
-    Kp = [synth.bits_to_f32(kv_host[l][0]) for l in range(n_layers_sample)]
-    Vp = [synth.bits_to_f32(kv_host[l][1]) for l in range(n_layers_sample)]
+    def weights(nl):
+        return {"embed": synth.bits_to_f32(host_bits[("embed", None)]),
+                "lm_head": synth.bits_to_f32(host_bits[("lm_head", None)]),
+                "final_norm": synth.norm_gain(shape), "layers": _PerLayer(nl, layer)}
+
+    Kp = _PerLayer(n_layers_sample, lambda l: synth.bits_to_f32(kv_host[l][0]))
+    Vp = _PerLayer(n_layers_sample, lambda l: synth.bits_to_f32(kv_host[l][1]))
+    full = n_layers_sample >= shape.n_layers
+    reps = CPU_REPEATS if full else 1
     times = {}
-    for nl in (0, n_layers_sample):
+    for nl in ((n_layers_sample,) if full else (0, n_layers_sample)):
         sh = shape.with_layers(nl)   # 0 layers: embedding, final norm, LM head only
         W = weights(nl)
-        t0 = time.perf_counter()
-        lg, _, _ = decoder.tree_forward(sh, W, Kp, Vp, kv_len, inp["tokens"], inp["parents"],
-                                        "bf16")
-        t1 = time.perf_counter()
-        r = sampling.accept_resample(inp["tokens"], inp["parents"], lg.astype(np.float32), 1.0,
+        fwd = walk = 0.0
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            lg, _, _ = decoder.tree_forward(sh, W, Kp, Vp, kv_len, inp["tokens"], inp["parents"],
+                                            "bf16")
+            t1 = time.perf_counter()
+            sampling.accept_resample(inp["tokens"], inp["parents"], lg.astype(np.float32), 1.0,
                                      inp["q"], inp["u"])
-        t2 = time.perf_counter()
-        times[nl] = (t1 - t0, t2 - t1)
+            t2 = time.perf_counter()
+            fwd += (t1 - t0) / reps
+            walk += (t2 - t1) / reps
+        times[nl] = (fwd, walk)
         del W
-    head, walk = times[0]
-    per_layer = max(0.0, times[n_layers_sample][0] - head) / n_layers_sample
-    step_s = head + walk + per_layer * shape.n_layers
     n_draft = len(inp["parents"]) - 1
+    if full:
+        fwd, walk = times[n_layers_sample]
+        step_s = fwd + walk
+        sample = (f"{reps} whole verify steps on the host, averaged: the oracle's bf16-emulation "
+                  f"forward of all {shape.n_layers} layers (+ embedding, final norm, LM head) "
+                  f"{fwd:.2f}s and its accept walk {walk:.3f}s per step, same weights, prefix KV, "
+                  f"tree, q and u as the GPU step")
+    else:
+        head, walk = times[0]
+        per_layer = max(0.0, times[n_layers_sample][0] - head) / n_layers_sample
+        step_s = head + walk + per_layer * shape.n_layers
+        sample = (f"oracle bf16-emulation forward of layers 0..{n_layers_sample - 1} of "
+                  f"{shape.n_layers} (+ embedding, final norm, LM head) and the accept walk "
+                  f"on the same inputs; step time = head {head:.2f}s + walk {walk:.3f}s + "
+                  f"{shape.n_layers} x per-layer {per_layer:.2f}s")
     return {"value": n_draft / step_s, "unit": "verified tokens/s", "cores": int(cores),
-            "kind": "oracle",
-            "sample": (f"oracle bf16-emulation forward of layers 0..{n_layers_sample - 1} of "
-                       f"{shape.n_layers} (+ embedding, final norm, LM head) and the accept walk "
-                       f"on the same inputs; step time = head {head:.2f}s + walk {walk:.3f}s + "
-                       f"{shape.n_layers} x per-layer {per_layer:.2f}s"),
-            "step_s": step_s}
+            "kind": "oracle", "sample": sample, "step_s": step_s}
 
 
 def main():
@@ -152,12 +366,25 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llama7b_b4k8_p2048")
+    ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--alpha", type=float, default=0.6)
-    ap.add_argument("--cpu-layers", type=int, default=4)
+    ap.add_argument("--cpu-layers", type=int, default=0,
+                    help="decoder layers the CPU oracle runs (0: all of them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-alpha-sweep", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="end with a device copy of known size (for rocprofv3 --pmc runs)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs of this script and exit")
+    ap.add_argument("--trace-summary", metavar="TRACE_DIR",
+                    help="summarise a rocprofv3 --kernel-trace --stats run of this script and exit")
     args = ap.parse_args()
+    if args.pmc_summary:
+        print(pmc_summary(*args.pmc_summary))
+        return
+    if args.trace_summary:
+        print(trace_summary(args.trace_summary))
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}), flush=True)
@@ -169,6 +396,8 @@ def main():
 
     w = synth.WORKLOADS[args.workload]
     shape = w.shape
+    if args.cpu_layers <= 0 or args.cpu_layers > shape.n_layers:
+        args.cpu_layers = shape.n_layers
     B, kd, P = w.branches, w.depth, w.prefix
     kv_len, n = w.kv_len, w.n_rows
     torch.cuda.set_device(0)
@@ -216,9 +445,15 @@ def main():
     res = api.new_result(dev)
     stream = torch.cuda.current_stream()
 
+    new_len = torch.zeros(1, dtype=torch.int32, device=dev)
+
     def step():
+        # a0-a8: tree metadata ... LM head + stats, the accept walk, and the
+        # rollback that compacts the kept path behind the prefix (it moves
+        # tree slots only, which the next step's forward rewrites)
         m.sb_verify_forward(k_, v_, kv_len, d_tok, parents, 1.0, logits, stats, ws, stream)
         api.sb_accept_resample(d_tok, parents, logits, stats, 1.0, d_q, d_u, res, sws, stream)
+        m.sb_kv_rollback(k_, v_, kv_len, res, new_len, stream)
 
     for _ in range(args.warmup):
         step()
@@ -246,14 +481,18 @@ def main():
     torch.cuda.synchronize()
     clean_ms = ev0.elapsed_time(ev1) / args.steps
 
-    # rollback, timed on its own
-    new_len = torch.zeros(1, dtype=torch.int32, device=dev)
-    ev0.record(stream)
-    m.sb_kv_rollback(k_, v_, kv_len, res, new_len, stream)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    rollback_ms = ev0.elapsed_time(ev1)
     r = api.decode_result(res)
+    if int(new_len.item()) != kv_len + 1 + r["n_accepted"]:
+        raise RuntimeError("rollback length does not match the accepted path")
+
+    if args.copy_calibration:
+        # a plain device copy of known size, for scaling the HBM byte counters
+        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     nbytes = algorithmic_bytes(shape, kv_len, n)
     k_avg_ms = k_ms / max(1, k_launches)
@@ -278,13 +517,12 @@ def main():
                    "depth": kd, "alpha": args.alpha},
         "roofline": {"bound": "hbm", "kernel": f"k_gemm (gate/up + SwiGLU), {k_launches} launches",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "avg_us": round(k_avg_ms * 1e3, 2)},
         "step_hbm": {"bytes": nbytes["step"],
                      "achieved_gbs": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9, 1),
                      "frac": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "ms_per_step_without_kernel_events": round(clean_ms, 4)},
-        "rollback_ms": round(rollback_ms, 4),
         "accepted": r["n_accepted"],
     }
 
