@@ -1,0 +1,235 @@
+"""Parity at the full sizes of the target shapes (GPU path vs the oracle).
+
+* 7B shape, the benchmarked step itself (32 layers, B=4 x k=8 = 33 rows,
+  prefix 2048, seeded N(0,1) prefix KV): every logit of the GPU forward
+  against the oracle's bf16-emulation forward of the whole model, the tree
+  K/V of the first and last layers, the softmax statistics, the accept walk
+  (bit-exact against the oracle walk run on the GPU's own logits, outside
+  1e-6 of a decision threshold) and the rollback.
+* The 7B, 13B and 70B shapes at full width, sliced to their first 2 decoder
+  layers, with the bf16 bound of 2e-2: 7B at the step's own tree; 13B with
+  prefixes 512 and 8192 and trees 1x4 and 8x16 (129 rows); 70B with grouped
+  queries 64/8 (264 query rows per KV head), vocabulary 128256, prefix 4096
+  and 4x8.  The slices run the same kernels at the same widths, tile counts
+  and vocabulary sizes as the full models.
+
+Why the whole 32-layer step has its own bound: this seeded N(0, 0.02) model
+amplifies float32-level differences through its depth.  Measured with the
+oracle alone on the 7B step: accumulating its GEMMs in float64 (then
+rounding to float32) moves the logits by 2.2e-2 (max row-relative), and
+perturbing every RMSNorm input by 6e-8 relative noise moves them by 1.6e-2.
+Two correct bf16 implementations therefore differ by about 2e-2 at this
+depth from summation order alone, so the 2e-2 bound is held per layer (the
+2-layer slices) and the full depth is held to FULL_DEPTH_TOL = 5e-2, about
+2.3 times the oracle's own summation-order spread.  The GPU path's largest
+single departure from the oracle is that it rounds the attention
+probabilities to bf16 for the matrix-core P.V product (the oracle keeps them
+float32); that alone accounts for 3.7e-2 at full depth in the same
+measurement.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import decision_margin, row_relerr, say
+from oracle import decoder, sampling
+from paper_2506_01979_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL_BF16 = 2e-2
+FULL_DEPTH_TOL = 5e-2
+TIE = 1e-6
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2506_01979_amd import api as A
+    assert torch.cuda.is_available()
+    return A
+
+
+class PerLayer:
+    """Read-only per-layer sequence built on access (one layer's float32
+    copy alive at a time while the oracle walks the layers)."""
+
+    def __init__(self, n, make):
+        self.n, self.make = n, make
+
+    def __len__(self):
+        return self.n
+
+    def __getitem__(self, i):
+        if not 0 <= i < self.n:
+            raise IndexError(i)
+        return self.make(i)
+
+
+def build(api, shape):
+    """GPU model with seeded weights; returns (model, bits) where bits keeps
+    the bf16 bit patterns for the oracle."""
+    bits = {}
+
+    def tensor_fn(name, layer=None):
+        if name.endswith("norm"):
+            return synth.norm_gain(shape)
+        b = synth.weight(shape, name, layer, 0, as_bits=True)
+        bits[(name, layer)] = b
+        return b
+
+    return api.Model(shape, tensor_fn), bits
+
+
+def oracle_weights(shape, bits):
+    def layer(l):
+        lw = {n: synth.bits_to_f32(bits[(n, l)]) for n in synth.LAYER_MATS}
+        lw["attn_norm"] = synth.norm_gain(shape)
+        lw["mlp_norm"] = synth.norm_gain(shape)
+        return lw
+    return {"embed": synth.bits_to_f32(bits[("embed", None)]),
+            "lm_head": synth.bits_to_f32(bits[("lm_head", None)]),
+            "final_norm": synth.norm_gain(shape),
+            "layers": PerLayer(shape.n_layers, layer)}
+
+
+def run_case(api, m, bits, shape, prefix, B, k, seed, tol=TOL_BF16, check_walk=True):
+    L = shape.n_layers
+    kv_len = prefix - 1
+    parents = synth.branch_parents(B, k)
+    n = len(parents)
+    ptoks = synth.prefix_tokens(shape.vocab, prefix, seed)
+    root_children = np.nonzero(parents == 0)[0]
+    q = synth.draft_q(n, shape.vocab, 0.7, seed, root_children)
+    toks = synth.draw_tokens(q, seed)
+    toks[0] = ptoks[-1]
+
+    cap = kv_len + n + 8
+    kc, vc = m.new_kv(cap)
+    kv_bits = []
+    for l in range(L):
+        kb = synth.synthetic_kv(shape, l, kv_len, kv_len, 0, as_bits=True)
+        vb = synth.synthetic_kv(shape, l, kv_len, kv_len, 1, as_bits=True)
+        kc[l, :, :kv_len] = torch.from_numpy(kb.view(np.int16)).view(torch.bfloat16).cuda()
+        vc[l, :, :, :kv_len] = torch.from_numpy(vb.view(np.int16)).view(torch.bfloat16).cuda() \
+            .transpose(1, 2)
+        kv_bits.append((kb, vb))
+
+    say(f"full-size forward {shape.name} layers={L} prefix={prefix} tree={B}x{k} rows={n}")
+    logits = torch.empty((n, shape.vocab), dtype=torch.float32, device="cuda")
+    stats = api.new_stats(n)
+    ws = m.workspace(n, kv_len)
+    d_tok = torch.from_numpy(toks.astype(np.int32)).cuda()
+    m.sb_verify_forward(kc, vc, kv_len, d_tok, parents, 1.0, logits, stats, ws)
+    torch.cuda.synchronize()
+    lg = logits.cpu().numpy()
+    st = api.decode_stats(stats)
+    tree_k, tree_v = {}, {}
+    for l in sorted({0, L - 1}):
+        tree_k[l] = kc[l, :, kv_len:kv_len + n].float().cpu().numpy()
+        tree_v[l] = vc[l, :, :, kv_len:kv_len + n].float().transpose(1, 2).cpu().numpy()
+
+    say(f"  oracle forward {shape.name} (host)")
+    W = oracle_weights(shape, bits)
+    Kp = PerLayer(L, lambda l: synth.bits_to_f32(kv_bits[l][0]))
+    Vp = PerLayer(L, lambda l: synth.bits_to_f32(kv_bits[l][1]))
+    ref, k_tree, v_tree = decoder.tree_forward(shape, W, Kp, Vp, kv_len, toks, parents, "bf16")
+    err = row_relerr(lg, ref)
+    say(f"  logits row-relative error {err:.3e} (bound {tol:.0e})")
+    assert err < tol
+    for l in tree_k:
+        ek = row_relerr(tree_k[l].reshape(-1, shape.head_dim), k_tree[l].reshape(-1, shape.head_dim))
+        ev = row_relerr(tree_v[l].reshape(-1, shape.head_dim), v_tree[l].reshape(-1, shape.head_dim))
+        say(f"  layer {l} tree K err {ek:.3e} V err {ev:.3e}")
+        # layer 0's K/V depend on no earlier layer: the per-layer bound
+        lt = TOL_BF16 if l == 0 else tol
+        assert ek < 5 * lt and ev < 5 * lt
+
+    # softmax statistics of the GPU's own logits
+    for i in range(n):
+        rs = sampling.row_stats(lg[i], 1.0)
+        assert st[i]["argmax"] == rs.argmax
+        assert st[i]["zmax"] == np.float32(rs.zmax)
+        assert abs(st[i]["total"] - rs.total) <= 1e-6 * rs.total
+
+    if not check_walk:
+        return
+    # the walk on the GPU's own logits, several uniform seeds
+    sws = torch.empty(api.sb_sample_workspace_bytes(shape.vocab), dtype=torch.uint8,
+                      device="cuda")
+    res = api.new_result()
+    d_q = torch.from_numpy(q).cuda()
+    checked, last = 0, None
+    for su in range(1, 6):
+        u = synth.uniforms(n, su)
+        tr = []
+        want = sampling.accept_resample(toks, parents, lg, 1.0, q, u, trace=tr)
+        say(f"  walk {shape.name} uniforms seed {su}")
+        api.sb_accept_resample(d_tok, parents, logits, stats, 1.0, d_q,
+                               torch.from_numpy(u).cuda(), res, sws)
+        got = api.decode_result(res)
+        if decision_margin(tr, u) < TIE:
+            continue
+        assert got["path"] == want.path
+        assert got["n_accepted"] == want.n_accepted
+        assert got["branch"] == want.branch
+        assert got["next_token"] == want.next_token
+        assert got["flags"] == want.flags
+        assert bool(got["bonus"]) == want.bonus
+        checked += 1
+        last, last_u = got, u
+    assert checked >= 3
+
+    # rollback of the last checked walk (run again so the device result is
+    # that walk's): the kept path's slots move behind the prefix
+    say(f"  rollback {shape.name}")
+    api.sb_accept_resample(d_tok, parents, logits, stats, 1.0, d_q,
+                           torch.from_numpy(last_u).cuda(), res, sws)
+    assert api.decode_result(res) == last
+    new_len = torch.zeros(1, dtype=torch.int32, device="cuda")
+    m.sb_kv_rollback(kc, vc, kv_len, res, new_len)
+    torch.cuda.synchronize()
+    assert int(new_len.item()) == kv_len + 1 + last["n_accepted"]
+    for l in tree_k:
+        kg = kc[l, :, kv_len:kv_len + len(last["path"])].float().cpu().numpy()
+        vg = vc[l, :, :, kv_len:kv_len + len(last["path"])].float().transpose(1, 2).cpu().numpy()
+        for i, row in enumerate(last["path"]):
+            assert np.array_equal(kg[:, i], tree_k[l][:, row])
+            assert np.array_equal(vg[:, i], tree_v[l][:, row])
+    # the prefix is untouched
+    kp = kc[0, :, :kv_len].float().cpu().numpy()
+    assert np.array_equal(kp, synth.bits_to_f32(kv_bits[0][0]))
+
+
+@pytest.mark.timeout(900)
+def test_llama7b_full_step(api):
+    w = synth.WORKLOADS["llama7b_b4k8_p2048"]
+    shape = w.shape
+    say("full-size 7B: generating and packing weights")
+    m, bits = build(api, shape)
+    run_case(api, m, bits, shape, w.prefix, w.branches, w.depth, seed=2, tol=FULL_DEPTH_TOL)
+
+
+@pytest.mark.timeout(600)
+def test_llama7b_two_layers(api):
+    w = synth.WORKLOADS["llama7b_b4k8_p2048"]
+    shape = w.shape.with_layers(2)
+    say("full-width 7B slice: the step's tree and prefix, first 2 layers")
+    m, bits = build(api, shape)
+    run_case(api, m, bits, shape, w.prefix, w.branches, w.depth, seed=2)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("prefix,B,k", [(512, 1, 4), (8192, 8, 16)])
+def test_llama13b_two_layers(api, prefix, B, k):
+    shape = synth.SHAPES["llama13b"].with_layers(2)
+    say(f"full-width 13B slice: prefix {prefix}, tree {B}x{k}")
+    m, bits = build(api, shape)
+    run_case(api, m, bits, shape, prefix, B, k, seed=3)
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_two_layers(api):
+    shape = synth.SHAPES["llama70b"].with_layers(2)
+    say("full-width 70B slice: GQA 64/8, vocabulary 128256, prefix 4096, tree 4x8")
+    m, bits = build(api, shape)
+    run_case(api, m, bits, shape, 4096, 4, 8, seed=4)
