@@ -132,39 +132,14 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
   // exp(x * scale) = exp2(x * c): one FMA per score before the exp2
   const float c = a.scale * 1.44269504088896340736f;
 
-  // ---- the workgroup's cache reads, once, into registers.  Lanes whose
-  // slot is >= nkeys (or past the workgroup's steps) get an offset past the
-  // end of the head's buffer and read zero.
-  // K: the wave's steps w + NW u; row rho of key tile i is key
-  // 8 (rho / 4) + 4 i + rho % 4
-  i32x4 kf[SW][2][KSD];
-#pragma unroll
-  for (int u = 0; u < SW; ++u) {
-    const int sl = w + NW * u;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int slot = (st0 + sl) * 32 + 8 * (lr >> 2) + 4 * i + (lr & 3);
-      const int vo = (sl < nst && slot < nkeys) ? (slot * D + 8 * lg) * 2 : kbytes;
-#pragma unroll
-      for (int ks = 0; ks < KSD; ++ks)
-        kf[u][i][ks] = __builtin_amdgcn_raw_buffer_load_b128(krs, vo, ks * 64, 0);
-    }
-  }
-  // V^T: dimensions 16 w + lr, keys 8 lg .. 8 lg + 7 of every step j
-  i32x4 vf[MS];
-#pragma unroll
-  for (int j = 0; j < MS; ++j) {
-    const int key = (st0 + j) * 32 + 8 * lg;
-    const int vo = (j < nst && key < nkeys) ? ((16 * w + lr) * a.cap + key) * 2 : vbytes;
-    vf[j] = __builtin_amdgcn_raw_buffer_load_b128(vrs, vo, 0, 0);
-  }
-
-  for (int rb = 0; rb < R; rb += RB) {
-    // ---- stage the block's query rows and ancestor masks
-    constexpr int QPT = (RB * (D / 8) + NT - 1) / NT;
-    constexpr int APT = (RB * 8 + NT - 1) / NT;
-    i32x4 qst[QPT];
-    int ast[APT];
+  // The staging loads of a row block (query rows, ancestor masks) go out
+  // before the cache reads: in-order completion lets the staging wait cover
+  // only them, and scoring (which needs K) starts while V is still arriving.
+  constexpr int QPT = (RB * (D / 8) + NT - 1) / NT;
+  constexpr int APT = (RB * 8 + NT - 1) / NT;
+  i32x4 qst[QPT];
+  int ast[APT];
+  auto stage_loads = [&](int rb) {
 #pragma unroll
     for (int j = 0; j < QPT; ++j) {
       const int idx = threadIdx.x + j * NT;
@@ -183,6 +158,42 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
       const int vo = (rr < RB && r < R) ? (t * 8 + wd) * 4 : abytes;
       ast[j] = __builtin_amdgcn_raw_buffer_load_b32(ars, vo, 0, 0);
     }
+  };
+  stage_loads(0);
+  __builtin_amdgcn_sched_barrier(0);  // issue order: staging, K, V
+
+  // ---- the workgroup's cache reads, once, into registers.  Lanes whose
+  // slot is >= nkeys (or past the workgroup's steps) get an offset past the
+  // end of the head's buffer and read zero.
+  // K: the wave's steps w + NW u; row rho of key tile i is key
+  // 8 (rho / 4) + 4 i + rho % 4
+  i32x4 kf[SW][2][KSD];
+#pragma unroll
+  for (int u = 0; u < SW; ++u) {
+    const int sl = w + NW * u;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int slot = (st0 + sl) * 32 + 8 * (lr >> 2) + 4 * i + (lr & 3);
+      const int vo = (sl < nst && slot < nkeys) ? (slot * D + 8 * lg) * 2 : kbytes;
+#pragma unroll
+      for (int ks = 0; ks < KSD; ++ks)
+        kf[u][i][ks] = __builtin_amdgcn_raw_buffer_load_b128(krs, vo, ks * 64, 0);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  // V^T: dimensions 16 w + lr, keys 8 lg .. 8 lg + 7 of every step j
+  i32x4 vf[MS];
+#pragma unroll
+  for (int j = 0; j < MS; ++j) {
+    const int key = (st0 + j) * 32 + 8 * lg;
+    const int vo = (j < nst && key < nkeys) ? ((16 * w + lr) * a.cap + key) * 2 : vbytes;
+    vf[j] = __builtin_amdgcn_raw_buffer_load_b128(vrs, vo, 0, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // one block of query rows (its staging loads already issued)
+  auto row_block = [&](int rb) {
+    // ---- stage the block's query rows and ancestor masks
 #pragma unroll
     for (int j = 0; j < QPT; ++j) {
       const int idx = threadIdx.x + j * NT;
@@ -306,18 +317,28 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
       }
     }
     lds_barrier();  // sp, sq, sanc, smax, ssum free for the next row block
+  };
+  // the first block straight after the cache reads (no loop around it, so
+  // the cache registers are not loop-carried and only the staging loads are
+  // waited for before scoring starts)
+  row_block(0);
+  for (int rb = RB; rb < R; rb += RB) {
+    stage_loads(rb);
+    row_block(rb);
   }
 }
 
-// Combines the chunks of one (row t, query head) and writes the attention
-// output in the packed operand layout of the O projection.  The 256 threads
-// form 4 chunk groups x 64 column lanes: the chunk weights exp(m_c - M) are
-// computed once into LDS, each group sums its chunks with independent loads,
-// and the groups are added in LDS.
+// Combines the key ranges of one (row t, query head) and writes the
+// attention output in the packed operand layout of the O projection.  The
+// 256 threads form 4 range groups x 64 column lanes.  The partial outputs of
+// the first 4 ranges of every group are loaded together with the row
+// statistics, before any wait (one memory round trip for up to 16 ranges);
+// the range weights exp(m_c - M) go through LDS; the groups are added in LDS.
 template <int D>
 __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, uint16_t *__restrict__ out, int ks) {
   constexpr int DPT = D / 64;  // columns per lane
   constexpr int MAXC = 512;
+  constexpr int PK = 4;        // ranges per group loaded up front
   __shared__ float sw[MAXC];
   __shared__ float red[8];
   __shared__ float acc[4][D];
@@ -327,49 +348,57 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, uint16_t *__rest
   const int R = a.n_tok * G;
   const int r = t * G + (head - g * G);
   const int nc = a.n_chunks;
+  const int cg = threadIdx.x >> 6, lt = threadIdx.x & 63;
   const float2 *ml = (const float2 *)a.part_ml + (size_t)g * nc * R + r;
-  float m = -INFINITY;
-  for (int cc = threadIdx.x; cc < nc; cc += 256) {
-    const float mv = ml[(size_t)cc * R].x;
-    sw[cc] = mv;
-    m = fmaxf(m, mv);
+  const float *po = a.part_o + ((size_t)g * nc * R + r) * D + lt * DPT;
+  const size_t cstride = (size_t)R * D;
+  // ---- every load first: this thread's range statistics, its group's
+  // first PK partial outputs
+  float2 mlv = make_float2(-INFINITY, 0.0f);
+  if ((int)threadIdx.x < nc) mlv = ml[(size_t)threadIdx.x * R];
+  float v[PK][DPT];
+#pragma unroll
+  for (int k = 0; k < PK; ++k) {
+    const int cc = cg + 4 * k;
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) v[k][e] = cc < nc ? po[(size_t)cc * cstride + e] : 0.0f;
   }
+  float m = mlv.x;
+  for (int cc = threadIdx.x + 256; cc < nc; cc += 256) m = fmaxf(m, ml[(size_t)cc * R].x);
   for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
   __syncthreads();
   const float M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   float l = 0.0f;
-  for (int cc = threadIdx.x; cc < nc; cc += 256) {
-    const float mv = sw[cc];
-    const float wgt = mv == -INFINITY ? 0.0f : expf(mv - M);
+  if ((int)threadIdx.x < nc) {
+    const float wgt = mlv.x == -INFINITY ? 0.0f : expf(mlv.x - M);
+    sw[threadIdx.x] = wgt;
+    l = wgt * mlv.y;
+  }
+  for (int cc = threadIdx.x + 256; cc < nc; cc += 256) {
+    const float2 x = ml[(size_t)cc * R];
+    const float wgt = x.x == -INFINITY ? 0.0f : expf(x.x - M);
     sw[cc] = wgt;
-    l += wgt * ml[(size_t)cc * R].y;
+    l += wgt * x.y;
   }
   for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
   if ((threadIdx.x & 63) == 0) red[4 + (threadIdx.x >> 6)] = l;
   __syncthreads();
   const float L = red[4] + red[5] + red[6] + red[7];
-  const int cg = threadIdx.x >> 6, lt = threadIdx.x & 63;
   float o[DPT];
 #pragma unroll
   for (int e = 0; e < DPT; ++e) o[e] = 0.0f;
-  const float *po = a.part_o + ((size_t)g * nc * R + r) * D + lt * DPT;
-  const size_t cstride = (size_t)R * D;
-  int cc = cg;
-  for (; cc + 12 < nc; cc += 16) {  // four chunks of this group per batch
-    float v[4][DPT];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+  for (int k = 0; k < PK; ++k) {
+    const int cc = cg + 4 * k;
+    if (cc < nc)
 #pragma unroll
-      for (int e = 0; e < DPT; ++e) v[j][e] = po[(size_t)(cc + 4 * j) * cstride + e];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int e = 0; e < DPT; ++e) o[e] += sw[cc + 4 * j] * v[j][e];
+      for (int e = 0; e < DPT; ++e) o[e] += sw[cc] * v[k][e];
   }
-  for (; cc < nc; cc += 4)
+  for (int cc = cg + 4 * PK; cc < nc; cc += 4)
 #pragma unroll
     for (int e = 0; e < DPT; ++e) o[e] += sw[cc] * po[(size_t)cc * cstride + e];
+
 #pragma unroll
   for (int e = 0; e < DPT; ++e) acc[cg][lt * DPT + e] = o[e];
   __syncthreads();

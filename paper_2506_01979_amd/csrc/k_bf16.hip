@@ -144,6 +144,11 @@ __global__ __launch_bounds__(256) void k_embed_meta(EmbedArgs a, TreeArg tree) {
 // With delta set, the n_delta slices of the previous projection (one per K
 // range of a split-K GEMM, [n_delta][n_tok][hidden]) are first summed in
 // slice order and added to the residual row, which is written back.
+//
+// Every load of a thread (residual, all kMaxSplit delta slices, gains) is a
+// buffer load issued before the first use, so a row costs one memory round
+// trip; slices past n_delta, columns past hidden and rows past n_tok read
+// zero (out-of-range offsets).
 template <int IPT>
 __global__ __launch_bounds__(256) void k_rmsnorm_pack(float *__restrict__ h,
                                                       const float *__restrict__ delta,
@@ -154,38 +159,56 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(float *__restrict__ h,
   const int t = blockIdx.x;
   __shared__ float red[4];
   const int items = ks * 4;
-  float x[IPT][8];
-  float ss = 0.0f;
   const bool live = t < n_tok;
+  const int row_bytes = hidden * 4;
+  const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(h + (size_t)(live ? t : 0) * hidden), 0, live ? row_bytes : 0, kBufferDword3);
+  const int dbytes = delta ? n_delta * n_tok * row_bytes : 0;
+  const __amdgpu_buffer_rsrc_t drs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)(delta ? delta : h), 0, dbytes, kBufferDword3);
+  const __amdgpu_buffer_rsrc_t grs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)g, 0, row_bytes, kBufferDword3);
+  f32x4 hv[IPT][2], dv[IPT][kMaxSplit][2], gv[IPT][2];
 #pragma unroll
   for (int j = 0; j < IPT; ++j) {
-    const int it = threadIdx.x + j * 256;
-    const int k0 = it * 8;
-    if (live && it < items && k0 < hidden) {
-      float4 *src = (float4 *)(h + (size_t)t * hidden + k0);
-      float4 p0 = src[0], p1 = src[1];
-      if (delta) {  // residual add of the previous projection
-        const float4 *dd = (const float4 *)(delta + (size_t)t * hidden + k0);
-        float4 d0 = dd[0], d1 = dd[1];
-        const size_t stride = (size_t)n_tok * hidden / 4;
-        for (int sl = 1; sl < n_delta; ++sl) {
-          const float4 e0 = dd[sl * stride], e1 = dd[sl * stride + 1];
-          d0.x += e0.x; d0.y += e0.y; d0.z += e0.z; d0.w += e0.w;
-          d1.x += e1.x; d1.y += e1.y; d1.z += e1.z; d1.w += e1.w;
-        }
-        p0.x += d0.x; p0.y += d0.y; p0.z += d0.z; p0.w += d0.w;
-        p1.x += d1.x; p1.y += d1.y; p1.z += d1.z; p1.w += d1.w;
-        src[0] = p0;
-        src[1] = p1;
-      }
-      x[j][0] = p0.x; x[j][1] = p0.y; x[j][2] = p0.z; x[j][3] = p0.w;
-      x[j][4] = p1.x; x[j][5] = p1.y; x[j][6] = p1.z; x[j][7] = p1.w;
-    } else {
+    const int k0 = (threadIdx.x + j * 256) * 8;
+    const int vo = k0 < hidden ? k0 * 4 : row_bytes;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[j][e] = 0.0f;
+    for (int hh = 0; hh < 2; ++hh) {
+      hv[j][hh] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(hrs, vo, hh * 16, 0));
+      gv[j][hh] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(grs, vo, hh * 16, 0));
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) ss += x[j][e] * x[j][e];
+    for (int sl = 0; sl < kMaxSplit; ++sl) {
+      const int dvo = (k0 < hidden && live) ? ((sl * n_tok + t) * hidden + k0) * 4 : dbytes;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+        dv[j][sl][hh] =
+            __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(drs, dvo, hh * 16, 0));
+    }
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const int k0 = (threadIdx.x + j * 256) * 8;
+    if (delta) {  // residual add of the previous projection, slices in order
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        f32x4 d = dv[j][0][hh];
+#pragma unroll
+        for (int sl = 1; sl < kMaxSplit; ++sl) d += dv[j][sl][hh];  // missing slices read 0
+        hv[j][hh] += d;
+      }
+      if (live && k0 < hidden) {
+        f32x4 *dst = (f32x4 *)(h + (size_t)t * hidden + k0);
+        dst[0] = hv[j][0];
+        dst[1] = hv[j][1];
+      }
+    }
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ss += hv[j][hh][e] * hv[j][hh][e];
   }
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
@@ -197,16 +220,10 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(float *__restrict__ h,
     const int it = threadIdx.x + j * 256;
     if (it >= items) continue;
     const int k0 = it * 8;
+    // columns past hidden have zero residual and gain: they pack to zero
     uint16_t v[8];
-    if (k0 < hidden) {
-      const float4 g0 = *(const float4 *)(g + k0), g1 = *(const float4 *)(g + k0 + 4);
-      const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = f2bf((x[j][e] * scale) * gg[e]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = 0;
-    }
+    for (int e = 0; e < 8; ++e) v[e] = f2bf((hv[j][e >> 2][e & 3] * scale) * gv[j][e >> 2][e & 3]);
     uint4 o;
     o.x = v[0] | ((uint32_t)v[1] << 16);
     o.y = v[2] | ((uint32_t)v[3] << 16);
