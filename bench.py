@@ -195,7 +195,7 @@ def trace_summary(trace_dir: str) -> str:
     out = [f"# Kernel trace of the verify step, {WORKLOAD}", "",
            "Command: `cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
            "--output-format csv -d <repo>/gpurun_out/prof_step -o run -- python3 <repo>/bench.py "
-           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep`, then "
+           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-graph`, then "
            "`python3 bench.py --trace-summary gpurun_out/prof_step`", "",
            f"Last {len(steps)} complete steps (embed .. stats, then the accept walk and the rollback "
            f"when traced): span "
@@ -372,6 +372,8 @@ def main():
                     help="decoder layers the CPU oracle runs (0: all of them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-alpha-sweep", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the HIP-graph replay measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="end with a device copy of known size (for rocprofv3 --pmc runs)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -447,19 +449,20 @@ def main():
 
     new_len = torch.zeros(1, dtype=torch.int32, device=dev)
 
-    def step():
+    def step(st=None):
         # a0-a8: tree metadata ... LM head + stats, the accept walk, and the
         # rollback that compacts the kept path behind the prefix (it moves
         # tree slots only, which the next step's forward rewrites)
-        m.sb_verify_forward(k_, v_, kv_len, d_tok, parents, 1.0, logits, stats, ws, stream)
-        api.sb_accept_resample(d_tok, parents, logits, stats, 1.0, d_q, d_u, res, sws, stream)
-        m.sb_kv_rollback(k_, v_, kv_len, res, new_len, stream)
+        st = st or stream
+        m.sb_verify_forward(k_, v_, kv_len, d_tok, parents, 1.0, logits, stats, ws, st)
+        api.sb_accept_resample(d_tok, parents, logits, stats, 1.0, d_q, d_u, res, sws, st)
+        m.sb_kv_rollback(k_, v_, kv_len, res, new_len, st)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    m.sb_timer_start(DOMINANT, args.steps * shape.n_layers)
+    # the timed steps: K steps between two events, nothing else enqueued
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -468,22 +471,48 @@ def main():
         step()
     ev1.record(stream)
     torch.cuda.synchronize()
-    total_ms = ev0.elapsed_time(ev1)
-    k_ms, k_launches = m.sb_timer_stop()
-    ms_per_step = total_ms / args.steps
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
 
-    # same loop without the per-kernel events, for the clean step time
+    # the same K steps again with HIP events around every launch of the
+    # dominant kernel (its average duration for the roofline); the events
+    # cost time of their own, so this loop is not the step time
+    m.sb_timer_start(DOMINANT, args.steps * shape.n_layers)
     torch.cuda.synchronize()
     ev0.record(stream)
     for _ in range(args.steps):
         step()
     ev1.record(stream)
     torch.cuda.synchronize()
-    clean_ms = ev0.elapsed_time(ev1) / args.steps
+    evented_ms = ev0.elapsed_time(ev1) / args.steps
+    k_ms, k_launches = m.sb_timer_stop()
 
     r = api.decode_result(res)
     if int(new_len.item()) != kv_len + 1 + r["n_accepted"]:
         raise RuntimeError("rollback length does not match the accepted path")
+
+    # The same step captured once in a HIP graph and replayed (kernel
+    # arguments, including kv_len and the tree, are fixed in the graph).
+    graph_ms = None
+    if not args.no_graph:
+        gs = torch.cuda.Stream()
+        gs.wait_stream(stream)
+        with torch.cuda.stream(gs):
+            step(gs)            # warm outside the capture
+        gs.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=gs):
+            step(gs)
+        graph.replay()
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = ev0.elapsed_time(ev1) / args.steps
+        rg = api.decode_result(res)
+        if rg != r:
+            raise RuntimeError("graph replay changed the step's result")
 
     if args.copy_calibration:
         # a plain device copy of known size, for scaling the HBM byte counters
@@ -522,7 +551,8 @@ def main():
         "step_hbm": {"bytes": nbytes["step"],
                      "achieved_gbs": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9, 1),
                      "frac": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "ms_per_step_without_kernel_events": round(clean_ms, 4)},
+                     "ms_per_step_with_kernel_events": round(evented_ms, 4),
+                     "ms_per_step_graph_replay": None if graph_ms is None else round(graph_ms, 4)},
         "accepted": r["n_accepted"],
     }
 

@@ -98,9 +98,35 @@ __global__ __launch_bounds__(256) void k_embed_meta(EmbedArgs a, TreeArg tree) {
   if (t < a.n_tok) {
     int tok = a.tokens[t];
     tok = tok < 0 ? 0 : (tok >= a.vocab ? a.vocab - 1 : tok);  // ids are clamped
-    const ET *e = (const ET *)a.embed;
-    for (int k = threadIdx.x; k < a.hidden; k += blockDim.x)
-      h[k] = load_embed<ET>(e, (size_t)tok * a.hidden + k);
+    const ET *e = (const ET *)a.embed + (size_t)tok * a.hidden;
+    if (sizeof(ET) == 2 && (a.hidden & 7) == 0) {
+      // bf16 rows: 8 elements per 16-byte load, every load of the row issued
+      // before the first store (hidden <= 16384: at most 8 per thread)
+      constexpr int kMaxV = 8;
+      uint4 v[kMaxV];
+      const int nv = a.hidden >> 3;
+#pragma unroll
+      for (int j = 0; j < kMaxV; ++j) {
+        const int i = threadIdx.x + j * 256;
+        if (i < nv) v[j] = ((const uint4 *)e)[i];
+      }
+#pragma unroll
+      for (int j = 0; j < kMaxV; ++j) {
+        const int i = threadIdx.x + j * 256;
+        if (i < nv) {
+          const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+          float4 lo, hi;
+          lo.x = bf2f((uint16_t)(w[0] & 0xffff)); lo.y = bf2f((uint16_t)(w[0] >> 16));
+          lo.z = bf2f((uint16_t)(w[1] & 0xffff)); lo.w = bf2f((uint16_t)(w[1] >> 16));
+          hi.x = bf2f((uint16_t)(w[2] & 0xffff)); hi.y = bf2f((uint16_t)(w[2] >> 16));
+          hi.z = bf2f((uint16_t)(w[3] & 0xffff)); hi.w = bf2f((uint16_t)(w[3] >> 16));
+          ((float4 *)h)[2 * i] = lo;
+          ((float4 *)h)[2 * i + 1] = hi;
+        }
+      }
+    } else {
+      for (int k = threadIdx.x; k < a.hidden; k += blockDim.x) h[k] = load_embed<ET>(e, k);
+    }
   } else {
     for (int k = threadIdx.x; k < a.hidden; k += blockDim.x) h[k] = 0.0f;
   }

@@ -19,6 +19,7 @@
 #include <limits.h>
 #include <math.h>
 
+#include "sb_device.h"
 #include "sb_internal.h"
 
 namespace sb {
@@ -108,12 +109,24 @@ struct Dist {
   const double *arr;  // non-null: residual array
   double zdiv;
 
+  // p~(v), divided exactly (used for the accept ratio of a single token)
   __device__ __forceinline__ double at(int v) const {
     if (arr) return arr[v] / zdiv;
     if (greedy) return v == argmax ? 1.0 : 0.0;
     float z = l[v] * inv_t;
     float e = expf(z - zmax);
     return (double)e / total;
+  }
+  // 1 / (total or Z): vocabulary passes multiply by it instead of dividing
+  // every element (an fp64 division is dozens of instructions); the values
+  // differ from at() by at most an ulp
+  __device__ __forceinline__ double recip() const { return 1.0 / (arr ? zdiv : total); }
+  __device__ __forceinline__ double at_fast(int v, double rcp) const {
+    if (arr) return arr[v] * rcp;
+    if (greedy) return v == argmax ? 1.0 : 0.0;
+    float z = l[v] * inv_t;
+    float e = expf(z - zmax);
+    return (double)e * rcp;
   }
 };
 
@@ -140,13 +153,14 @@ struct Shared {
 
 // Elements of a vocabulary pass handled per thread per batch: their loads are
 // issued together so a batch costs one memory latency.
-constexpr int kBatch = 8;
+constexpr int kBatch = 16;
 
 // After candidate with draft row q is rejected: r = max(0, p~ - q) into
 // dst; returns Z = sum r (all threads).  The new p~ is r / Z.
 __device__ double residual_pass(const Dist &cur, const float *q, int vocab, double *dst,
                                 Shared &sh) {
   double part = 0.0;
+  const double rcp = cur.recip();
   for (int v0 = threadIdx.x; v0 < vocab; v0 += kBatch * kWalkThreads) {
     float qv[kBatch];
     double pv[kBatch];
@@ -154,7 +168,7 @@ __device__ double residual_pass(const Dist &cur, const float *q, int vocab, doub
     for (int j = 0; j < kBatch; ++j) {
       const int v = v0 + j * kWalkThreads;
       qv[j] = v < vocab ? q[v] : 0.0f;
-      pv[j] = v < vocab ? cur.at(v) : 0.0;
+      pv[j] = v < vocab ? cur.at_fast(v, rcp) : 0.0;
     }
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
@@ -171,20 +185,22 @@ __device__ double residual_pass(const Dist &cur, const float *q, int vocab, doub
 }
 
 // Inverse-CDF draw from p~ with uniform u (all threads return the token).
-// Each wave owns a contiguous segment of the vocabulary: pass 1 sums the
-// segments, pass 2 rescans its segment 64 elements at a time (a lane-parallel
-// inclusive scan on top of the running prefix) and stops at the first
-// C_v > u * W.  Both passes read kBatch blocks of 64 per batch.
+// Each wave owns a contiguous segment of the vocabulary.  Pass 1 sums the
+// segments.  Pass 2 walks its segment in blocks of 512: lane l holds the 8
+// consecutive elements 8l .. 8l + 7 of the block, one 64-lane inclusive scan
+// of the lane sums gives each lane's prefix, the first lane whose range
+// crosses u * W finds the exact token in its 8 elements.
 __device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int seg = ((vocab + kWaves - 1) / kWaves + 63) & ~63;
+  const int seg = ((vocab + kWaves - 1) / kWaves + 511) & ~511;
   const int lo = w * seg;
   const int hi = min(vocab, lo + seg);
+  const double rcp = d.recip();
   double part = 0.0;
   for (int v0 = lo + lane; v0 < hi; v0 += 64 * kBatch) {
     double x[kBatch];
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) x[j] = (v0 + 64 * j < hi) ? d.at(v0 + 64 * j) : 0.0;
+    for (int j = 0; j < kBatch; ++j) x[j] = (v0 + 64 * j < hi) ? d.at_fast(v0 + 64 * j, rcp) : 0.0;
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) part += x[j];
   }
@@ -206,25 +222,44 @@ __device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
   const double thr = (double)u * W;
   int cand = INT_MAX;
   double run = base;
-  for (int v0 = lo; v0 < hi && cand == INT_MAX; v0 += 64 * kBatch) {
-    double x[kBatch];
+  // skip whole segments that end below the threshold (their total is known)
+  const double seg_end = (w + 1 < kWaves) ? sh.red[w + 1] : W;
+  if (lo < hi && seg_end > thr) {
+    for (int b0 = lo; b0 < hi && cand == INT_MAX; b0 += 512) {
+      const int e0 = b0 + 8 * lane;
+      double x[8];
+      double ls = 0.0;
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int v = v0 + 64 * j + lane;
-      x[j] = v < hi ? d.at(v) : 0.0;
-    }
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      if (cand != INT_MAX) break;
-      const int v = v0 + 64 * j + lane;
-      double inc = x[j];
+      for (int e = 0; e < 8; ++e) {
+        x[e] = (e0 + e < hi) ? d.at_fast(e0 + e, rcp) : 0.0;
+        ls += x[e];
+      }
+      double inc = ls;
       for (int o = 1; o < 64; o <<= 1) {
         const double y = __shfl_up(inc, o, 64);
         if (lane >= o) inc += y;
       }
-      const double C = run + inc;
-      const unsigned long long hit = __ballot(v < hi && C > thr);
-      if (hit) cand = v0 + 64 * j + __ffsll((long long)hit) - 1;
+      const double lane_start = run + (inc - ls);
+      const unsigned long long hit = __ballot(e0 < hi && lane_start + ls > thr);
+      if (hit) {
+        const int first = __ffsll((long long)hit) - 1;
+        // the crossing lane finds the token among its 8 elements (its range
+        // crosses, so one of them does unless rounding says otherwise; then
+        // its last valid element)
+        int found = INT_MAX;
+        if (lane == first) {
+          double c = lane_start;
+          found = min(e0 + 7, hi - 1);
+          for (int e = 0; e < 8; ++e) {
+            c += x[e];
+            if (e0 + e < hi && c > thr) {
+              found = e0 + e;
+              break;
+            }
+          }
+        }
+        cand = __shfl(found, first, 64);
+      }
       run += __shfl(inc, 63, 64);
     }
   }
@@ -233,7 +268,7 @@ __device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
     // rounding left no crossing: the last token with positive mass
     int lp = -1;
     for (int v = threadIdx.x; v < vocab; v += kWalkThreads)
-      if (d.at(v) > 0.0) lp = v;
+      if (d.at_fast(v, rcp) > 0.0) lp = v;
     y = block_max<kWaves>(lp, sh.ired);
     if (y < 0) y = vocab - 1;
   }
@@ -251,9 +286,10 @@ __device__ int node_select(Dist *cur, const Cand &cand, int n_cand, int vocab, d
       const int x = cand.tok(i);
       double ratio = 0.0;  // a token id outside the vocabulary is rejected
       if (x >= 0 && x < vocab) {
-        const double qx = (double)cand.q(i)[x];
+        // p~(x) and q(x): gathered up front while p~ is still the row itself
+        const double qx = (double)(cur->arr ? cand.q(i)[x] : cand.qx(i));
         if (qx == 0.0) *flags |= SB_FLAG_QZERO;
-        ratio = cur->at(x) / qx;
+        ratio = (cur->arr ? cur->at(x) : cand.px(i)) / qx;
       } else {
         *flags |= SB_FLAG_QZERO;
       }
@@ -276,14 +312,19 @@ __device__ int node_select(Dist *cur, const Cand &cand, int n_cand, int vocab, d
   return -1;
 }
 
+// Candidate sets.  px(i) / qx(i): the row distribution's p at the
+// candidate's token and q(i) at it, valid while p~ is still that row.
 struct ExplicitCands {
   const int32_t *toks;
   const float *qbase;
   const float *ubase;
   int vocab;
+  const Dist *row;
   __device__ int tok(int i) const { return toks[i]; }
   __device__ const float *q(int i) const { return qbase + (size_t)i * vocab; }
   __device__ float u(int i) const { return ubase[i]; }
+  __device__ double px(int i) const { return row->at(toks[i]); }
+  __device__ float qx(int i) const { return q(i)[toks[i]]; }
 };
 
 struct ChildCands {
@@ -292,9 +333,13 @@ struct ChildCands {
   const float *qbase;
   const float *ubase;
   int vocab;
+  const double *pre_p;  // [row]: p of the row's parent at the row's token
+  const float *pre_q;   // [row]: q of the row at its token
   __device__ int tok(int i) const { return toks[kids[i]]; }
   __device__ const float *q(int i) const { return qbase + (size_t)kids[i] * vocab; }
   __device__ float u(int i) const { return ubase[kids[i]]; }
+  __device__ double px(int i) const { return pre_p[kids[i]]; }
+  __device__ float qx(int i) const { return pre_q[kids[i]]; }
 };
 
 // ---------------------------------------------------------------------------
@@ -303,6 +348,114 @@ struct ChildCands {
 // z = fl32(l / T) and a NaN/+inf scan; pass 2: float64 sum of
 // fl32(exp(z - zmax)).  Loads are 16-byte and independent across a thread's
 // items so a pass costs about one memory latency.
+// Row statistics with the whole row in registers (vocab a multiple of 4 and
+// at most NB * 4096): one read of the row, the max / argmax / non-finite
+// scan and the exp sum both run on the registers.
+template <int NB>
+__global__ __launch_bounds__(1024) void k_softmax_stats_reg(const float *__restrict__ logits,
+                                                            int vocab, float inv_t, int greedy,
+                                                            sb_row_stats *__restrict__ out) {
+  constexpr int NT = 1024, NW = NT / 64;
+  __shared__ float smax[NW], szmax[NW];
+  __shared__ int sarg[NW];
+  __shared__ int sbad[NW];
+  __shared__ double red[NW];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n4 = vocab >> 2;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(logits + (size_t)blockIdx.x * vocab), 0, vocab * 4, kBufferDword3);
+  f32x4 x[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int i = threadIdx.x + j * NT;
+    x[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16, 0, 0));
+  }
+  float best = -INFINITY;
+  int barg = INT_MAX;
+  float zbest = -INFINITY;
+  int bad = 0;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int i = threadIdx.x + j * NT;
+    if (i < n4) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float v = x[j][e];
+        if (isnan(v) || v == INFINITY) bad = 1;
+        if (v > best) {
+          best = v;
+          barg = 4 * i + e;
+        }
+        zbest = fmaxf(zbest, v * inv_t);
+      }
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o, 64);
+    const int oa = __shfl_xor(barg, o, 64);
+    if (ob > best || (ob == best && oa < barg)) {
+      best = ob;
+      barg = oa;
+    }
+    zbest = fmaxf(zbest, __shfl_xor(zbest, o, 64));
+    bad |= __shfl_xor(bad, o, 64);
+  }
+  if (lane == 0) {
+    smax[w] = best;
+    sarg[w] = barg;
+    sbad[w] = bad;
+    szmax[w] = zbest;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float b = smax[0], zb = szmax[0];
+    int a = sarg[0], bd = sbad[0];
+    for (int i = 1; i < NW; ++i) {
+      if (smax[i] > b || (smax[i] == b && sarg[i] < a)) {
+        b = smax[i];
+        a = sarg[i];
+      }
+      zb = fmaxf(zb, szmax[i]);
+      bd |= sbad[i];
+    }
+    smax[0] = greedy ? b : zb;
+    sarg[0] = (a == INT_MAX) ? 0 : a;
+    sbad[0] = bd;
+  }
+  __syncthreads();
+  const float zmax = smax[0];
+  const int arg = sarg[0];
+  const int anybad = sbad[0];
+  double total = 1.0;
+  if (!greedy) {
+    double part = 0.0;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int i = threadIdx.x + j * NT;
+      if (i < n4)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part += (double)expf(x[j][e] * inv_t - zmax);
+    }
+    part = wave_sum(part);
+    if (lane == 0) red[w] = part;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double t = 0.0;
+      for (int i = 0; i < NW; ++i) t += red[i];
+      red[0] = t;
+    }
+    __syncthreads();
+    total = red[0];
+  }
+  if (threadIdx.x == 0) {
+    sb_row_stats st;
+    st.zmax = zmax;
+    st.argmax = arg;
+    st.total = anybad ? (double)NAN : total;
+    out[blockIdx.x] = st;
+  }
+}
+
 __global__ __launch_bounds__(1024) void k_softmax_stats(const float *__restrict__ logits,
                                                         int vocab, float inv_t, int greedy,
                                                         sb_row_stats *__restrict__ out) {
@@ -440,19 +593,39 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
   __shared__ int16_t path[SB_MAX_ROWS];
   __shared__ int nk;
   __shared__ int s_flags;
+  __shared__ sb_row_stats s_st[SB_MAX_ROWS];
+  __shared__ double s_px[SB_MAX_ROWS];
+  __shared__ float s_qx[SB_MAX_ROWS];
   const int n = tree.n;
   double *ws0 = ws;
   double *ws1 = ws + vocab;
   if (threadIdx.x == 0) s_flags = 0;
+  // every row's statistics, then in parallel every row's test values: p of
+  // its parent at its token and q at its token (the walk's chain tests then
+  // read LDS instead of paying a memory round trip each)
+  if ((int)threadIdx.x < n) s_st[threadIdx.x] = stats[threadIdx.x];
   __syncthreads();
-  if ((int)threadIdx.x < n && isnan(stats[threadIdx.x].total)) atomicOr(&s_flags, SB_FLAG_NONFINITE);
+  if ((int)threadIdx.x < n && isnan(s_st[threadIdx.x].total)) atomicOr(&s_flags, SB_FLAG_NONFINITE);
+  if ((int)threadIdx.x >= 1 && (int)threadIdx.x < n) {
+    const int i = threadIdx.x;
+    const int x = tokens[i];
+    const int par = tree.parent[i];
+    double px = 0.0;
+    float qx = 0.0f;
+    if (x >= 0 && x < vocab) {
+      px = row_dist(logits + (size_t)par * vocab, s_st[par], inv_t, greedy).at(x);
+      qx = q[(size_t)i * vocab + x];
+    }
+    s_px[i] = px;
+    s_qx[i] = qx;
+  }
   __syncthreads();
   int flags = 0;  // thread 0 accumulates
   int nrej = 0;
   int node = 0;
   int plen = 1;
   if (threadIdx.x == 0) path[0] = 0;
-  Dist cur = row_dist(logits, stats[0], inv_t, greedy);
+  Dist cur = row_dist(logits, s_st[0], inv_t, greedy);
   int y = 0;
   int bonus = 0;
   for (;;) {
@@ -469,14 +642,14 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
       y = draw_pass(cur, u[0], vocab, sh);
       break;
     }
-    ChildCands cc{kids, tokens, q, u, vocab};
+    ChildCands cc{kids, tokens, q, u, vocab, s_px, s_qx};
     const int acc = node_select(&cur, cc, nkids, vocab, ws0, ws1, &flags, &nrej, sh);
     if (acc >= 0) {
       node = kids[acc];
       __syncthreads();
       if (threadIdx.x == 0) path[plen] = (int16_t)node;
       ++plen;
-      cur = row_dist(logits + (size_t)node * vocab, stats[node], inv_t, greedy);
+      cur = row_dist(logits + (size_t)node * vocab, s_st[node], inv_t, greedy);
       continue;
     }
     y = draw_pass(cur, u[0], vocab, sh);
@@ -517,7 +690,7 @@ __global__ __launch_bounds__(kWalkThreads) void k_select(int vocab, const float 
   const sb_row_stats s0 = st[0];
   if (isnan(s0.total)) flags |= SB_FLAG_NONFINITE;
   Dist cur = row_dist(lrow, s0, inv_t, greedy);
-  ExplicitCands ec{ctoks, q, u, vocab};
+  ExplicitCands ec{ctoks, q, u, vocab, &cur};
   const int acc = node_select(&cur, ec, n_cand, vocab, ws, ws + vocab, &flags, &nrej, sh);
   int tok;
   if (acc >= 0) {
@@ -546,6 +719,17 @@ hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, floa
   float inv_t;
   int greedy;
   temp_args(temperature, &inv_t, &greedy);
+  const int nb = (vocab + 4095) / 4096;  // float4 per thread with the row in registers
+  if ((vocab & 3) == 0 && nb <= 16) {
+#define SB_NB(k)                                                                                  \
+  if (nb <= k) {                                                                                  \
+    hipLaunchKernelGGL(k_softmax_stats_reg<k>, dim3(n_rows), dim3(1024), 0, s, logits, vocab,     \
+                       inv_t, greedy, stats);                                                     \
+    return hipGetLastError();                                                                     \
+  }
+    SB_NB(1) SB_NB(2) SB_NB(4) SB_NB(8) SB_NB(16)
+#undef SB_NB
+  }
   hipLaunchKernelGGL(k_softmax_stats, dim3(n_rows), dim3(1024), 0, s, logits, vocab, inv_t, greedy,
                      stats);
   return hipGetLastError();
