@@ -40,8 +40,9 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", f"traffic_gate_up_{WORKLOAD}.md")
 # stale once any of them changes)
 GEMM_SOURCES = ("paper_2506_01979_amd/csrc/k_gemm.hip", "paper_2506_01979_amd/csrc/sb_device.h",
                 "paper_2506_01979_amd/csrc/sb_internal_fwd.h")
-# kernels of one verify step, in launch order: embed, 8 per layer, final
-# norm, LM head, stats; the gate/up GEMM is the 7th kernel of a layer
+# kernels of one verify step, in launch order: embed, 8 per layer (7 when
+# the attention kernel merges its key ranges itself), final norm, LM head,
+# stats
 PER_LAYER = ("norm", "qkv", "attn", "attn_merge", "o", "norm", "gate_up", "down")
 
 
@@ -79,14 +80,18 @@ def _gate_up_dispatches(rows, n_layers, last):
     steps (the timed ones; earlier steps generate the drafts on partial
     trees)."""
     out = []
+    per_layer = list(PER_LAYER)
+    if not any("k_attn_merge" in r["name"] for r in rows):
+        per_layer.remove("attn_merge")
+    nk = 1 + len(per_layer) * n_layers + 3
     for i, r in enumerate(rows):
         if "k_embed_meta" not in r["name"]:
             continue
-        step = rows[i:i + 1 + len(PER_LAYER) * n_layers + 3]
-        if len(step) < 1 + len(PER_LAYER) * n_layers + 3 or "k_softmax_stats" not in step[-1]["name"]:
+        step = rows[i:i + nk]
+        if len(step) < nk or "k_softmax_stats" not in step[-1]["name"]:
             continue
         for l in range(n_layers):
-            g = step[1 + len(PER_LAYER) * l + PER_LAYER.index("gate_up")]
+            g = step[1 + len(per_layer) * l + per_layer.index("gate_up")]
             if "k_gemm" not in g["name"]:
                 raise RuntimeError(f"unexpected kernel order: {g['name']}")
             out.append(g)
@@ -172,10 +177,14 @@ def trace_summary(trace_dir: str) -> str:
     trace = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
     rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
     starts = [i for i, r in enumerate(rows) if "k_embed_meta" in r["Kernel_Name"]]
-    n_k = 1 + len(PER_LAYER) * shape.n_layers + 3
+    # the attention merge runs inside the attention kernel when heads are small
+    per_layer = list(PER_LAYER)
+    if not any("k_attn_merge" in r["Kernel_Name"] for r in rows[starts[-1]:]):
+        per_layer.remove("attn_merge")
+    n_k = 1 + len(per_layer) * shape.n_layers + 3
     steps = [i for i in starts if i + n_k <= len(rows) and
              "k_softmax_stats" in rows[i + n_k - 1]["Kernel_Name"]][-5:]
-    cls = ["embed"] + list(PER_LAYER) * shape.n_layers + ["norm", "lm_head", "stats"]
+    cls = ["embed"] + per_layer * shape.n_layers + ["norm", "lm_head", "stats"]
     # the bench step goes on with the accept walk and the rollback
     tail = [c for c in ("k_walk", "k_rollback")]
     n_s = n_k
