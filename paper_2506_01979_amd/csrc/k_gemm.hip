@@ -32,8 +32,8 @@ __device__ __forceinline__ void rope_pair(float x1, float x2, float2 cs, float *
 // Epilogue of one finished output pair: rows p and p + 8 of tile `tile`,
 // activation row t < n_tok, values v1 / v2 (K range `split` of a split-K
 // launch).
-__device__ __forceinline__ void epilogue(const GemmArgs &a, int split, int tile, int p, int t,
-                                         float v1, float v2) {
+__device__ __forceinline__ void epilogue(const GemmArgs &a, const float2 *rope, int split,
+                                         int tile, int p, int t, float v1, float v2) {
   if (a.epi == EPI_QKV) {
     const int d = a.head_dim, ht = d / 16;
     const int qt = a.n_heads * ht, kt = a.n_kv * ht;
@@ -43,7 +43,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs &a, int split, int tile,
       const int head = idx / ht, u = idx % ht;
       const int j = 8 * u + p;
       float o1, o2;
-      rope_pair(v1, v2, a.rope[t * (d / 2) + j], &o1, &o2);
+      rope_pair(v1, v2, rope[t * (d / 2) + j], &o1, &o2);
       uint16_t *dst = isq ? a.q + ((size_t)t * a.n_heads + head) * d
                           : a.kc + ((size_t)head * a.cap + a.kv_len + t) * d;
       dst[j] = f2bf(o1);
@@ -98,8 +98,10 @@ struct Ring {
   static constexpr int R = r > 4 ? 4 : (r < 1 ? 1 : r);
 };
 
-// token tiles reduced per LDS round
-constexpr int kRedTT = 4;
+// (tile, token tile) accumulator pairs reduced per LDS round (128 KB)
+constexpr int kRedPairs = 16;
+// RoPE table staged in LDS for the QKV epilogue (float2 entries)
+constexpr int kRopeLds = 4096;
 
 // Workgroup barrier for LDS traffic only (does not wait for global loads).
 __device__ __forceinline__ void lds_barrier() {
@@ -108,9 +110,10 @@ __device__ __forceinline__ void lds_barrier() {
 
 template <int TT, int NT>
 __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
-  __shared__ f32x4 red[kGemmWaves][kRedTT][64];
+  __shared__ f32x4 red[kGemmWaves][kRedPairs][64];
+  __shared__ float2 srope[kRopeLds];
   constexpr int R = Ring<TT, NT>::R;
-  constexpr int RT = TT < kRedTT ? TT : kRedTT;
+  constexpr int TPR = kRedPairs / TT > 0 ? kRedPairs / TT : 1;  // tiles per reduction round
   // wave-uniform quantities live in scalar registers
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -131,6 +134,19 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
 #pragma unroll
   for (int tt = 0; tt < TT; ++tt)
     xvo[tt] = (tt * 16 + (lane & 15)) < a.n_tok ? tt * ks * 1024 + lane * 16 : xbytes;
+
+  // QKV: the step's RoPE table goes to LDS by direct-to-LDS loads issued
+  // now (no registers held; each wave instruction moves 1 KB), ready long
+  // before the epilogue.  The table buffer holds whole 1 KB blocks
+  // (rows padded to 16).
+  const bool rope_lds = a.epi == EPI_QKV && a.n_tok * (a.head_dim / 2) <= kRopeLds;
+  if (rope_lds) {
+    const int nblk = (a.n_tok * (a.head_dim / 2) * 8 + 1023) >> 10;
+    for (int b = w; b < nblk; b += kGemmWaves)
+      __builtin_amdgcn_global_load_lds((const void *)((const char *)a.rope + b * 1024 + lane * 16),
+                                       (__attribute__((address_space(3))) void *)((char *)srope + b * 1024),
+                                       16, 0, 0);
+  }
 
   for (int gb = t_lo; gb < t_hi; gb += NT) {
     const int n_here = t_hi - gb < NT ? t_hi - gb : NT;
@@ -199,41 +215,48 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
       }
     }
 
-    // reduce the 8 waves' partial sums tile by tile, kRedTT token tiles at
-    // a time, and run the epilogue on each finished (row pair, token)
+    // Reduce the 8 waves' partial sums, TPR tiles (all token tiles of each)
+    // per LDS round, and run the epilogue on each finished (row pair, token).
+    // Every load of this workgroup has been consumed (or is a RoPE load to
+    // LDS): waiting for all of them here is free and makes the staged table
+    // visible after the barrier.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const float2 *rope = rope_lds ? srope : a.rope;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      if (t < n_here) {
+    for (int t0 = 0; t0 < NT; t0 += TPR) {
+      if (t0 < n_here) {
 #pragma unroll
-        for (int t0 = 0; t0 < TT; t0 += RT) {
-          if (t0 * 16 < a.n_tok) {
+        for (int tl = 0; tl < TPR; ++tl)
+          if (t0 + tl < NT)
 #pragma unroll
-            for (int j = 0; j < RT; ++j)
-              if (t0 + j < TT) red[w][j][lane] = acc[t][t0 + j];
-            lds_barrier();
-            for (int it = threadIdx.x; it < 128 * RT; it += kGemmThreads) {
-              const int p = it & 7;
-              const int tl = it >> 3;  // token within this round
-              const int j = tl >> 4;
-              const int tok = t0 * 16 + tl;
-              const int l1 = (tl & 15) + 16 * (p >> 2), e1 = p & 3;
-              const int l2 = (tl & 15) + 16 * ((p + 8) >> 2), e2 = (p + 8) & 3;
-              if (t0 + j < TT && tok < a.n_tok) {
-                float v1 = 0.f, v2 = 0.f;
+            for (int tt = 0; tt < TT; ++tt) red[w][tl * TT + tt][lane] = acc[t0 + tl][tt];
+        lds_barrier();
+        const int tiles_here = n_here - t0 < TPR ? n_here - t0 : TPR;
+        const int items = tiles_here * TT * 128;
+        for (int it = threadIdx.x; it < items; it += kGemmThreads) {
+          const int p = it & 7;
+          const int rest = it >> 3;
+          const int tl = rest / (TT * 16);
+          const int tok = rest - tl * (TT * 16);
+          const int tt = tok >> 4;
+          if (tok < a.n_tok) {
+            const int l1 = (tok & 15) + 16 * (p >> 2), e1 = p & 3;
+            const int l2 = (tok & 15) + 16 * ((p + 8) >> 2), e2 = (p + 8) & 3;
+            float v1 = 0.f, v2 = 0.f;
 #pragma unroll
-                for (int ww = 0; ww < kGemmWaves; ++ww) {
-                  v1 += red[ww][j][l1][e1];
-                  v2 += red[ww][j][l2][e2];
-                }
-                epilogue(a, split, gb + t, p, tok, v1, v2);
-              }
+            for (int ww = 0; ww < kGemmWaves; ++ww) {
+              v1 += red[ww][tl * TT + tt][l1][e1];
+              v2 += red[ww][tl * TT + tt][l2][e2];
             }
-            lds_barrier();
+            epilogue(a, rope, split, gb + t0 + tl, p, tok, v1, v2);
           }
         }
+        lds_barrier();
       }
     }
   }
+  // a workgroup without tiles still owns its RoPE loads into LDS
+  if (rope_lds) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 int device_cus() {
