@@ -38,12 +38,26 @@ WORKLOAD = "llama7b_b4k8_p2048"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", f"traffic_gate_up_{WORKLOAD}.md")
 # sources the dominant GEMM kernel is built from (its byte counters are
 # stale once any of them changes)
-GEMM_SOURCES = ("paper_2506_01979_amd/csrc/k_gemm.hip", "paper_2506_01979_amd/csrc/sb_device.h",
+GEMM_SOURCES = ("paper_2506_01979_amd/csrc/k_gemm.hip", "paper_2506_01979_amd/csrc/k_gemm_swiglu.hip",
+                "paper_2506_01979_amd/csrc/sb_gemm_kernel.h", "paper_2506_01979_amd/csrc/sb_device.h",
                 "paper_2506_01979_amd/csrc/sb_internal_fwd.h")
-# kernels of one verify step, in launch order: embed, 8 per layer (7 when
-# the attention kernel merges its key ranges itself), final norm, LM head,
-# stats
-PER_LAYER = ("norm", "qkv", "attn", "attn_merge", "o", "norm", "gate_up", "down")
+# kernels of one verify step, in launch order: embed, the layers, final
+# norm, LM head, stats.  A layer is norm, QKV, attention, [attention merge],
+# O, [post-attention norm, unless O applies it], gate/up, down.
+
+
+def layer_classes(names):
+    """Kernel classes of one layer, read off the kernel names of a step
+    (names[0] is the embedding kernel)."""
+    pl, i = ["norm", "qkv", "attn"], 4
+    if "k_attn_merge" in names[i]:
+        pl.append("attn_merge")
+        i += 1
+    pl.append("o")
+    i += 1
+    if "k_rmsnorm_pack" in names[i]:
+        pl.append("norm")
+    return pl + ["gate_up", "down"]
 
 
 def log(*a):
@@ -80,13 +94,11 @@ def _gate_up_dispatches(rows, n_layers, last):
     steps (the timed ones; earlier steps generate the drafts on partial
     trees)."""
     out = []
-    per_layer = list(PER_LAYER)
-    if not any("k_attn_merge" in r["name"] for r in rows):
-        per_layer.remove("attn_merge")
-    nk = 1 + len(per_layer) * n_layers + 3
     for i, r in enumerate(rows):
-        if "k_embed_meta" not in r["name"]:
+        if "k_embed_meta" not in r["name"] or i + 8 > len(rows):
             continue
+        per_layer = layer_classes([x["name"] for x in rows[i:i + 8]])
+        nk = 1 + len(per_layer) * n_layers + 3
         step = rows[i:i + nk]
         if len(step) < nk or "k_softmax_stats" not in step[-1]["name"]:
             continue
@@ -177,10 +189,7 @@ def trace_summary(trace_dir: str) -> str:
     trace = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
     rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
     starts = [i for i, r in enumerate(rows) if "k_embed_meta" in r["Kernel_Name"]]
-    # the attention merge runs inside the attention kernel when heads are small
-    per_layer = list(PER_LAYER)
-    if not any("k_attn_merge" in r["Kernel_Name"] for r in rows[starts[-1]:]):
-        per_layer.remove("attn_merge")
+    per_layer = layer_classes([r["Kernel_Name"] for r in rows[starts[-1]:starts[-1] + 8]])
     n_k = 1 + len(per_layer) * shape.n_layers + 3
     steps = [i for i in starts if i + n_k <= len(rows) and
              "k_softmax_stats" in rows[i + n_k - 1]["Kernel_Name"]][-5:]

@@ -37,7 +37,7 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
   size_t meta, rope, h, delta;
   // bf16
-  size_t xa, act, q, part_o, part_ml;
+  size_t xa, act, q, part_o, part_ml, xn, ss;
   // f32
   size_t fa, qkv, fq, fo, gu, fact;
   size_t total;
@@ -70,6 +70,10 @@ Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
     L.n_chunks = attn_splits(c.n_kv_heads, c.head_dim, kv_len + n_rows);
     L.xa = take((size_t)np * ksx * 32 * 2);
     L.act = take((size_t)np * L.ks_f * 32 * 2);
+    // the post-attention RMSNorm fused into the O projection: gated
+    // residual (packed) and per-(token, group) sums of squares
+    L.xn = take((size_t)np * L.ks_h * 32 * 2);
+    L.ss = take((size_t)np * kSsGroups * sizeof(float));
     L.q = take((size_t)np * qd * 2);
     L.part_o = take((size_t)c.n_kv_heads * L.n_chunks * n_rows * G * d * sizeof(float));
     L.part_ml = take((size_t)c.n_kv_heads * L.n_chunks * n_rows * G * 2 * sizeof(float));
@@ -189,6 +193,8 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   uint16_t *xa = (uint16_t *)(ws + L.xa);
   uint16_t *act = (uint16_t *)(ws + L.act);
   uint16_t *q = (uint16_t *)(ws + L.q);
+  uint16_t *xn = (uint16_t *)(ws + L.xn);
+  float *ss = (float *)(ws + L.ss);
 
   EmbedArgs ea = embed_args(m, tokens, h, n, kv_len, meta, rope);
   SB_TRY(launch_embed_meta(ea, tree, L.np, 1, s));
@@ -226,6 +232,10 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   aa.part_o = (float *)(ws + L.part_o);
   aa.part_ml = (float *)(ws + L.part_ml);
 
+  // The O projection also applies the post-attention RMSNorm when its
+  // launch shape allows (RESID_NORM); gate/up then scales by 1 / rms.
+  int o_groups = 0;
+  const bool fuse_norm = resid_norm_fusable(go.tiles, go.ks, n, &o_groups);
   int split = 0;  // delta slices left by the last residual projection
   for (int l = 0; l < c.n_layers; ++l) {
     const sb_layer_weights &lw = m->layers[l];
@@ -248,13 +258,29 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
     ga.X = xa;
     ga.ks = go.ks;
     ga.out_rows = H;
-    SB_TIMED(SB_KC_O, launch_gemm(EPI_RESID, ga, go.tiles, &split, s));
-    SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, delta, split, lw.mlp_norm, H, L.ks_h, n, L.np,
-                                             c.rms_eps, xa, s));
+    if (fuse_norm) {
+      GemmArgs gn = ga;
+      gn.h = h;
+      gn.gain = lw.mlp_norm;
+      gn.xn = xn;
+      gn.xn_ks = L.ks_h;
+      gn.ss = ss;
+      SB_TIMED(SB_KC_O, launch_gemm(EPI_RESID_NORM, gn, go.tiles, nullptr, s));
+      ga.X = xn;
+      ga.ss_in = ss;
+      ga.ss_groups = o_groups;
+      ga.norm_dim = H;
+      ga.eps = c.rms_eps;
+    } else {
+      SB_TIMED(SB_KC_O, launch_gemm(EPI_RESID, ga, go.tiles, &split, s));
+      SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, delta, split, lw.mlp_norm, H, L.ks_h, n, L.np,
+                                               c.rms_eps, xa, s));
+      ga.X = xa;
+    }
     ga.W = (const uint16_t *)lw.gate_up;
-    ga.X = xa;
     ga.ks = gg.ks;
     SB_TIMED(SB_KC_GATE_UP, launch_gemm(EPI_SWIGLU, ga, gg.tiles, nullptr, s));
+    ga.ss_in = nullptr;
     ga.W = (const uint16_t *)lw.down;
     ga.X = act;
     ga.ks = gd.ks;

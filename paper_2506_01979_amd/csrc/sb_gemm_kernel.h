@@ -1,0 +1,426 @@
+// Skinny matrix-core GEMM kernel with fused epilogues (gfx950), included
+// by one translation unit per epilogue kind.
+//
+// The verify forward multiplies n_rows (5..256) activation rows by every
+// weight matrix once; the weights (13-140 GB) dominate the bytes, so the
+// GEMM streams each weight tile from HBM exactly once with 16-byte loads in
+// the operand order of v_mfma_f32_16x16x32_bf16 (the layout sb_pack_weight
+// writes).  One workgroup per compute unit owns a range of weight tiles and
+// walks K in chunks, reusing each activation fragment across all of its
+// tiles.  The epilogue kind is a template parameter, so a kernel holds the
+// registers of its own epilogue only.
+#pragma once
+
+#include <math.h>
+
+#include "sb_device.h"
+#include "sb_internal_fwd.h"
+
+namespace sb {
+namespace {
+
+constexpr int kGemmThreads = 512;
+constexpr int kGemmWaves = kGemmThreads / 64;
+
+// ---------------------------------------------------------------------------
+// skinny matrix-core GEMM with fused epilogues
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void rope_pair(float x1, float x2, float2 cs, float *o1, float *o2) {
+  *o1 = x1 * cs.x - x2 * cs.y;
+  *o2 = x2 * cs.x + x1 * cs.y;
+}
+
+// Epilogue of one finished output pair: rows p and p + 8 of tile `tile`,
+// activation row t < n_tok, values v1 / v2 (K range `split` of a split-K
+// launch).
+template <int EPI>
+__device__ __forceinline__ void epilogue(const GemmArgs &a, const float2 *rope, int split,
+                                         int tile, int p, int t, float v1, float v2) {
+  if constexpr (EPI == EPI_QKV) {
+    const int d = a.head_dim, ht = d / 16;
+    const int qt = a.n_heads * ht, kt = a.n_kv * ht;
+    if (tile < qt + kt) {
+      const bool isq = tile < qt;
+      const int idx = isq ? tile : tile - qt;
+      const int head = idx / ht, u = idx % ht;
+      const int j = 8 * u + p;
+      float o1, o2;
+      rope_pair(v1, v2, rope[t * (d / 2) + j], &o1, &o2);
+      uint16_t *dst = isq ? a.q + ((size_t)t * a.n_heads + head) * d
+                          : a.kc + ((size_t)head * a.cap + a.kv_len + t) * d;
+      dst[j] = f2bf(o1);
+      dst[j + d / 2] = f2bf(o2);
+    } else {
+      // V is cached transposed: [head][d][slot]
+      const int idx = tile - qt - kt;
+      const int head = idx / ht, u = idx % ht;
+      uint16_t *col = a.vc + ((size_t)head * d + 16 * u + p) * a.cap + a.kv_len + t;
+      col[0] = f2bf(v1);
+      col[(size_t)8 * a.cap] = f2bf(v2);
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    // the projection is stored as a delta (one slice per K range); the next
+    // RMSNorm adds the slices to the residual stream
+    const int d1 = tile * 16 + p, d2 = d1 + 8;
+    float *drow = a.h + ((size_t)split * a.n_tok + t) * a.out_rows;
+    if (d1 < a.out_rows) drow[d1] = v1;
+    if (d2 < a.out_rows) drow[d2] = v2;
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    const int f = tile * 8 + p;
+    const float gsil = v1 / (1.0f + expf(-v1));
+    a.act[packed_index(t, f, a.act_ks)] = f2bf(gsil * v2);
+  } else if constexpr (EPI == EPI_LOGITS) {
+    const int v1i = tile * 16 + p, v2i = v1i + 8;
+    float *lrow = a.logits + (size_t)t * a.out_rows;
+    if (v1i < a.out_rows) lrow[v1i] = v1;
+    if (v2i < a.out_rows) lrow[v2i] = v2;
+  }
+}
+
+// Chunk-major weight-streaming GEMM.
+//
+// K is cut into chunks of 8 k-steps; wave w of a workgroup owns k-step
+// 8c + w of every chunk c.  A workgroup owns a range of 16-row weight tiles
+// (and, for split-K launches, one K range), and a wave walks its chunks in
+// order: per chunk it loads its TT activation fragments once and the NT
+// weight fragments of that k-step (one per tile), so each activation
+// fragment feeds NT matrix-core products.  Activation re-reads from L2 are
+// what limits a skinny GEMM whose waves stream one tile at a time; reusing
+// them across the workgroup's tiles cuts that traffic NT-fold.  Loads run R
+// chunks ahead in a register ring.  At the end the 8 waves' partial sums of
+// every tile are reduced in LDS and the epilogue runs.
+//
+// Ring depth per (TT, NT): as deep as the 256-register budget of two waves
+// per SIMD allows (ring 4R(NT+TT), accumulators 4*NT*TT, lane offsets NT+TT,
+// about 48 for the rest).
+template <int TT, int NT>
+struct Ring {
+  static constexpr int free_regs = 208 - TT - NT - 4 * NT * TT;
+  static constexpr int r = free_regs / (4 * (NT + TT));
+  static constexpr int R = r > 4 ? 4 : (r < 1 ? 1 : r);
+};
+
+// LDS staging area (32 KB): the step's RoPE table (QKV), the residual rows
+// and gains of the group's tiles (RESID_NORM), or the RMSNorm scales of the
+// tokens (the consumer of a RESID_NORM launch).
+constexpr int kStageBytes = 32768;
+constexpr int kRopeLds = kStageBytes / 8;  // float2 entries
+constexpr int kStageGain = 16384;          // RESID_NORM: gains (1 KB)
+constexpr int kStageSq = 17408;            // RESID_NORM: per-(tile, token) sums of squares
+
+// Workgroup barrier for LDS traffic only (does not wait for global loads).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// RESID_NORM epilogue of one output pair (rows p, p + 8 of the tile, token
+// t): adds the projection to the residual (staged row hrow), stores it,
+// packs bf16(h * gain) for the next projection and returns the pair's sum
+// of squares.
+__device__ __forceinline__ float resid_norm(const GemmArgs &a, const float *hrow, const float *gain,
+                                            int tile, int p, int t, float v1, float v2) {
+  const int d1 = tile * 16 + p, d2 = d1 + 8;
+  const float h1 = hrow[p] + v1, h2 = hrow[p + 8] + v2;
+  float *hg = a.h + (size_t)t * a.out_rows;
+  float sq = 0.0f;
+  if (d1 < a.out_rows) {
+    hg[d1] = h1;
+    a.xn[packed_index(t, d1, a.xn_ks)] = f2bf(h1 * gain[p]);
+    sq = h1 * h1;
+  }
+  if (d2 < a.out_rows) {
+    hg[d2] = h2;
+    a.xn[packed_index(t, d2, a.xn_ks)] = f2bf(h2 * gain[p + 8]);
+    sq += h2 * h2;
+  }
+  return sq;
+}
+
+template <int EPI, int TT, int NT>
+__global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
+  __shared__ f32x4 red[kGemmWaves][kRedPairs][64];
+  __shared__ __attribute__((aligned(16))) char stage[kStageBytes];
+  constexpr int R = Ring<TT, NT>::R;
+  constexpr int TPR = kRedPairs / TT > 0 ? kRedPairs / TT : 1;  // tiles per reduction round
+  // wave-uniform quantities live in scalar registers
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int ks = a.ks;
+  const int S = a.split;
+  const int split = blockIdx.x % S, grp = blockIdx.x / S;
+  const int t_lo = (int)(((long long)a.tiles * grp) / a.groups);
+  const int t_hi = (int)(((long long)a.tiles * (grp + 1)) / a.groups);
+  const int nc = ks >> 3;
+  const int c_begin = (nc * split) / S;
+  const int n_ch = (nc * (split + 1)) / S - c_begin;
+  // Activation lanes of rows >= n_tok point past the end of the buffer and
+  // read as zero; weight lanes of tiles past the group's end likewise.
+  const int xbytes = ((a.n_tok + 15) >> 4) * ks * 1024;
+  const __amdgpu_buffer_rsrc_t xrs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.X, 0, xbytes, kBufferDword3);
+  int xvo[TT];
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt)
+    xvo[tt] = (tt * 16 + (lane & 15)) < a.n_tok ? tt * ks * 1024 + lane * 16 : xbytes;
+
+  // Operands of the epilogue go to LDS by direct-to-LDS loads issued now (no
+  // registers held; each wave instruction moves 1 KB), long before the
+  // epilogue needs them.
+  // QKV: the step's RoPE table (its buffer holds whole 1 KB blocks: rows
+  // padded to 16).
+  const bool rope_lds = EPI == EPI_QKV && a.n_tok * (a.head_dim / 2) <= kRopeLds;
+  if (rope_lds) {
+    const int nblk = (a.n_tok * (a.head_dim / 2) * 8 + 1023) >> 10;
+    for (int b = w; b < nblk; b += kGemmWaves)
+      __builtin_amdgcn_global_load_lds((const void *)((const char *)a.rope + b * 1024 + lane * 16),
+                                       (lds_void *)(stage + b * 1024), 16, 0, 0);
+  }
+  // RESID_NORM (one pass, one reduction round): block (tile tl, token tile
+  // tt) of the residual, [16 tokens][16 rows] fp32, and the group's gains.
+  // Tokens >= n_tok read zero.
+  if constexpr (EPI == EPI_RESID_NORM) {
+    const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.h, 0, a.n_tok * a.out_rows * 4, kBufferDword3);
+    for (int b = w; b < (t_hi - t_lo) * TT; b += kGemmWaves) {
+      const int tl = b / TT, tt = b - tl * TT;
+      const int tok = tt * 16 + (lane >> 2), row = (t_lo + tl) * 16 + 4 * (lane & 3);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(hrs, (lds_void *)(stage + b * 1024), 16,
+                                               (tok * a.out_rows + row) * 4, 0, 0, 0);
+    }
+    if (w == kGemmWaves - 1) {
+      const __amdgpu_buffer_rsrc_t grs =
+          __builtin_amdgcn_make_buffer_rsrc((void *)a.gain, 0, a.out_rows * 4, kBufferDword3);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(grs, (lds_void *)(stage + kStageGain), 16,
+                                               (t_lo * 16 + 4 * lane) * 4, 0, 0, 0);
+    }
+  }
+  // Consumer of RESID_NORM: row t of the sums of squares (kSsGroups floats,
+  // 1 KB) into the reduction buffer, reduced after the first pass's loads.
+  if (EPI == EPI_SWIGLU && a.ss_in) {
+    const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.ss_in, 0, a.n_tok * kSsGroups * 4, kBufferDword3);
+    for (int t = w; t < a.n_tok; t += kGemmWaves)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(srs, (lds_void *)((char *)red + t * 1024), 16,
+                                               lane * 16, t * 1024, 0, 0);
+  }
+
+  for (int gb = t_lo; gb < t_hi; gb += NT) {
+    const int n_here = t_hi - gb < NT ? t_hi - gb : NT;
+    const int wbytes = n_here * ks * 1024;
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)a.W + (size_t)gb * ks * 1024), 0, wbytes, kBufferDword3);
+    int wvo[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) wvo[t] = t < n_here ? t * ks * 1024 + lane * 16 : wbytes;
+
+    i32x4 wr[R][NT], xr[R][TT];
+    f32x4 acc[NT][TT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt) acc[t][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // loads of this wave's k-step of chunk c (relative to the K range)
+    auto issue = [&](int r, int c) {
+      const int koff = ((c_begin + c) * 8 + w) * 1024;
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt)
+        xr[r][tt] = __builtin_amdgcn_raw_buffer_load_b128(xrs, xvo[tt], koff, 0);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        wr[r][t] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo[t], koff, kNonTemporal);
+    };
+    auto mac = [&](int r) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt)
+          acc[t][tt] = mfma16(__builtin_bit_cast(bf16x8, wr[r][t]),
+                              __builtin_bit_cast(bf16x8, xr[r][tt]), acc[t][tt]);
+    };
+    int c = 0;
+    if (n_ch >= R) {
+      // fill the ring in slot order (the oldest loads are consumed first)
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        issue(r, r);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // steady state: every consumed slot is refilled R chunks ahead
+      for (; c + 2 * R <= n_ch; c += R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          mac(r);
+          issue(r, c + R + r);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      // the last one or two rings: refill only while chunks remain
+      for (; c < n_ch; c += R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if (c + r < n_ch) {
+            mac(r);
+            if (c + r + R < n_ch) issue(r, c + r + R);
+          }
+        }
+      }
+    } else {
+      for (; c < n_ch; ++c) {
+        issue(0, c);
+        mac(0);
+      }
+    }
+
+    // Every load of this workgroup has been consumed or is a staging load
+    // into LDS: waiting for all of them is free here, and the barriers below
+    // make the staged data visible.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    float *sinv = (float *)stage;  // consumer of RESID_NORM: 1 / rms per token
+    if (EPI == EPI_SWIGLU && a.ss_in && gb == t_lo) {
+      lds_barrier();
+      // 4 threads per token, 64 groups each (16-byte reads staggered by
+      // token across the LDS banks; groups past the producer's count are
+      // zero), then the 4 quarters in order
+      const int t = threadIdx.x >> 2, qtr = threadIdx.x & 3;
+      float sum = 0.0f;
+      if (t < a.n_tok) {
+        const char *row = (const char *)red + t * 1024 + qtr * 256;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const f32x4 v = *(const f32x4 *)(row + ((j + t) & 15) * 16);
+          sum += (v[0] + v[1]) + (v[2] + v[3]);
+        }
+      }
+      sum += __shfl_xor(sum, 1, 64);
+      sum += __shfl_xor(sum, 2, 64);
+      if (t < a.n_tok && qtr == 0) sinv[t] = 1.0f / sqrtf(sum / (float)a.norm_dim + a.eps);
+      lds_barrier();  // the scales are visible, the reduction buffer is free
+    }
+    const float2 *rope = rope_lds ? (const float2 *)stage : a.rope;
+    const float *sh = (const float *)stage;                  // RESID_NORM residual blocks
+    const float *sg = (const float *)(stage + kStageGain);   // RESID_NORM gains
+    float *ssq = (float *)(stage + kStageSq);                // RESID_NORM [tile][token]
+    // Reduce the 8 waves' partial sums, TPR tiles (all token tiles of each)
+    // per LDS round, and run the epilogue on each finished (row pair, token).
+#pragma unroll
+    for (int t0 = 0; t0 < NT; t0 += TPR) {
+      if (t0 < n_here) {
+#pragma unroll
+        for (int tl = 0; tl < TPR; ++tl)
+          if (t0 + tl < NT)
+#pragma unroll
+            for (int tt = 0; tt < TT; ++tt) red[w][tl * TT + tt][lane] = acc[t0 + tl][tt];
+        lds_barrier();
+        const int tiles_here = n_here - t0 < TPR ? n_here - t0 : TPR;
+        const int items = tiles_here * TT * 128;
+        // items of one wave share a trip count (items is a multiple of 128)
+        for (int it = threadIdx.x; it < items; it += kGemmThreads) {
+          const int p = it & 7;
+          const int rest = it >> 3;
+          const int tl = rest / (TT * 16);
+          const int tok = rest - tl * (TT * 16);
+          const int tt = tok >> 4;
+          float sq = 0.0f;
+          if (tok < a.n_tok) {
+            const int l1 = (tok & 15) + 16 * (p >> 2), e1 = p & 3;
+            const int l2 = (tok & 15) + 16 * ((p + 8) >> 2), e2 = (p + 8) & 3;
+            float v1 = 0.f, v2 = 0.f;
+#pragma unroll
+            for (int ww = 0; ww < kGemmWaves; ++ww) {
+              v1 += red[ww][tl * TT + tt][l1][e1];
+              v2 += red[ww][tl * TT + tt][l2][e2];
+            }
+            if constexpr (EPI == EPI_RESID_NORM) {
+              sq = resid_norm(a, sh + ((tl * TT + tt) * 16 + (tok & 15)) * 16, sg + tl * 16,
+                              gb + t0 + tl, p, tok, v1, v2);
+            } else {
+              if (EPI == EPI_SWIGLU && a.ss_in) {
+                const float r = sinv[tok];
+                v1 *= r;
+                v2 *= r;
+              }
+              epilogue<EPI>(a, rope, split, gb + t0 + tl, p, tok, v1, v2);
+            }
+          }
+          if constexpr (EPI == EPI_RESID_NORM) {
+            // the 8 pairs of (tile, token): lanes 8m .. 8m + 7, fixed order
+            sq += __shfl_xor(sq, 1, 64);
+            sq += __shfl_xor(sq, 2, 64);
+            sq += __shfl_xor(sq, 4, 64);
+            if (p == 0) ssq[tl * (TT * 16) + tok] = sq;
+          }
+        }
+        lds_barrier();
+      }
+    }
+    if constexpr (EPI == EPI_RESID_NORM) {
+      // the group's sum of squares per token, its tiles in order
+      if ((int)threadIdx.x < a.n_tok) {
+        float sum = 0.0f;
+        for (int tl = 0; tl < n_here; ++tl) sum += ssq[tl * (TT * 16) + threadIdx.x];
+        a.ss[threadIdx.x * kSsGroups + grp] = sum;
+      }
+      // group 0 zeroes the row entries of groups that do not exist
+      if (grp == 0) {
+        const int gap = kSsGroups - a.groups;
+        for (int i = threadIdx.x; i < a.n_tok * gap; i += kGemmThreads)
+          a.ss[(i / gap) * kSsGroups + a.groups + i % gap] = 0.0f;
+      }
+      // the last group zeroes the packed columns past the width
+      if (grp == a.groups - 1) {
+        const int pad = a.xn_ks * 32 - a.out_rows;
+        for (int i = threadIdx.x; i < a.n_tok * pad; i += kGemmThreads)
+          a.xn[packed_index(i / pad, a.out_rows + i % pad, a.xn_ks)] = 0;
+      }
+    }
+  }
+  // a workgroup without tiles still owns its staging loads into LDS
+  if (t_lo >= t_hi) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+
+template <int EPI, int TT, int NT>
+hipError_t launch_tt_nt(const GemmArgs &a, int grid, hipStream_t s) {
+  if constexpr (NT > gemm_nt_cap(TT)) {
+    return hipErrorInvalidValue;
+  } else {
+    hipLaunchKernelGGL((k_gemm<EPI, TT, NT>), dim3(grid), dim3(kGemmThreads), 0, s, a);
+    return hipGetLastError();
+  }
+}
+
+template <int EPI, int TT>
+hipError_t launch_tt(const GemmArgs &a, int nt, int grid, hipStream_t s) {
+  switch (nt) {
+    case 1: return launch_tt_nt<EPI, TT, 1>(a, grid, s);
+    case 2: return launch_tt_nt<EPI, TT, 2>(a, grid, s);
+    case 3: return launch_tt_nt<EPI, TT, 3>(a, grid, s);
+    case 4: return launch_tt_nt<EPI, TT, 4>(a, grid, s);
+    case 6: return launch_tt_nt<EPI, TT, 6>(a, grid, s);
+    case 8: return launch_tt_nt<EPI, TT, 8>(a, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// Launch of a planned GEMM with epilogue EPI (the kernel for its token
+// tiles and tiles per pass).
+template <int EPI>
+hipError_t launch_epi(const GemmArgs &b, const GemmPlan &p, hipStream_t s) {
+  switch (p.tt) {
+    case 1: return launch_tt<EPI, 1>(b, p.nt, p.grid, s);
+    case 2: return launch_tt<EPI, 2>(b, p.nt, p.grid, s);
+    case 3: return launch_tt<EPI, 3>(b, p.nt, p.grid, s);
+    case 4: return launch_tt<EPI, 4>(b, p.nt, p.grid, s);
+    case 6: return launch_tt<EPI, 6>(b, p.nt, p.grid, s);
+    case 8: return launch_tt<EPI, 8>(b, p.nt, p.grid, s);
+    case 12: return launch_tt<EPI, 12>(b, p.nt, p.grid, s);
+    case 16: return launch_tt<EPI, 16>(b, p.nt, p.grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+}  // namespace sb

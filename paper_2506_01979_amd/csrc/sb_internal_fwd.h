@@ -8,7 +8,7 @@
 
 namespace sb {
 
-enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3, EPI_RESID_NORM = 4 };
 
 // Per-row tree metadata kept in the workspace.
 struct Meta {
@@ -104,7 +104,28 @@ struct GemmArgs {
   int cap, kv_len;
   int n_heads, n_kv, head_dim;
   const float2 *rope;  // [rows][head_dim/2]
+  // RESID_NORM (a residual projection fused with the following RMSNorm):
+  // h, fp32 [n_tok][out_rows], is the residual stream itself and is updated
+  // in place; the norm's input scaled by its gain, bf16(h * gain), is packed
+  // into xn (xn_ks k-steps); ss[t][group] (kSsGroups per row) receives the
+  // group's sum of h^2 over its rows for token t.
+  const float *gain;
+  uint16_t *xn;
+  int xn_ks;
+  float *ss;
+  // Consumer of a RESID_NORM launch (X = its xn): every output of token t
+  // is multiplied by 1 / sqrt(sum_{g < ss_groups} ss_in[t][g] / norm_dim + eps),
+  // the RMSNorm scale applied after the projection.  Null: X is normalised.
+  const float *ss_in;
+  int ss_groups, norm_dim;
+  float eps;
 };
+
+// Row stride of the per-(token, group) sums of squares of a RESID_NORM
+// launch (its largest group count).
+constexpr int kSsGroups = 256;
+// Largest token count of a RESID_NORM launch and its consumer.
+constexpr int kNormFuseRows = 128;
 
 struct AttnArgs {
   const void *q;        // bf16 or f32 [rows][n_heads][d]
@@ -127,12 +148,29 @@ hipError_t launch_rmsnorm_pack(float *h, const float *delta, int n_delta, const 
                                hipStream_t s);
 // Launch geometry of a GEMM: token tiles (rounded up to a kernel's), tiles per
 // pass, K split, tile groups and grid.
+// Largest tiles per pass of the GEMM kernel per token-tile count (its
+// register budget), and the (tile, token tile) accumulator pairs it reduces
+// per LDS round.
+constexpr int gemm_nt_cap(int tt) {
+  return tt <= 4 ? 8 : tt <= 6 ? 6 : tt <= 8 ? 4 : tt <= 12 ? 2 : 1;
+}
+constexpr int kRedPairs = 16;
 struct GemmPlan {
   int tt, nt, split, groups, grid;
 };
 GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok);
+// Launches of a planned GEMM, one per epilogue kind (k_gemm_*.hip).
+hipError_t launch_gemm_qkv(const GemmArgs &a, const GemmPlan &p, hipStream_t s);
+hipError_t launch_gemm_resid(const GemmArgs &a, const GemmPlan &p, hipStream_t s);
+hipError_t launch_gemm_swiglu(const GemmArgs &a, const GemmPlan &p, hipStream_t s);
+hipError_t launch_gemm_logits(const GemmArgs &a, const GemmPlan &p, hipStream_t s);
+hipError_t launch_gemm_resid_norm(const GemmArgs &a, const GemmPlan &p, hipStream_t s);
 // *split receives the K split used (the number of delta slices for RESID).
 hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int *split, hipStream_t s);
+// Whether a residual projection of `tiles` tiles over n_tok rows can run as
+// RESID_NORM (one pass, one reduction round, at most kSsGroups groups,
+// n_tok <= kNormFuseRows); *groups receives its group count.
+bool resid_norm_fusable(int tiles, int ks, int n_tok, int *groups);
 
 // k_attn.hip
 // Key ranges per KV head: about kAttnTargetGroups workgroups in all.
