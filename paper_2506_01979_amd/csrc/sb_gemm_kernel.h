@@ -31,50 +31,80 @@ __device__ __forceinline__ void rope_pair(float x1, float x2, float2 cs, float *
   *o2 = x2 * cs.x + x1 * cs.y;
 }
 
-// Epilogue of one finished output pair: rows p and p + 8 of tile `tile`,
-// activation row t < n_tok, values v1 / v2 (K range `split` of a split-K
-// launch).
+// Four floats to bf16 (round to nearest even), as one 8-byte word.
+__device__ __forceinline__ uint2 pack4_bf16(float x0, float x1, float x2, float x3) {
+  return make_uint2(f2bf(x0) | ((uint32_t)f2bf(x1) << 16), f2bf(x2) | ((uint32_t)f2bf(x3) << 16));
+}
+
+// Four consecutive floats row[d .. d + 3] (d a multiple of 4), only those
+// below n; one 16-byte store when the row is 16-byte aligned (n % 4 == 0).
+__device__ __forceinline__ void store4f(float *row, int d, int n, const f32x4 &v) {
+  if ((n & 3) == 0 && d + 3 < n) {
+    *(f32x4 *)(row + d) = v;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (d + i < n) row[d + i] = v[i];
+  }
+}
+
+// Epilogue of four finished output pairs of tile `tile`: rows p0 + i and
+// p0 + 8 + i (i < 4, p0 = 0 or 4), activation row t < n_tok, values v1[i] /
+// v2[i] (K range `split` of a split-K launch).
 template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs &a, const float2 *rope, int split,
-                                         int tile, int p, int t, float v1, float v2) {
+__device__ __forceinline__ void epilogue4(const GemmArgs &a, const float2 *rope, int split,
+                                          int tile, int p0, int t, const f32x4 &v1,
+                                          const f32x4 &v2) {
   if constexpr (EPI == EPI_QKV) {
     const int d = a.head_dim, ht = d / 16;
     const int qt = a.n_heads * ht, kt = a.n_kv * ht;
     if (tile < qt + kt) {
+      // a Q / K tile holds the RoPE pairs (j, j + d/2), j = 8u .. 8u + 7
       const bool isq = tile < qt;
       const int idx = isq ? tile : tile - qt;
       const int head = idx / ht, u = idx % ht;
-      const int j = 8 * u + p;
-      float o1, o2;
-      rope_pair(v1, v2, rope[t * (d / 2) + j], &o1, &o2);
+      const int j0 = 8 * u + p0;
+      const f32x4 c01 = *(const f32x4 *)(rope + t * (d / 2) + j0);
+      const f32x4 c23 = *(const f32x4 *)(rope + t * (d / 2) + j0 + 2);
+      float o1[4], o2[4];
+      rope_pair(v1[0], v2[0], make_float2(c01[0], c01[1]), &o1[0], &o2[0]);
+      rope_pair(v1[1], v2[1], make_float2(c01[2], c01[3]), &o1[1], &o2[1]);
+      rope_pair(v1[2], v2[2], make_float2(c23[0], c23[1]), &o1[2], &o2[2]);
+      rope_pair(v1[3], v2[3], make_float2(c23[2], c23[3]), &o1[3], &o2[3]);
       uint16_t *dst = isq ? a.q + ((size_t)t * a.n_heads + head) * d
                           : a.kc + ((size_t)head * a.cap + a.kv_len + t) * d;
-      dst[j] = f2bf(o1);
-      dst[j + d / 2] = f2bf(o2);
+      *(uint2 *)(dst + j0) = pack4_bf16(o1[0], o1[1], o1[2], o1[3]);
+      *(uint2 *)(dst + j0 + d / 2) = pack4_bf16(o2[0], o2[1], o2[2], o2[3]);
     } else {
       // V is cached transposed: [head][d][slot]
       const int idx = tile - qt - kt;
       const int head = idx / ht, u = idx % ht;
-      uint16_t *col = a.vc + ((size_t)head * d + 16 * u + p) * a.cap + a.kv_len + t;
-      col[0] = f2bf(v1);
-      col[(size_t)8 * a.cap] = f2bf(v2);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint16_t *col = a.vc + ((size_t)head * d + 16 * u + p0 + i) * a.cap + a.kv_len + t;
+        col[0] = f2bf(v1[i]);
+        col[(size_t)8 * a.cap] = f2bf(v2[i]);
+      }
     }
   } else if constexpr (EPI == EPI_RESID) {
     // the projection is stored as a delta (one slice per K range); the next
     // RMSNorm adds the slices to the residual stream
-    const int d1 = tile * 16 + p, d2 = d1 + 8;
     float *drow = a.h + ((size_t)split * a.n_tok + t) * a.out_rows;
-    if (d1 < a.out_rows) drow[d1] = v1;
-    if (d2 < a.out_rows) drow[d2] = v2;
+    store4f(drow, tile * 16 + p0, a.out_rows, v1);
+    store4f(drow, tile * 16 + p0 + 8, a.out_rows, v2);
   } else if constexpr (EPI == EPI_SWIGLU) {
-    const int f = tile * 8 + p;
-    const float gsil = v1 / (1.0f + expf(-v1));
-    a.act[packed_index(t, f, a.act_ks)] = f2bf(gsil * v2);
+    // rows p of a tile are gate rows, rows p + 8 the matching up rows;
+    // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (the
+    // result is rounded to bf16)
+    float o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      o[i] = v1[i] * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(v1[i] * -1.44269504f)) * v2[i];
+    *(uint2 *)(a.act + packed_index(t, tile * 8 + p0, a.act_ks)) = pack4_bf16(o[0], o[1], o[2], o[3]);
   } else if constexpr (EPI == EPI_LOGITS) {
-    const int v1i = tile * 16 + p, v2i = v1i + 8;
     float *lrow = a.logits + (size_t)t * a.out_rows;
-    if (v1i < a.out_rows) lrow[v1i] = v1;
-    if (v2i < a.out_rows) lrow[v2i] = v2;
+    store4f(lrow, tile * 16 + p0, a.out_rows, v1);
+    store4f(lrow, tile * 16 + p0 + 8, a.out_rows, v2);
   }
 }
 
@@ -116,25 +146,46 @@ __device__ __forceinline__ void lds_barrier() {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// RESID_NORM epilogue of one output pair (rows p, p + 8 of the tile, token
-// t): adds the projection to the residual (staged row hrow), stores it,
-// packs bf16(h * gain) for the next projection and returns the pair's sum
-// of squares.
-__device__ __forceinline__ float resid_norm(const GemmArgs &a, const float *hrow, const float *gain,
-                                            int tile, int p, int t, float v1, float v2) {
-  const int d1 = tile * 16 + p, d2 = d1 + 8;
-  const float h1 = hrow[p] + v1, h2 = hrow[p + 8] + v2;
-  float *hg = a.h + (size_t)t * a.out_rows;
+// RESID_NORM epilogue of four output pairs (rows p0 + i, p0 + 8 + i of the
+// tile, token t): adds the projection to the residual (staged row hrow),
+// stores it, packs bf16(h * gain) for the next projection and returns the
+// pairs' sum of squares.
+__device__ __forceinline__ float resid_norm4(const GemmArgs &a, const float *hrow,
+                                             const float *gain, int tile, int p0, int t,
+                                             const f32x4 &v1, const f32x4 &v2) {
+  const int n = a.out_rows;
+  const f32x4 h1 = *(const f32x4 *)(hrow + p0) + v1;
+  const f32x4 h2 = *(const f32x4 *)(hrow + p0 + 8) + v2;
+  const f32x4 g1 = *(const f32x4 *)(gain + p0);
+  const f32x4 g2 = *(const f32x4 *)(gain + p0 + 8);
+  float *hg = a.h + (size_t)t * n;
+  const int d1 = tile * 16 + p0, d2 = d1 + 8;
+  store4f(hg, d1, n, h1);
+  store4f(hg, d2, n, h2);
   float sq = 0.0f;
-  if (d1 < a.out_rows) {
-    hg[d1] = h1;
-    a.xn[packed_index(t, d1, a.xn_ks)] = f2bf(h1 * gain[p]);
-    sq = h1 * h1;
+  if (d1 + 3 < n) {
+    *(uint2 *)(a.xn + packed_index(t, d1, a.xn_ks)) =
+        pack4_bf16(h1[0] * g1[0], h1[1] * g1[1], h1[2] * g1[2], h1[3] * g1[3]);
+    sq = (h1[0] * h1[0] + h1[1] * h1[1]) + (h1[2] * h1[2] + h1[3] * h1[3]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (d1 + i < n) {
+        a.xn[packed_index(t, d1 + i, a.xn_ks)] = f2bf(h1[i] * g1[i]);
+        sq += h1[i] * h1[i];
+      }
   }
-  if (d2 < a.out_rows) {
-    hg[d2] = h2;
-    a.xn[packed_index(t, d2, a.xn_ks)] = f2bf(h2 * gain[p + 8]);
-    sq += h2 * h2;
+  if (d2 + 3 < n) {
+    *(uint2 *)(a.xn + packed_index(t, d2, a.xn_ks)) =
+        pack4_bf16(h2[0] * g2[0], h2[1] * g2[1], h2[2] * g2[2], h2[3] * g2[3]);
+    sq += (h2[0] * h2[0] + h2[1] * h2[1]) + (h2[2] * h2[2] + h2[3] * h2[3]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (d2 + i < n) {
+        a.xn[packed_index(t, d2 + i, a.xn_ks)] = f2bf(h2[i] * g2[i]);
+        sq += h2[i] * h2[i];
+      }
   }
   return sq;
 }
@@ -315,42 +366,41 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
             for (int tt = 0; tt < TT; ++tt) red[w][tl * TT + tt][lane] = acc[t0 + tl][tt];
         lds_barrier();
         const int tiles_here = n_here - t0 < TPR ? n_here - t0 : TPR;
-        const int items = tiles_here * TT * 128;
-        // items of one wave share a trip count (items is a multiple of 128)
+        // An item is (accumulator pair, token, g): lanes l1 = token + 16 g and
+        // l1 + 32 of the 8 waves' accumulators hold rows 4g .. 4g + 3 and
+        // 4g + 8 .. 4g + 11 of the token's column, i.e. the output pairs
+        // (p, p + 8) for p = 4g .. 4g + 3.  Items of a 32-lane half-wave
+        // share a trip count (items is a multiple of 32).
+        const int items = tiles_here * TT * 32;
         for (int it = threadIdx.x; it < items; it += kGemmThreads) {
-          const int p = it & 7;
-          const int rest = it >> 3;
-          const int tl = rest / (TT * 16);
-          const int tok = rest - tl * (TT * 16);
-          const int tt = tok >> 4;
+          const int tok16 = it & 15, g = (it >> 4) & 1, pr = it >> 5;
+          const int tl = pr / TT, tt = pr - tl * TT;
+          const int tok = tt * 16 + tok16;
           float sq = 0.0f;
           if (tok < a.n_tok) {
-            const int l1 = (tok & 15) + 16 * (p >> 2), e1 = p & 3;
-            const int l2 = (tok & 15) + 16 * ((p + 8) >> 2), e2 = (p + 8) & 3;
-            float v1 = 0.f, v2 = 0.f;
+            const int l1 = tok16 + 16 * g;
+            f32x4 v1 = red[0][pr][l1], v2 = red[0][pr][l1 + 32];
 #pragma unroll
-            for (int ww = 0; ww < kGemmWaves; ++ww) {
-              v1 += red[ww][tl * TT + tt][l1][e1];
-              v2 += red[ww][tl * TT + tt][l2][e2];
+            for (int ww = 1; ww < kGemmWaves; ++ww) {
+              v1 += red[ww][pr][l1];
+              v2 += red[ww][pr][l1 + 32];
             }
             if constexpr (EPI == EPI_RESID_NORM) {
-              sq = resid_norm(a, sh + ((tl * TT + tt) * 16 + (tok & 15)) * 16, sg + tl * 16,
-                              gb + t0 + tl, p, tok, v1, v2);
+              sq = resid_norm4(a, sh + (pr * 16 + tok16) * 16, sg + tl * 16, gb + t0 + tl, 4 * g,
+                               tok, v1, v2);
             } else {
               if (EPI == EPI_SWIGLU && a.ss_in) {
                 const float r = sinv[tok];
                 v1 *= r;
                 v2 *= r;
               }
-              epilogue<EPI>(a, rope, split, gb + t0 + tl, p, tok, v1, v2);
+              epilogue4<EPI>(a, rope, split, gb + t0 + tl, 4 * g, tok, v1, v2);
             }
           }
           if constexpr (EPI == EPI_RESID_NORM) {
-            // the 8 pairs of (tile, token): lanes 8m .. 8m + 7, fixed order
-            sq += __shfl_xor(sq, 1, 64);
-            sq += __shfl_xor(sq, 2, 64);
-            sq += __shfl_xor(sq, 4, 64);
-            if (p == 0) ssq[tl * (TT * 16) + tok] = sq;
+            // the two halves (g = 0, 1) of (tile, token): lanes it, it ^ 16
+            sq += __shfl_xor(sq, 16, 64);
+            if (g == 0) ssq[tl * (TT * 16) + tok] = sq;
           }
         }
         lds_barrier();
