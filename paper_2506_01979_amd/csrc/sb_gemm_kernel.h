@@ -201,7 +201,13 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
   const int lane = threadIdx.x & 63;
   const int ks = a.ks;
   const int S = a.split;
-  const int split = blockIdx.x % S, grp = blockIdx.x / S;
+  // Workgroups are dispatched round-robin over the 8 XCDs (block b runs on
+  // XCD b % 8).  Work unit u = (tile group, K range) is numbered XCD-major,
+  // so each XCD streams one contiguous eighth of the weights: the XCDs move
+  // equal bytes even when the groups' tile counts differ by one.
+  const int nb = gridDim.x;
+  const int u = (nb & 7) == 0 ? (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+  const int split = u % S, grp = u / S;
   const int t_lo = (int)(((long long)a.tiles * grp) / a.groups);
   const int t_hi = (int)(((long long)a.tiles * (grp + 1)) / a.groups);
   const int nc = ks >> 3;
