@@ -92,6 +92,9 @@ SHAPES = {
     "small_bf16": Shape("small_bf16", 2, 256, 4, 4, 64, 688, 1000, "bf16"),
     "small_gqa_bf16": Shape("small_gqa_bf16", 2, 512, 8, 2, 64, 1376, 1000, "bf16"),
     "small_h128_bf16": Shape("small_h128_bf16", 2, 512, 4, 4, 128, 1024, 2048, "bf16"),
+    # ragged everywhere: hidden 328 (not a multiple of 16 or 256; != heads x
+    # head_dim), ffn 600, vocabulary 1001 (odd)
+    "ragged_bf16": Shape("ragged_bf16", 2, 328, 4, 2, 64, 600, 1001, "bf16"),
 }
 
 WORKLOADS = {

@@ -4,8 +4,10 @@ Logits must match per row within 1e-4 (float32 models, against the float64
 oracle) or 2e-2 (bfloat16 models, against the oracle's bfloat16 emulation)
 relative to the row's largest logit; the K/V the step writes for the tree
 rows must match to the same bound.  Shapes span several GEMM tiles, ragged K
-(ffn 688), ragged vocabularies (1000), ragged attention chunks, GQA, both
-head widths and 5..129-row trees.  Invariant (a) -- branch-masked rows equal
+(ffn 688, 600), ragged vocabularies (1000, 1001), a hidden width that is not
+a multiple of 16 (328), ragged attention chunks, GQA, both head widths and
+5..137-row trees (the O projection applies the post-attention RMSNorm up to
+128 rows and hands it to a separate kernel above).  Invariant (a) -- branch-masked rows equal
 each branch run alone -- is checked on the GPU path too.
 """
 import numpy as np
@@ -74,6 +76,8 @@ CASES = [
     ("small_gqa_bf16", 300, ("branch", 4, 8)),
     ("small_h128_bf16", 200, ("branch", 8, 16)),
     ("small_bf16", 1, ("chain", 40)),
+    ("ragged_bf16", 300, ("branch", 4, 8)),
+    ("ragged_bf16", 90, ("branch", 8, 17)),
 ]
 
 
