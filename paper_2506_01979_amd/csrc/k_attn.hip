@@ -425,6 +425,87 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, uint16_t *__rest
   }
 }
 
+// A pointer the compiler is told is the same in every lane (kept in scalar
+// registers, so a buffer descriptor built from it needs no per-lane loop).
+__device__ __forceinline__ void *uniform_ptr(const void *p) {
+  const unsigned long long v = (unsigned long long)p;
+  const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)v);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(v >> 32));
+  return (void *)(((unsigned long long)hi << 32) | lo);
+}
+
+// Merge for few key ranges (nc <= NCM): one thread per (row t, query head,
+// 8 output dimensions).  Every load -- the range statistics and the 8
+// dimensions of every range's partial output -- goes out before any use
+// (one memory round trip); the thread writes its 8 dimensions as one
+// 16-byte word of the packed operand layout of the O projection.
+template <int D, int NCM>
+__global__ __launch_bounds__(256) void k_attn_merge_reg(AttnArgs a, uint16_t *__restrict__ out,
+                                                        int ks) {
+  constexpr int TPP = D / 8;  // threads per (row, head)
+  const int nc = a.n_chunks;
+  const int G = a.n_heads / a.n_kv;
+  const int R = a.n_tok * G;
+  // wave-uniform descriptors of the whole partial buffers; every load is
+  // branch-free (ranges c >= nc and threads past the last (row, head) point
+  // past the end and read zero)
+  const int mbytes = __builtin_amdgcn_readfirstlane(a.n_kv * nc * R * 8);
+  const int obytes = __builtin_amdgcn_readfirstlane(a.n_kv * nc * R * D * 4);
+  const __amdgpu_buffer_rsrc_t mrs =
+      __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(a.part_ml), 0, mbytes, kBufferDword3);
+  const __amdgpu_buffer_rsrc_t ors =
+      __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(a.part_o), 0, obytes, kBufferDword3);
+  const int gid = blockIdx.x * 256 + threadIdx.x;
+  const int pair = gid / TPP, part = gid - pair * TPP;
+  const bool live = pair < a.n_tok * a.n_heads;
+  const int t = pair / a.n_heads, head = pair - t * a.n_heads;
+  const int g = head / G;
+  const int r = t * G + (head - g * G);
+  float2 st[NCM];
+  f32x4 lo[NCM], hi[NCM];
+#pragma unroll
+  for (int c = 0; c < NCM; ++c) {
+    const int row = (g * nc + c) * R + r;
+    const bool in = live && c < nc;
+    const int mo = in ? row * 8 : mbytes;
+    const int oo = in ? (row * D + part * 8) * 4 : obytes;
+    st[c].x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(mrs, mo, 0, 0));
+    st[c].y = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(mrs, mo + 4, 0, 0));
+    lo[c] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ors, oo, 0, 0));
+    hi[c] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ors, oo + 16, 0, 0));
+  }
+  __builtin_amdgcn_sched_barrier(0);  // all loads issued before any use
+#pragma unroll
+  for (int c = 0; c < NCM; ++c)
+    if (c >= nc) st[c].x = -INFINITY;
+  float M = st[0].x;
+#pragma unroll
+  for (int c = 1; c < NCM; ++c) M = fmaxf(M, st[c].x);
+  float L = 0.0f;
+  f32x4 o0 = {0.f, 0.f, 0.f, 0.f}, o1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NCM; ++c) {
+    const float wgt = st[c].x == -INFINITY ? 0.0f : expf(st[c].x - M);
+    L += wgt * st[c].y;
+    o0 += wgt * lo[c];
+    o1 += wgt * hi[c];
+  }
+  const float inv = 1.0f / L;
+  uint4 pk;
+  pk.x = f2bf(o0[0] * inv) | ((uint32_t)f2bf(o0[1] * inv) << 16);
+  pk.y = f2bf(o0[2] * inv) | ((uint32_t)f2bf(o0[3] * inv) << 16);
+  pk.z = f2bf(o1[0] * inv) | ((uint32_t)f2bf(o1[1] * inv) << 16);
+  pk.w = f2bf(o1[2] * inv) | ((uint32_t)f2bf(o1[3] * inv) << 16);
+  if (!live) return;
+  *(uint4 *)(out + packed_index(t, head * D + part * 8, ks)) = pk;
+  // the last head's threads clear the row's padding columns (the GEMM
+  // reads K in whole chunks)
+  if (head == a.n_heads - 1) {
+    for (int k0 = a.n_heads * D + part * 8; k0 < ks * 32; k0 += TPP * 8)
+      *(uint4 *)(out + packed_index(t, k0, ks)) = make_uint4(0, 0, 0, 0);
+  }
+}
+
 }  // namespace
 
 int attn_splits(int n_kv, int head_dim, int nkeys) {
@@ -465,6 +546,22 @@ hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s) {
 hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,
                                   hipStream_t s) {
   if (a.n_chunks > 512) return hipErrorInvalidValue;
+  if (a.n_chunks <= 16 && (a.head_dim == 128 || a.head_dim == 64)) {
+    const int threads = a.n_tok * a.n_heads * (a.head_dim / 8);
+    const dim3 g((threads + 255) / 256);
+    if (a.head_dim == 128) {
+      if (a.n_chunks <= 8)
+        hipLaunchKernelGGL((k_attn_merge_reg<128, 8>), g, dim3(256), 0, s, a, out_packed, out_ks);
+      else
+        hipLaunchKernelGGL((k_attn_merge_reg<128, 16>), g, dim3(256), 0, s, a, out_packed, out_ks);
+    } else {
+      if (a.n_chunks <= 8)
+        hipLaunchKernelGGL((k_attn_merge_reg<64, 8>), g, dim3(256), 0, s, a, out_packed, out_ks);
+      else
+        hipLaunchKernelGGL((k_attn_merge_reg<64, 16>), g, dim3(256), 0, s, a, out_packed, out_ks);
+    }
+    return hipGetLastError();
+  }
   dim3 grid(a.n_tok, a.n_heads);
   if (a.head_dim == 128)
     hipLaunchKernelGGL(k_attn_merge<128>, grid, dim3(256), 0, s, a, out_packed, out_ks);
