@@ -425,6 +425,10 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, uint16_t *__rest
   }
 }
 
+// Threads per workgroup of the register merge: one wave, so that the few
+// thousand threads of a step spread over many compute units.
+constexpr int kMergeThreads = 64;
+
 // A pointer the compiler is told is the same in every lane (kept in scalar
 // registers, so a buffer descriptor built from it needs no per-lane loop).
 __device__ __forceinline__ void *uniform_ptr(const void *p) {
@@ -440,8 +444,8 @@ __device__ __forceinline__ void *uniform_ptr(const void *p) {
 // (one memory round trip); the thread writes its 8 dimensions as one
 // 16-byte word of the packed operand layout of the O projection.
 template <int D, int NCM>
-__global__ __launch_bounds__(256) void k_attn_merge_reg(AttnArgs a, uint16_t *__restrict__ out,
-                                                        int ks) {
+__global__ __launch_bounds__(kMergeThreads) void k_attn_merge_reg(AttnArgs a,
+                                                                  uint16_t *__restrict__ out, int ks) {
   constexpr int TPP = D / 8;  // threads per (row, head)
   const int nc = a.n_chunks;
   const int G = a.n_heads / a.n_kv;
@@ -455,7 +459,7 @@ __global__ __launch_bounds__(256) void k_attn_merge_reg(AttnArgs a, uint16_t *__
       __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(a.part_ml), 0, mbytes, kBufferDword3);
   const __amdgpu_buffer_rsrc_t ors =
       __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(a.part_o), 0, obytes, kBufferDword3);
-  const int gid = blockIdx.x * 256 + threadIdx.x;
+  const int gid = blockIdx.x * kMergeThreads + threadIdx.x;
   const int pair = gid / TPP, part = gid - pair * TPP;
   const bool live = pair < a.n_tok * a.n_heads;
   const int t = pair / a.n_heads, head = pair - t * a.n_heads;
@@ -548,17 +552,17 @@ hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int o
   if (a.n_chunks > 512) return hipErrorInvalidValue;
   if (a.n_chunks <= 16 && (a.head_dim == 128 || a.head_dim == 64)) {
     const int threads = a.n_tok * a.n_heads * (a.head_dim / 8);
-    const dim3 g((threads + 255) / 256);
+    const dim3 g((threads + kMergeThreads - 1) / kMergeThreads), b(kMergeThreads);
     if (a.head_dim == 128) {
       if (a.n_chunks <= 8)
-        hipLaunchKernelGGL((k_attn_merge_reg<128, 8>), g, dim3(256), 0, s, a, out_packed, out_ks);
+        hipLaunchKernelGGL((k_attn_merge_reg<128, 8>), g, b, 0, s, a, out_packed, out_ks);
       else
-        hipLaunchKernelGGL((k_attn_merge_reg<128, 16>), g, dim3(256), 0, s, a, out_packed, out_ks);
+        hipLaunchKernelGGL((k_attn_merge_reg<128, 16>), g, b, 0, s, a, out_packed, out_ks);
     } else {
       if (a.n_chunks <= 8)
-        hipLaunchKernelGGL((k_attn_merge_reg<64, 8>), g, dim3(256), 0, s, a, out_packed, out_ks);
+        hipLaunchKernelGGL((k_attn_merge_reg<64, 8>), g, b, 0, s, a, out_packed, out_ks);
       else
-        hipLaunchKernelGGL((k_attn_merge_reg<64, 16>), g, dim3(256), 0, s, a, out_packed, out_ks);
+        hipLaunchKernelGGL((k_attn_merge_reg<64, 16>), g, b, 0, s, a, out_packed, out_ks);
     }
     return hipGetLastError();
   }
