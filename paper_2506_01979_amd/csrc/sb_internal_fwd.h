@@ -174,7 +174,7 @@ bool resid_norm_fusable(int tiles, int ks, int n_tok, int *groups);
 
 // k_attn.hip
 // Key ranges per KV head: about kAttnTargetGroups workgroups in all.
-constexpr int kAttnTargetGroups = 256;
+constexpr int kAttnTargetGroups = 192;
 int attn_splits(int n_kv, int head_dim, int nkeys);
 hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s);
 hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,
