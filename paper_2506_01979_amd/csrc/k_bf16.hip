@@ -130,16 +130,23 @@ __global__ __launch_bounds__(256) void k_embed_meta(EmbedArgs a, TreeArg tree) {
   } else {
     for (int k = threadIdx.x; k < a.hidden; k += blockDim.x) h[k] = 0.0f;
   }
-  // this row's depth, position and ancestor mask, then its RoPE angles
+  // this row's depth, position and ancestor mask, then its RoPE angles.
+  // The tree (kernel arguments: a dynamically indexed read is a memory
+  // access) goes to LDS in one parallel copy before the parent chase.
   __shared__ int s_pos;
+  __shared__ int16_t s_par[SB_MAX_ROWS];
+  for (int i = threadIdx.x; i < tree.n; i += blockDim.x) s_par[i] = tree.parent[i];
+  __syncthreads();
   if (threadIdx.x == 0) {
     uint32_t m[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int depth = 0;
     if (t < tree.n) {
       int j = t;
       for (int guard = 0; guard < SB_MAX_ROWS && j >= 0; ++guard) {
-        m[j >> 5] |= 1u << (j & 31);
-        j = tree.parent[j];
+#pragma unroll
+        for (int w = 0; w < 8; ++w)
+          if (w == (j >> 5)) m[w] |= 1u << (j & 31);
+        j = s_par[j];
         if (j >= 0) ++depth;
       }
     }

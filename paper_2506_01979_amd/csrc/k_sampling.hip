@@ -596,20 +596,26 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
   __shared__ sb_row_stats s_st[SB_MAX_ROWS];
   __shared__ double s_px[SB_MAX_ROWS];
   __shared__ float s_qx[SB_MAX_ROWS];
+  __shared__ int16_t s_par[SB_MAX_ROWS];
   const int n = tree.n;
   double *ws0 = ws;
   double *ws1 = ws + vocab;
   if (threadIdx.x == 0) s_flags = 0;
-  // every row's statistics, then in parallel every row's test values: p of
-  // its parent at its token and q at its token (the walk's chain tests then
-  // read LDS instead of paying a memory round trip each)
-  if ((int)threadIdx.x < n) s_st[threadIdx.x] = stats[threadIdx.x];
+  // the tree (kernel arguments: every dynamically indexed read is a memory
+  // access) and every row's statistics into LDS, then in parallel every
+  // row's test values: p of its parent at its token and q at its token (the
+  // walk's chain tests then read LDS instead of paying a memory round trip
+  // each)
+  if ((int)threadIdx.x < n) {
+    s_par[threadIdx.x] = tree.parent[threadIdx.x];
+    s_st[threadIdx.x] = stats[threadIdx.x];
+  }
   __syncthreads();
   if ((int)threadIdx.x < n && isnan(s_st[threadIdx.x].total)) atomicOr(&s_flags, SB_FLAG_NONFINITE);
   if ((int)threadIdx.x >= 1 && (int)threadIdx.x < n) {
     const int i = threadIdx.x;
     const int x = tokens[i];
-    const int par = tree.parent[i];
+    const int par = s_par[i];
     double px = 0.0;
     float qx = 0.0f;
     if (x >= 0 && x < vocab) {
@@ -632,7 +638,7 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
     if (threadIdx.x == 0) {
       int c = 0;
       for (int j = node + 1; j < n; ++j)
-        if (tree.parent[j] == node) kids[c++] = (int16_t)j;
+        if (s_par[j] == node) kids[c++] = (int16_t)j;
       nk = c;
     }
     __syncthreads();
@@ -661,7 +667,7 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
     if (plen > 1) {
       int ord = 0;
       for (int j = 1; j < path[1]; ++j)
-        if (tree.parent[j] == 0) ++ord;
+        if (s_par[j] == 0) ++ord;
       branch = ord;
     }
     result->n_accepted = plen - 1;
