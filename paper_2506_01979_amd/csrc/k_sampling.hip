@@ -597,6 +597,7 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
   __shared__ double s_px[SB_MAX_ROWS];
   __shared__ float s_qx[SB_MAX_ROWS];
   __shared__ int16_t s_par[SB_MAX_ROWS];
+  __shared__ unsigned long long s_kmask[(SB_MAX_ROWS + 63) / 64];
   const int n = tree.n;
   double *ws0 = ws;
   double *ws1 = ws + vocab;
@@ -635,10 +636,23 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
   int y = 0;
   int bonus = 0;
   for (;;) {
+    // the children of `node` in index order: one ballot per wave over the
+    // rows, then thread 0 lists the set bits
+    {
+      const int j = threadIdx.x;
+      const unsigned long long m = __ballot(j > node && j < n && s_par[j] == node);
+      if ((j & 63) == 0 && j < SB_MAX_ROWS) s_kmask[j >> 6] = m;
+    }
+    __syncthreads();
     if (threadIdx.x == 0) {
       int c = 0;
-      for (int j = node + 1; j < n; ++j)
-        if (s_par[j] == node) kids[c++] = (int16_t)j;
+      for (int wv = 0; wv * 64 < n; ++wv) {
+        unsigned long long m = s_kmask[wv];
+        while (m) {
+          kids[c++] = (int16_t)(wv * 64 + __ffsll((long long)m) - 1);
+          m &= m - 1;
+        }
+      }
       nk = c;
     }
     __syncthreads();
