@@ -149,6 +149,7 @@ struct Shared {
   int ired[kWaves + 1];
   int decision;
   double z;
+  double rcap;  // residual at the token a pass was asked to capture
 };
 
 // Elements of a vocabulary pass handled per thread per batch: their loads are
@@ -156,9 +157,11 @@ struct Shared {
 constexpr int kBatch = 16;
 
 // After candidate with draft row q is rejected: r = max(0, p~ - q) into
-// dst; returns Z = sum r (all threads).  The new p~ is r / Z.
+// dst; returns Z = sum r (all threads).  The new p~ is r / Z.  r at token
+// xcap (the next candidate's, or -1) is also left in sh.rcap, so the next
+// test needs no memory round trip.
 __device__ double residual_pass(const Dist &cur, const float *q, int vocab, double *dst,
-                                Shared &sh) {
+                                int xcap, Shared &sh) {
   double part = 0.0;
   const double rcp = cur.recip();
   for (int v0 = threadIdx.x; v0 < vocab; v0 += kBatch * kWalkThreads) {
@@ -178,6 +181,7 @@ __device__ double residual_pass(const Dist &cur, const float *q, int vocab, doub
       if (v < vocab) {
         dst[v] = r;
         part += r;
+        if (v == xcap) sh.rcap = r;
       }
     }
   }
@@ -281,15 +285,18 @@ __device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
 template <class Cand>
 __device__ int node_select(Dist *cur, const Cand &cand, int n_cand, int vocab, double *ws0,
                            double *ws1, int *flags, int *nrej, Shared &sh) {
+  bool captured = false;  // p~(tok(i)) is sh.rcap / cur->zdiv
   for (int i = 0; i < n_cand; ++i) {
     if (threadIdx.x == 0) {
       const int x = cand.tok(i);
       double ratio = 0.0;  // a token id outside the vocabulary is rejected
       if (x >= 0 && x < vocab) {
-        // p~(x) and q(x): gathered up front while p~ is still the row itself
-        const double qx = (double)(cur->arr ? cand.q(i)[x] : cand.qx(i));
+        // q(x) gathered up front; p~(x) gathered up front while p~ is still
+        // the row itself, else captured by the last residual pass
+        const double qx = (double)cand.qx(i);
         if (qx == 0.0) *flags |= SB_FLAG_QZERO;
-        ratio = (cur->arr ? cur->at(x) : cand.px(i)) / qx;
+        const double px = !cur->arr ? cand.px(i) : captured ? sh.rcap / cur->zdiv : cur->at(x);
+        ratio = px / qx;
       } else {
         *flags |= SB_FLAG_QZERO;
       }
@@ -301,10 +308,14 @@ __device__ int node_select(Dist *cur, const Cand &cand, int n_cand, int vocab, d
     if (acc) return i;
     ++*nrej;
     double *dst = (cur->arr == ws0) ? ws1 : ws0;
-    double Z = residual_pass(*cur, cand.q(i), vocab, dst, sh);
+    const int xn = i + 1 < n_cand ? cand.tok(i + 1) : -1;
+    const int xcap = xn >= 0 && xn < vocab ? xn : -1;
+    double Z = residual_pass(*cur, cand.q(i), vocab, dst, xcap, sh);
+    captured = false;
     if (Z > 0.0) {
       cur->arr = dst;
       cur->zdiv = Z;
+      captured = xcap >= 0;
     } else if (threadIdx.x == 0) {
       *flags |= SB_FLAG_ZERO_RESIDUAL;
     }
@@ -598,6 +609,8 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
   __shared__ float s_qx[SB_MAX_ROWS];
   __shared__ int16_t s_par[SB_MAX_ROWS];
   __shared__ unsigned long long s_kmask[(SB_MAX_ROWS + 63) / 64];
+  __shared__ int32_t s_tok[SB_MAX_ROWS];
+  __shared__ float s_u[SB_MAX_ROWS];
   const int n = tree.n;
   double *ws0 = ws;
   double *ws1 = ws + vocab;
@@ -610,6 +623,8 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
   if ((int)threadIdx.x < n) {
     s_par[threadIdx.x] = tree.parent[threadIdx.x];
     s_st[threadIdx.x] = stats[threadIdx.x];
+    s_tok[threadIdx.x] = tokens[threadIdx.x];
+    s_u[threadIdx.x] = u[threadIdx.x];
   }
   __syncthreads();
   if ((int)threadIdx.x < n && isnan(s_st[threadIdx.x].total)) atomicOr(&s_flags, SB_FLAG_NONFINITE);
@@ -662,7 +677,7 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
       y = draw_pass(cur, u[0], vocab, sh);
       break;
     }
-    ChildCands cc{kids, tokens, q, u, vocab, s_px, s_qx};
+    ChildCands cc{kids, s_tok, q, s_u, vocab, s_px, s_qx};
     const int acc = node_select(&cur, cc, nkids, vocab, ws0, ws1, &flags, &nrej, sh);
     if (acc >= 0) {
       node = kids[acc];
