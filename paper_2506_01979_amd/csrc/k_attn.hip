@@ -429,15 +429,6 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, uint16_t *__rest
 // thousand threads of a step spread over many compute units.
 constexpr int kMergeThreads = 64;
 
-// A pointer the compiler is told is the same in every lane (kept in scalar
-// registers, so a buffer descriptor built from it needs no per-lane loop).
-__device__ __forceinline__ void *uniform_ptr(const void *p) {
-  const unsigned long long v = (unsigned long long)p;
-  const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)v);
-  const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(v >> 32));
-  return (void *)(((unsigned long long)hi << 32) | lo);
-}
-
 // Merge for few key ranges (nc <= NCM): one thread per (row t, query head,
 // 8 output dimensions).  Every load -- the range statistics and the 8
 // dimensions of every range's partial output -- goes out before any use

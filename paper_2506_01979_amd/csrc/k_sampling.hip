@@ -130,6 +130,44 @@ struct Dist {
   }
 };
 
+// p~ at K tokens v[k] (invalid: v outside [0, vocab), reads as 0), the loads
+// of all K issued together through wave-uniform buffer descriptors (no
+// branch per element), then converted as at_fast() does.
+template <int K>
+__device__ __forceinline__ void load_p(const Dist &d, const int (&v)[K], int vocab, double rcp,
+                                       double (&out)[K]) {
+  if (d.arr) {
+    const __amdgpu_buffer_rsrc_t rs = uniform_rsrc(d.arr, vocab * 8);
+    uint32_t lo[K], hi[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int off = (v[k] >= 0 && v[k] < vocab) ? v[k] * 8 : vocab * 8;
+      lo[k] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+      hi[k] = __builtin_amdgcn_raw_buffer_load_b32(rs, off + 4, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+      out[k] = __builtin_bit_cast(double, ((uint64_t)hi[k] << 32) | lo[k]) * rcp;
+  } else if (d.greedy) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) out[k] = v[k] == d.argmax ? 1.0 : 0.0;
+  } else {
+    const __amdgpu_buffer_rsrc_t rs = uniform_rsrc(d.l, vocab * 4);
+    float raw[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int off = (v[k] >= 0 && v[k] < vocab) ? v[k] * 4 : vocab * 4;
+      raw[k] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const float z = raw[k] * d.inv_t;
+      const double p = (double)expf(z - d.zmax) * rcp;
+      out[k] = (v[k] >= 0 && v[k] < vocab) ? p : 0.0;
+    }
+  }
+}
+
 __device__ __forceinline__ Dist row_dist(const float *l, const sb_row_stats &st, float inv_t,
                                          int greedy) {
   Dist d;
@@ -164,15 +202,18 @@ __device__ double residual_pass(const Dist &cur, const float *q, int vocab, doub
                                 int xcap, Shared &sh) {
   double part = 0.0;
   const double rcp = cur.recip();
+  const __amdgpu_buffer_rsrc_t qrs = uniform_rsrc(q, vocab * 4);
   for (int v0 = threadIdx.x; v0 < vocab; v0 += kBatch * kWalkThreads) {
+    int vv[kBatch];
     float qv[kBatch];
     double pv[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
-      const int v = v0 + j * kWalkThreads;
-      qv[j] = v < vocab ? q[v] : 0.0f;
-      pv[j] = v < vocab ? cur.at_fast(v, rcp) : 0.0;
+      vv[j] = v0 + j * kWalkThreads;
+      qv[j] = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(qrs, (vv[j] < vocab ? vv[j] : vocab) * 4, 0, 0));
     }
+    load_p<kBatch>(cur, vv, vocab, rcp, pv);
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const int v = v0 + j * kWalkThreads;
@@ -202,9 +243,11 @@ __device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
   const double rcp = d.recip();
   double part = 0.0;
   for (int v0 = lo + lane; v0 < hi; v0 += 64 * kBatch) {
+    int vv[kBatch];
     double x[kBatch];
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) x[j] = (v0 + 64 * j < hi) ? d.at_fast(v0 + 64 * j, rcp) : 0.0;
+    for (int j = 0; j < kBatch; ++j) vv[j] = v0 + 64 * j < hi ? v0 + 64 * j : -1;
+    load_p<kBatch>(d, vv, vocab, rcp, x);
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) part += x[j];
   }
@@ -231,13 +274,14 @@ __device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
   if (lo < hi && seg_end > thr) {
     for (int b0 = lo; b0 < hi && cand == INT_MAX; b0 += 512) {
       const int e0 = b0 + 8 * lane;
+      int vv[8];
       double x[8];
       double ls = 0.0;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        x[e] = (e0 + e < hi) ? d.at_fast(e0 + e, rcp) : 0.0;
-        ls += x[e];
-      }
+      for (int e = 0; e < 8; ++e) vv[e] = e0 + e < hi ? e0 + e : -1;
+      load_p<8>(d, vv, vocab, rcp, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ls += x[e];
       double inc = ls;
       for (int o = 1; o < 64; o <<= 1) {
         const double y = __shfl_up(inc, o, 64);

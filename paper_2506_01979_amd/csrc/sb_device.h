@@ -16,6 +16,22 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 constexpr int kBufferDword3 = 0x00020000;
 constexpr int kNonTemporal = 2;
 
+// A pointer the compiler is told is the same in every lane (kept in scalar
+// registers, so a buffer descriptor built from it needs no per-lane loop).
+__device__ __forceinline__ void *uniform_ptr(const void *p) {
+  const unsigned long long v = (unsigned long long)p;
+  const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)v);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(v >> 32));
+  return (void *)(((unsigned long long)hi << 32) | lo);
+}
+
+// Buffer descriptor of `bytes` bytes at p, both wave-uniform: loads through
+// it at offsets >= bytes read zero (branch-free bounds).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void *p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(p), 0, __builtin_amdgcn_readfirstlane(bytes),
+                                           kBufferDword3);
+}
+
 // 16-byte streaming load (data read once: weights)
 __device__ __forceinline__ uint4 load_stream(const uint4 *p) {
   u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
