@@ -171,6 +171,9 @@ __global__ __launch_bounds__(256) void k_embed_meta(EmbedArgs a, TreeArg tree) {
 // RMSNorm of the fp32 residual rows into the packed bf16 operand layout
 // ---------------------------------------------------------------------------
 
+// Threads per row of the RMSNorm kernel.
+constexpr int kNormThreads = 512;
+
 // One workgroup per row; a thread holds IPT groups of 8 columns in registers
 // (one read of the row), the sum of squares is reduced across the block, and
 // each group is written as one 16-byte store.
@@ -183,14 +186,15 @@ __global__ __launch_bounds__(256) void k_embed_meta(EmbedArgs a, TreeArg tree) {
 // trip; slices past n_delta, columns past hidden and rows past n_tok read
 // zero (out-of-range offsets).
 template <int IPT>
-__global__ __launch_bounds__(256) void k_rmsnorm_pack(float *__restrict__ h,
-                                                      const float *__restrict__ delta,
-                                                      int n_delta,
-                                                      const float *__restrict__ g, int hidden,
-                                                      int ks, int n_tok, float eps,
-                                                      uint16_t *__restrict__ out) {
+__global__ __launch_bounds__(kNormThreads) void k_rmsnorm_pack(float *__restrict__ h,
+                                                               const float *__restrict__ delta,
+                                                               int n_delta,
+                                                               const float *__restrict__ g,
+                                                               int hidden, int ks, int n_tok,
+                                                               float eps,
+                                                               uint16_t *__restrict__ out) {
   const int t = blockIdx.x;
-  __shared__ float red[4];
+  __shared__ float red[kNormThreads / 64];
   const int items = ks * 4;
   const bool live = t < n_tok;
   const int row_bytes = hidden * 4;
@@ -204,7 +208,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(float *__restrict__ h,
   f32x4 hv[IPT][2], dv[IPT][kMaxSplit][2], gv[IPT][2];
 #pragma unroll
   for (int j = 0; j < IPT; ++j) {
-    const int k0 = (threadIdx.x + j * 256) * 8;
+    const int k0 = (threadIdx.x + j * kNormThreads) * 8;
     const int vo = k0 < hidden ? k0 * 4 : row_bytes;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
@@ -223,7 +227,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(float *__restrict__ h,
   float ss = 0.0f;
 #pragma unroll
   for (int j = 0; j < IPT; ++j) {
-    const int k0 = (threadIdx.x + j * 256) * 8;
+    const int k0 = (threadIdx.x + j * kNormThreads) * 8;
     if (delta) {  // residual add of the previous projection, slices in order
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
@@ -246,11 +250,13 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(float *__restrict__ h,
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
-  ss = red[0] + red[1] + red[2] + red[3];
+  ss = red[0];
+#pragma unroll
+  for (int i = 1; i < kNormThreads / 64; ++i) ss += red[i];
   const float scale = live ? 1.0f / sqrtf(ss / (float)hidden + eps) : 0.0f;
 #pragma unroll
   for (int j = 0; j < IPT; ++j) {
-    const int it = threadIdx.x + j * 256;
+    const int it = threadIdx.x + j * kNormThreads;
     if (it >= items) continue;
     const int k0 = it * 8;
     // columns past hidden have zero residual and gain: they pack to zero
@@ -305,12 +311,12 @@ hipError_t launch_rmsnorm_pack(float *h, const float *delta, int n_delta, const 
                                int hidden, int ks, int n_tok, int n_pad, float eps, uint16_t *out,
                                hipStream_t s) {
   if (hidden % 8 != 0 || n_delta < 1 || n_delta > kMaxSplit) return hipErrorInvalidValue;
-  const int ipt = (ks * 4 + 255) / 256;
+  const int ipt = (ks * 4 + kNormThreads - 1) / kNormThreads;
   switch (ipt) {
 #define SB_IPT(n)                                                                              \
   case n:                                                                                      \
-    hipLaunchKernelGGL(k_rmsnorm_pack<n>, dim3(n_pad), dim3(256), 0, s, h, delta, n_delta, g,    \
-                       hidden, ks, n_tok, eps, out);                                           \
+    hipLaunchKernelGGL(k_rmsnorm_pack<n>, dim3(n_pad), dim3(kNormThreads), 0, s, h, delta,        \
+                       n_delta, g, hidden, ks, n_tok, eps, out);                               \
     break;
     SB_IPT(1) SB_IPT(2) SB_IPT(3) SB_IPT(4) SB_IPT(5) SB_IPT(6) SB_IPT(7) SB_IPT(8)
 #undef SB_IPT
