@@ -123,12 +123,15 @@ __device__ __forceinline__ void epilogue4(const GemmArgs &a, const float2 *rope,
 //
 // Ring depth per (TT, NT): as deep as the 256-register budget of two waves
 // per SIMD allows (ring 4R(NT+TT), accumulators 4*NT*TT, lane offsets NT+TT,
-// about 48 for the rest).
+// about 48 for the rest), up to about 12 KB of weights in flight per wave
+// (96 KB per compute unit: what covers the HBM latency at the per-unit
+// share of the bandwidth), and at least 4 chunks.
 template <int TT, int NT>
 struct Ring {
   static constexpr int free_regs = 208 - TT - NT - 4 * NT * TT;
   static constexpr int r = free_regs / (4 * (NT + TT));
-  static constexpr int R = r > 4 ? 4 : (r < 1 ? 1 : r);
+  static constexpr int cap = 12 / NT > 4 ? 12 / NT : 4;
+  static constexpr int R = r > cap ? cap : (r < 1 ? 1 : r);
 };
 
 // LDS staging area (32 KB): the step's RoPE table (QKV), the residual rows

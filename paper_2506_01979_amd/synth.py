@@ -95,6 +95,8 @@ SHAPES = {
     # ragged everywhere: hidden 328 (not a multiple of 16 or 256; != heads x
     # head_dim), ffn 600, vocabulary 1001 (odd)
     "ragged_bf16": Shape("ragged_bf16", 2, 328, 4, 2, 64, 600, 1001, "bf16"),
+    # 32 KV heads on a narrow model: few key ranges per head
+    "heads32_bf16": Shape("heads32_bf16", 2, 256, 32, 32, 64, 512, 1000, "bf16"),
 }
 
 WORKLOADS = {

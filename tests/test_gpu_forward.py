@@ -7,7 +7,8 @@ rows must match to the same bound.  Shapes span several GEMM tiles, ragged K
 (ffn 688, 600), ragged vocabularies (1000, 1001), a hidden width that is not
 a multiple of 16 (328), ragged attention chunks, GQA, both head widths and
 5..137-row trees (the O projection applies the post-attention RMSNorm up to
-128 rows and hands it to a separate kernel above).  Invariant (a) -- branch-masked rows equal
+128 rows and hands it to a separate kernel above), and 32 KV heads on a
+narrow model (few key ranges per head).  Invariant (a) -- branch-masked rows equal
 each branch run alone -- is checked on the GPU path too.
 """
 import numpy as np
@@ -78,6 +79,8 @@ CASES = [
     ("small_bf16", 1, ("chain", 40)),
     ("ragged_bf16", 300, ("branch", 4, 8)),
     ("ragged_bf16", 90, ("branch", 8, 17)),
+    ("heads32_bf16", 300, ("branch", 4, 8)),
+    ("heads32_bf16", 90, ("branch", 8, 7)),
 ]
 
 
