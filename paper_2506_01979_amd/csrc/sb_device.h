@@ -55,13 +55,16 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// Index of element (row t, column k) in the "packed operand" layout used for
-// every bf16 matrix-core input: [t/16][k/32][lane][8] with
-// lane = (t % 16) + 16 * ((k % 32) / 8) and element k % 8.  ksteps = K/32.
+// Index of element (row t, column k) in the "packed operand" layout of the
+// bf16 activations the matrix-core GEMMs read: [t/16][k/32][t%16][k%32],
+// 1 KB per (16-row tile, k-step) in which each row's 32 values are
+// contiguous.  Lane l of the GEMM's operand fragment (row l % 16, columns
+// 8 (l / 16) .. + 7 of the k-step) reads 16 bytes at (l % 16) * 64 +
+// (l / 16) * 16, so a tile with a single valid row costs one 64-byte
+// sector per k-step.  ksteps = K/32.
 __device__ __forceinline__ size_t packed_index(int t, int k, int ksteps) {
   const int tt = t >> 4, s = k >> 5;
-  const int lane = (t & 15) + 16 * ((k & 31) >> 3);
-  return (((size_t)tt * ksteps + s) * 64 + lane) * 8 + (k & 7);
+  return (((size_t)tt * ksteps + s) * 16 + (t & 15)) * 32 + (k & 31);
 }
 
 }  // namespace sb

@@ -224,7 +224,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
   int xvo[TT];
 #pragma unroll
   for (int tt = 0; tt < TT; ++tt)
-    xvo[tt] = (tt * 16 + (lane & 15)) < a.n_tok ? tt * ks * 1024 + lane * 16 : xbytes;
+    xvo[tt] = (tt * 16 + (lane & 15)) < a.n_tok
+                  ? tt * ks * 1024 + (lane & 15) * 64 + (lane >> 4) * 16
+                  : xbytes;
 
   // Operands of the epilogue go to LDS by direct-to-LDS loads issued now (no
   // registers held; each wave instruction moves 1 KB), long before the
