@@ -134,7 +134,7 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
 
   // The staging loads of a row block (query rows, ancestor masks) go out
   // before the cache reads: in-order completion lets the staging wait cover
-  // only them, and scoring (which needs K) starts while V is still arriving.
+  // only them.
   constexpr int QPT = (RB * (D / 8) + NT - 1) / NT;
   constexpr int APT = (RB * 8 + NT - 1) / NT;
   i32x4 qst[QPT];
@@ -160,7 +160,7 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
     }
   };
   stage_loads(0);
-  __builtin_amdgcn_sched_barrier(0);  // issue order: staging, K, V
+  __builtin_amdgcn_sched_barrier(0);  // issue order: staging, K (V after scoring)
 
   // ---- the workgroup's cache reads, once, into registers.  Lanes whose
   // slot is >= nkeys (or past the workgroup's steps) get an offset past the
@@ -181,15 +181,10 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
     }
   }
   __builtin_amdgcn_sched_barrier(0);
-  // V^T: dimensions 16 w + lr, keys 8 lg .. 8 lg + 7 of every step j
+  // V^T (dimensions 16 w + lr, keys 8 lg .. 8 lg + 7 of every step j) is
+  // requested once the wave has scored its steps: issued with K, its
+  // requests delayed the keys the scoring waits for
   i32x4 vf[MS];
-#pragma unroll
-  for (int j = 0; j < MS; ++j) {
-    const int key = (st0 + j) * 32 + 8 * lg;
-    const int vo = (j < nst && key < nkeys) ? ((16 * w + lr) * a.cap + key) * 2 : vbytes;
-    vf[j] = __builtin_amdgcn_raw_buffer_load_b128(vrs, vo, 0, 0);
-  }
-  __builtin_amdgcn_sched_barrier(0);
 
   // one block of query rows (its staging loads already issued)
   auto row_block = [&](int rb) {
@@ -240,6 +235,16 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
       }
       mx = max_x32(max_x16(mx));
       if (lg == 0) smax[w][rt * 16 + lr] = mx;
+    }
+    if (rb == 0) {
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < MS; ++j) {
+        const int key = (st0 + j) * 32 + 8 * lg;
+        const int vo = (j < nst && key < nkeys) ? ((16 * w + lr) * a.cap + key) * 2 : vbytes;
+        vf[j] = __builtin_amdgcn_raw_buffer_load_b128(vrs, vo, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
     lds_barrier();
 
