@@ -305,10 +305,13 @@ class Model:
         h = C.c_void_p()
         _check(lib.sb_model_create(C.byref(self.cfg), C.byref(mw), C.byref(h)), "sb_model_create")
         self.handle = h
+        # bound now: at interpreter exit the module's globals may be gone
+        # before the model is collected
+        self._destroy = lib.sb_model_destroy
 
     def __del__(self):
-        if getattr(self, "handle", None):
-            lib.sb_model_destroy(self.handle)
+        if getattr(self, "handle", None) and getattr(self, "_destroy", None):
+            self._destroy(self.handle)
             self.handle = None
 
     def _check_kv(self, k: torch.Tensor, v: torch.Tensor) -> None:
