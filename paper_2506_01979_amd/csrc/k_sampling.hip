@@ -655,6 +655,8 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
   __shared__ unsigned long long s_kmask[(SB_MAX_ROWS + 63) / 64];
   __shared__ int32_t s_tok[SB_MAX_ROWS];
   __shared__ float s_u[SB_MAX_ROWS];
+  __shared__ int s_first[SB_MAX_ROWS];  // lowest-index child of a row (INT_MAX: none)
+  __shared__ int s_node, s_plen;
   const int n = tree.n;
   double *ws0 = ws;
   double *ws1 = ws + vocab;
@@ -670,7 +672,10 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
     s_tok[threadIdx.x] = tokens[threadIdx.x];
     s_u[threadIdx.x] = u[threadIdx.x];
   }
+  if ((int)threadIdx.x < SB_MAX_ROWS) s_first[threadIdx.x] = INT_MAX;
   __syncthreads();
+  // first children: the candidates tried first at every node
+  if ((int)threadIdx.x >= 1 && (int)threadIdx.x < n) atomicMin(&s_first[s_par[threadIdx.x]], (int)threadIdx.x);
   if ((int)threadIdx.x < n && isnan(s_st[threadIdx.x].total)) atomicOr(&s_flags, SB_FLAG_NONFINITE);
   if ((int)threadIdx.x >= 1 && (int)threadIdx.x < n) {
     const int i = threadIdx.x;
@@ -688,10 +693,37 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
   __syncthreads();
   int flags = 0;  // thread 0 accumulates
   int nrej = 0;
-  int node = 0;
-  int plen = 1;
-  if (threadIdx.x == 0) path[0] = 0;
-  Dist cur = row_dist(logits, s_st[0], inv_t, greedy);
+  // Accept chain: while every node's first candidate is accepted against
+  // the node's own row (no residual yet), the tests read LDS only, so one
+  // thread walks them with no barrier per level.  The walk below resumes at
+  // the first node whose first candidate fails (it repeats that test and
+  // goes on with the residuals) or at the leaf reached.
+  if (threadIdx.x == 0) {
+    int nd = 0, pl = 1;
+    path[0] = 0;
+    for (;;) {
+      const int c = s_first[nd];
+      if (c == INT_MAX) break;
+      const int x = s_tok[c];
+      double ratio = 0.0;
+      if (x >= 0 && x < vocab) {
+        const double qx = (double)s_qx[c];
+        if (qx == 0.0) flags |= SB_FLAG_QZERO;
+        ratio = s_px[c] / qx;
+      } else {
+        flags |= SB_FLAG_QZERO;
+      }
+      if (!((double)s_u[c] < ratio)) break;
+      path[pl++] = (int16_t)c;
+      nd = c;
+    }
+    s_node = nd;
+    s_plen = pl;
+  }
+  __syncthreads();
+  int node = s_node;
+  int plen = s_plen;
+  Dist cur = row_dist(logits + (size_t)node * vocab, s_st[node], inv_t, greedy);
   int y = 0;
   int bonus = 0;
   for (;;) {
@@ -718,7 +750,6 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
     const int nkids = nk;
     if (nkids == 0) {
       bonus = 1;
-      y = draw_pass(cur, u[0], vocab, sh);
       break;
     }
     ChildCands cc{kids, s_tok, q, s_u, vocab, s_px, s_qx};
@@ -731,9 +762,10 @@ __global__ __launch_bounds__(kWalkThreads) void k_walk(int vocab, TreeArg tree,
       cur = row_dist(logits + (size_t)node * vocab, s_st[node], inv_t, greedy);
       continue;
     }
-    y = draw_pass(cur, u[0], vocab, sh);
     break;
   }
+  // the bonus token from an accepted leaf's p, or the residual's draw
+  y = draw_pass(cur, u[0], vocab, sh);
   __syncthreads();
   if (threadIdx.x == 0) {
     int branch = -1;
