@@ -168,6 +168,46 @@ __device__ __forceinline__ void load_p(const Dist &d, const int (&v)[K], int voc
   }
 }
 
+// p~ at the 8 consecutive tokens e0 .. e0 + 7 (e0 a multiple of 8, vocab a
+// multiple of 8, so the 8 are all in range when e0 is), loaded as 16-byte
+// words: a lane's 8 neighbours cost 2 (logits) or 4 (residual) loads
+// instead of 8.  Converted exactly as load_p converts; !valid reads 0.
+__device__ __forceinline__ void load_p8(const Dist &d, int e0, bool valid, int vocab, double rcp,
+                                        double (&out)[8]) {
+  if (d.arr) {
+    const __amdgpu_buffer_rsrc_t rs = uniform_rsrc(d.arr, vocab * 8);
+    const int off = valid ? e0 * 8 : vocab * 8;
+    u32x4 w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      w[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 * k, 0, 0));
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      out[2 * k] = __builtin_bit_cast(double, ((uint64_t)w[k][1] << 32) | w[k][0]) * rcp;
+      out[2 * k + 1] = __builtin_bit_cast(double, ((uint64_t)w[k][3] << 32) | w[k][2]) * rcp;
+    }
+  } else if (d.greedy) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = valid && e0 + e == d.argmax ? 1.0 : 0.0;
+  } else {
+    const __amdgpu_buffer_rsrc_t rs = uniform_rsrc(d.l, vocab * 4);
+    const int off = valid ? e0 * 4 : vocab * 4;
+    float raw[8];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const f32x4 v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 * k, 0, 0));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) raw[4 * k + e] = v[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float z = raw[e] * d.inv_t;
+      const double p = (double)expf(z - d.zmax) * rcp;
+      out[e] = valid ? p : 0.0;
+    }
+  }
+}
+
 __device__ __forceinline__ Dist row_dist(const float *l, const sb_row_stats &st, float inv_t,
                                          int greedy) {
   Dist d;
@@ -274,12 +314,16 @@ __device__ int draw_pass(const Dist &d, float u, int vocab, Shared &sh) {
   if (lo < hi && seg_end > thr) {
     for (int b0 = lo; b0 < hi && cand == INT_MAX; b0 += 512) {
       const int e0 = b0 + 8 * lane;
-      int vv[8];
       double x[8];
       double ls = 0.0;
+      if ((vocab & 7) == 0) {
+        load_p8(d, e0, e0 < hi, vocab, rcp, x);
+      } else {
+        int vv[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) vv[e] = e0 + e < hi ? e0 + e : -1;
-      load_p<8>(d, vv, vocab, rcp, x);
+        for (int e = 0; e < 8; ++e) vv[e] = e0 + e < hi ? e0 + e : -1;
+        load_p<8>(d, vv, vocab, rcp, x);
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) ls += x[e];
       double inc = ls;
