@@ -251,30 +251,36 @@ def algorithmic_bytes(shape, P_kv: int, n: int) -> dict:
             "prefix_kv": prefix_kv, "gate_up_launch": gate_up}
 
 
-def partial_tree(B: int, k: int, depth: int):
-    """Rows of the B x k tree with depth < `depth`, in ascending row order,
-    with parents re-indexed; returns (rows, parents)."""
-    rows = [0] + [1 + b * k + t for b in range(B) for t in range(depth - 1)]
-    rows.sort()
+def partial_tree(parents, depth: int):
+    """Rows of the tree with depth < `depth`, in ascending row order, with
+    parents re-indexed; returns (rows, parents)."""
+    from paper_2506_01979_amd import synth
+
+    dep = synth.tree_depths(np.asarray(parents))
+    rows = [i for i in range(len(parents)) if dep[i] < depth]
     pos = {r: i for i, r in enumerate(rows)}
-    full = [-1] + [0 if t == 0 else 1 + b * k + t - 1 for b in range(B) for t in range(k)]
-    return rows, [-1] + [pos[full[r]] for r in rows[1:]]
+    return rows, [-1] + [pos[int(parents[r])] for r in rows[1:]]
 
 
-def make_drafts(api, synth, m, k_, v_, kv_len, root_tok, B, kd, alpha, q_temp, seed):
-    """Drafts generated depth by depth: q = alpha * p_target + (1 - alpha) *
-    softmax(N(0,1)/q_temp); the root's children are i.i.d. draws from one q."""
+def make_drafts(api, synth, m, k_, v_, kv_len, root_tok, parents, alpha, q_temp, seed):
+    """Drafts generated depth by depth over the tree `parents`: q = alpha *
+    p_target + (1 - alpha) * softmax(N(0,1)/q_temp) of the parent's target
+    row; the children of one row are i.i.d. draws from one q."""
     import torch
 
     V = m.shape.vocab
-    n = 1 + B * kd
+    n = len(parents)
+    dep = synth.tree_depths(np.asarray(parents))
+    first = {}
+    for i in range(1, n):
+        first.setdefault(int(parents[i]), i)
     g = np.random.default_rng(seed)
     qrand = synth.softmax_rows(synth.random_logits(n, V, 1.0 / q_temp, seed=seed + 7))
     tokens = np.zeros(n, dtype=np.int32)
     tokens[0] = root_tok
     q = np.zeros((n, V), dtype=np.float32)
-    for depth in range(1, kd + 1):
-        rows, par = partial_tree(B, kd, depth)
+    for depth in range(1, int(dep.max()) + 1):
+        rows, par = partial_tree(parents, depth)
         nr = len(rows)
         logits = torch.empty((nr, V), dtype=torch.float32, device="cuda")
         stats = api.new_stats(nr)
@@ -284,11 +290,12 @@ def make_drafts(api, synth, m, k_, v_, kv_len, root_tok, B, kd, alpha, q_temp, s
         lg -= lg.max(axis=1, keepdims=True)
         p = np.exp(lg)
         p /= p.sum(axis=1, keepdims=True)
-        for b in range(B):
-            row = 1 + b * kd + depth - 1
-            parent = 0 if depth == 1 else row - 1
+        for row in range(1, n):
+            if dep[row] != depth:
+                continue
+            parent = int(parents[row])
             pr = p[rows.index(parent)]
-            qr = qrand[1] if depth == 1 else qrand[row]   # root children share one q
+            qr = qrand[first[parent]]   # siblings share one q
             qq = alpha * pr + (1 - alpha) * qr.astype(np.float64)
             qq /= qq.sum()
             q[row] = qq.astype(np.float32)
@@ -386,6 +393,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--alpha", type=float, default=0.6)
+    ap.add_argument("--tree", choices=("branch", "fork"), default="branch",
+                    help="branch: the workload's B x k branches off the root; fork: a chain "
+                         "of --trunk drafts, then B branches of --fork-depth drafts")
+    ap.add_argument("--trunk", type=int, default=4)
+    ap.add_argument("--fork-depth", type=int, default=7)
     ap.add_argument("--cpu-layers", type=int, default=0,
                     help="decoder layers the CPU oracle runs (0: all of them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -419,7 +431,13 @@ def main():
     if args.cpu_layers <= 0 or args.cpu_layers > shape.n_layers:
         args.cpu_layers = shape.n_layers
     B, kd, P = w.branches, w.depth, w.prefix
-    kv_len, n = w.kv_len, w.n_rows
+    if args.tree == "fork":
+        parents = synth.fork_parents(args.trunk, B, args.fork_depth)
+        tree_desc = f"chain of {args.trunk} + fork of B={B} x {args.fork_depth} drafts"
+    else:
+        parents = synth.branch_parents(B, kd)
+        tree_desc = f"B={B} branches x k={kd} drafts"
+    kv_len, n = w.kv_len, len(parents)
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
 
@@ -449,9 +467,8 @@ def main():
             kv_host[l] = (kb, vb)
     log(f"prefix KV ready ({kv_len} slots) at {time.time() - t0:.1f}s")
 
-    parents = synth.branch_parents(B, kd)
     root = int(synth.prefix_tokens(shape.vocab, P)[-1])
-    tokens, q = make_drafts(api, synth, m, k_, v_, kv_len, root, B, kd, args.alpha, w.q_temp, 11)
+    tokens, q = make_drafts(api, synth, m, k_, v_, kv_len, root, parents, args.alpha, w.q_temp, 11)
     u = synth.uniforms(n, 1)
     inp = {"tokens": tokens, "parents": parents, "q": q, "u": u}
 
@@ -544,7 +561,7 @@ def main():
     nbytes = algorithmic_bytes(shape, kv_len, n)
     k_avg_ms = k_ms / max(1, k_launches)
     achieved = nbytes["gate_up_launch"] / (k_avg_ms * 1e-3) / 1e9
-    verified = B * kd / (ms_per_step * 1e-3)
+    verified = (n - 1) / (ms_per_step * 1e-3)
     out = {
         "metric": "verified tokens/s per verify step + % HBM roofline, 7B-shape bf16, B=4 k=8",
         "value": round(verified, 1),
@@ -559,9 +576,10 @@ def main():
         "dtype": "bf16",
         "data": "synthetic: seeded N(0,0.02) bf16 weights, seeded N(0,1) prefix KV, "
                 "drafts drawn from alpha*p+(1-alpha)*softmax(N(0,1)/0.7)",
-        "config": {"workload": f"{shape.name} verify step: B={B} branches x k={kd} drafts, "
-                               f"prefix {P}", "rows": n, "prefix": P, "branches": B,
-                   "depth": kd, "alpha": args.alpha},
+        "config": {"workload": f"{shape.name} verify step: {tree_desc}, prefix {P}",
+                   "rows": n, "prefix": P, "branches": B,
+                   "depth": kd if args.tree == "branch" else args.trunk + args.fork_depth,
+                   "alpha": args.alpha},
         "roofline": {"bound": "hbm", "kernel": f"k_gemm (gate/up + SwiGLU), {k_launches} launches",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
@@ -577,7 +595,7 @@ def main():
     if not args.no_alpha_sweep:
         sweep = {}
         for a in (0.3, 0.6, 0.9):
-            toks_a, q_a = make_drafts(api, synth, m, k_, v_, kv_len, root, B, kd, a, w.q_temp, 21)
+            toks_a, q_a = make_drafts(api, synth, m, k_, v_, kv_len, root, parents, a, w.q_temp, 21)
             dt, dq = torch.from_numpy(toks_a).to(dev), torch.from_numpy(q_a).to(dev)
             m.sb_verify_forward(k_, v_, kv_len, dt, parents, 1.0, logits, stats, ws, stream)
             lens = []

@@ -239,6 +239,21 @@ def chain_parents(n: int) -> np.ndarray:
     return np.arange(-1, n - 1, dtype=np.int32)
 
 
+def fork_parents(trunk: int, branches: int, depth: int) -> np.ndarray:
+    """Parents of a chain-plus-fork tree, the verification shape of the
+    paper's Section "Branch Verification": rows 1..trunk form a chain from
+    the root (the drafts before the branch point), and `branches` branches
+    of `depth` rows hang off the last of them (the branch point's candidates,
+    each followed by its continuation).  trunk = 0 gives branch_parents."""
+    par = [-1] + list(range(trunk))
+    fork = trunk
+    for b in range(branches):
+        base = 1 + trunk + b * depth
+        for j in range(depth):
+            par.append(fork if j == 0 else base + j - 1)
+    return np.asarray(par, dtype=np.int32)
+
+
 def tree_depths(parents: np.ndarray) -> np.ndarray:
     """Depth of every row (root 0); used to pick per-depth draft inputs."""
     dep = np.zeros(len(parents), dtype=np.int64)

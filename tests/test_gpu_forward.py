@@ -7,8 +7,10 @@ rows must match to the same bound.  Shapes span several GEMM tiles, ragged K
 (ffn 688, 600), ragged vocabularies (1000, 1001), a hidden width that is not
 a multiple of 16 (328), ragged attention chunks, GQA, both head widths and
 5..137-row trees (the O projection applies the post-attention RMSNorm up to
-128 rows and hands it to a separate kernel above), and 32 KV heads on a
-narrow model (few key ranges per head).  Invariant (a) -- branch-masked rows equal
+128 rows and hands it to a separate kernel above), the paper's
+chain-plus-fork verification shape (a chain of drafts, then B candidates
+with or without continuations), and 32 KV heads on a narrow model (few key
+ranges per head).  Invariant (a) -- branch-masked rows equal
 each branch run alone -- is checked on the GPU path too.
 """
 import numpy as np
@@ -81,12 +83,16 @@ CASES = [
     ("ragged_bf16", 90, ("branch", 8, 17)),
     ("heads32_bf16", 300, ("branch", 4, 8)),
     ("heads32_bf16", 90, ("branch", 8, 7)),
+    ("small_bf16", 300, ("fork", 4, 4, 7)),
+    ("tiny", 64, ("fork", 6, 3, 1)),
 ]
 
 
 def tree_of(spec):
     if spec[0] == "branch":
         return synth.branch_parents(spec[1], spec[2])
+    if spec[0] == "fork":
+        return synth.fork_parents(spec[1], spec[2], spec[3])
     return synth.chain_parents(spec[1])
 
 

@@ -158,6 +158,8 @@ TREES = [
     ("b8k16", synth.branch_parents(8, 16)),
     ("b2k1", synth.branch_parents(2, 1)),
     ("chain20", synth.chain_parents(20)),
+    ("fork4x4x7", synth.fork_parents(4, 4, 7)),
+    ("fork6x5x1", synth.fork_parents(6, 5, 1)),
     ("random60", _random_tree(60, 3)),
     ("root_only", np.array([-1], dtype=np.int32)),
 ]

@@ -138,6 +138,30 @@ def test_branch_mask_equals_per_branch_forward(wname, shape):
         assert relerr(lt[rows], lh[P - 1:]) < 1e-6
 
 
+def test_fork_tree_equals_chain_plus_candidate():
+    """The chain-plus-fork shape: every root-to-leaf path of the tree
+    forward equals a causal forward of the prefix followed by that path
+    (the trunk, one candidate, its continuation), checked against the
+    library model."""
+    shape = synth.SHAPES["exact"]
+    W = synth.model_weights(shape)
+    P, trunk, B, d = 10, 3, 3, 2
+    par = synth.fork_parents(trunk, B, d)
+    assert list(par) == [-1, 0, 1, 2, 3, 4, 3, 6, 3, 8]
+    assert tree.children(par, trunk) == [4, 6, 8]
+    ptoks = synth.prefix_tokens(shape.vocab, P)
+    _, Kp, Vp = decoder.prefill(shape, W, ptoks[:-1], "f64")
+    g = np.random.default_rng(11)
+    toks = g.integers(0, shape.vocab, len(par)).astype(np.int32)
+    toks[0] = ptoks[-1]
+    lt, _, _ = decoder.tree_forward(shape, W, Kp, Vp, P - 1, toks, par, "f64")
+    m = hf_model(shape, W, exact_rope=True)
+    for leaf in (5, 7, 9):
+        rows = tree.root_path(par, leaf)
+        lh, _, _ = hf_forward(m, np.concatenate([ptoks, toks[rows[1:]]]))
+        assert relerr(lt[rows], lh[P - 1:]) < 1e-6
+
+
 def test_tree_positions_and_paths():
     par = synth.branch_parents(2, 3)
     assert list(par) == [-1, 0, 1, 2, 0, 4, 5]
