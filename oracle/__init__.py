@@ -11,7 +11,10 @@ MI355X path computes, written from the paper:
   speculative accept test min(1, p/q) with residual norm(max(0, p - q))
   (Preliminaries, "Speculative Decoding"), Branch Speculative Sampling
   (Appendix, Algorithm 1) at multi-child nodes, and inverse-CDF draws;
-* ``oracle.rollback`` -- KV compaction to the accepted path.
+* ``oracle.rollback`` -- KV compaction to the accepted path;
+* ``oracle.hrad``     -- H-RAD's length predictor (Section "H-RAD"): the
+  last K layers' hidden states and the new token's embedding through a
+  256/64/3 ReLU MLP, s_t = argmax.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's CPU baseline
 may import this package.  It shares no code with the HIP path and imports
@@ -23,4 +26,4 @@ output distribution, closed forms printed in the paper, hand-worked golden
 cases).  Nothing here is "parity unpinned".
 """
 
-from . import tree, decoder, sampling, rollback  # noqa: F401
+from . import tree, decoder, sampling, rollback, hrad  # noqa: F401

@@ -97,14 +97,15 @@ def silu(x: np.ndarray) -> np.ndarray:
 
 
 def tree_forward(shape, weights: dict, prefix_k, prefix_v, kv_len: int, tokens, parents,
-                 mode: str = "f64"):
+                 mode: str = "f64", hidden: list | None = None):
     """Forward of the token tree (tokens[i], parents[i]) on a prefix KV cache.
 
     prefix_k / prefix_v: per layer [n_kv_heads][>= kv_len][head_dim] arrays
     (a list, or an array with a leading layer axis; only slots < kv_len are
     read).  Returns (logits [N][V], k_tree, v_tree) where k_tree / v_tree are
     [n_layers][n_kv_heads][N][head_dim]: the keys/values the tree rows write
-    to cache slots kv_len + i.
+    to cache slots kv_len + i.  If `hidden` is a list, the residual stream
+    after every layer ([N][hidden], layer 0 first) is appended to it.
     """
     P = _Prec(mode)
     dt = P.dt
@@ -153,6 +154,8 @@ def tree_forward(shape, weights: dict, prefix_k, prefix_v, kv_len: int, tokens, 
         up = m @ P.cast(W["wu"]).T
         act = P.store(silu(gt) * up)
         h = h + act @ P.cast(W["wd"]).T
+        if hidden is not None:
+            hidden.append(h.copy())
     fin = P.store(rms_norm(h, weights["final_norm"], eps, dt))
     logits = fin @ P.cast(weights["lm_head"]).T
     return logits, k_tree, v_tree
