@@ -143,7 +143,8 @@ def pmc_summary(fetch_dir: str, write_dir: str) -> str:
     cmd = ("cd /tmp && export TMPDIR=/tmp && "
            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <repo>/gpurun_out/pmc_fetch -o run -- "
            "python3 <repo>/bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-alpha-sweep "
-           "--copy-calibration; the same with --pmc WRITE_SIZE into gpurun_out/pmc_write; then "
+           "--no-hrad --no-graph --copy-calibration; the same with --pmc WRITE_SIZE into "
+           "gpurun_out/pmc_write; then "
            "python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write")
     return "\n".join([
         f"# HBM traffic of the gate/up GEMM launch, {WORKLOAD}",
@@ -213,7 +214,7 @@ def trace_summary(trace_dir: str) -> str:
     out = [f"# Kernel trace of the verify step, {WORKLOAD}", "",
            "Command: `cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
            "--output-format csv -d <repo>/gpurun_out/prof_step -o run -- python3 <repo>/bench.py "
-           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-graph`, then "
+           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-graph`, then "
            "`python3 bench.py --trace-summary gpurun_out/prof_step`", "",
            f"Last {len(steps)} complete steps (embed .. stats, then the accept walk and the rollback "
            f"when traced): span "
@@ -404,6 +405,8 @@ def main():
     ap.add_argument("--no-alpha-sweep", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the HIP-graph replay measurement")
+    ap.add_argument("--no-hrad", action="store_true",
+                    help="skip the H-RAD measurement (feature tap + predictor)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="end with a device copy of known size (for rocprofv3 --pmc runs)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -549,6 +552,45 @@ def main():
         if rg != r:
             raise RuntimeError("graph replay changed the step's result")
 
+    # H-RAD (Section "H-RAD"): the step again with the last 4 layers' hidden
+    # states tapped, and the predictor on the walk's result (random MLP
+    # weights: the trained ones are not available).  Not part of `value`.
+    hrad_out = None
+    if not args.no_hrad:
+        HK = 4
+        taps = torch.empty((HK, n, shape.hidden), dtype=torch.float32, device=dev)
+        m.sb_model_set_tap(taps, HK, n)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            step()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        tap_ms = ev0.elapsed_time(ev1) / args.steps
+        m.sb_model_set_tap(None)
+        gw = np.random.default_rng(5)
+        din = (HK + 1) * shape.hidden
+        hw = {"w1": gw.standard_normal((256, din)) / np.sqrt(din), "b1": gw.standard_normal(256) * 0.1,
+              "w2": gw.standard_normal((64, 256)) / 16.0, "b2": gw.standard_normal(64) * 0.1,
+              "w3": gw.standard_normal((3, 64)) / 8.0, "b3": gw.standard_normal(3) * 0.1}
+        hw = {key: torch.from_numpy(val.astype(np.float32)).to(dev) for key, val in hw.items()}
+        hws = torch.empty(api.lib.sb_hrad_workspace_bytes(), dtype=torch.uint8, device=dev)
+        lg3 = torch.empty(3, dtype=torch.float32, device=dev)
+        cls = torch.empty(1, dtype=torch.int32, device=dev)
+        for _ in range(3):
+            m.sb_hrad_predict(taps, HK, n, res, hw, lg3, cls, hws, stream)
+        reps = 100
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(reps):
+            m.sb_hrad_predict(taps, HK, n, res, hw, lg3, cls, hws, stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        hrad_out = {"k_layers": HK, "ms_per_step_with_tap": round(tap_ms, 4),
+                    "predict_us": round(ev0.elapsed_time(ev1) * 1e3 / reps, 2),
+                    "w1_bytes": 256 * din * 4, "class": int(cls.item())}
+        del taps
+
     if args.copy_calibration:
         # a plain device copy of known size, for scaling the HBM byte counters
         src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
@@ -591,6 +633,8 @@ def main():
                      "ms_per_step_graph_replay": None if graph_ms is None else round(graph_ms, 4)},
         "accepted": r["n_accepted"],
     }
+    if hrad_out is not None:
+        out["hrad"] = hrad_out
 
     if not args.no_alpha_sweep:
         sweep = {}

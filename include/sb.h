@@ -235,6 +235,47 @@ sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_le
                          const sb_step_result *d_result, int32_t *d_new_len,
                          hipStream_t stream);
 
+/* ---- H-RAD: the draft-length predictor's features and MLP ------------ */
+
+/* Hidden widths of H-RAD's MLP (Appendix, "H-RAD Training"). */
+#define SB_HRAD_H1 256
+#define SB_HRAD_H2 64
+#define SB_HRAD_CLASSES 3
+
+/* Feature tap of H-RAD (Section "H-RAD", z_t): while set, every
+ * sb_verify_forward of this model also writes the residual stream after
+ * each of its last k_layers layers, float32 d_taps[k][row][hidden] with
+ * k = 0 the layer n_layers - k_layers (rows of the call's tree, at most
+ * max_rows of them; a call with more rows returns SB_ERR_CAPACITY).
+ * d_taps = NULL clears the tap.  SB_BF16 models only (SB_ERR_DTYPE
+ * otherwise); 1 <= k_layers <= n_layers. */
+sb_status sb_model_set_tap(sb_model *m, float *d_taps, int32_t k_layers, int32_t max_rows);
+
+/* H-RAD's MLP weights, float32 device arrays, y = W x + b per layer:
+ * w1 [SB_HRAD_H1][(k_layers + 1) * hidden], w2 [SB_HRAD_H2][SB_HRAD_H1],
+ * w3 [SB_HRAD_CLASSES][SB_HRAD_H2]; biases of the output widths. */
+typedef struct {
+  const float *w1, *b1, *w2, *b2, *w3, *b3;
+} sb_hrad_weights;
+
+/* Workspace bytes of sb_hrad_predict. */
+size_t sb_hrad_workspace_bytes(void);
+
+/* H-RAD's class for the next round (Section "H-RAD", eqs. z_t, s_t):
+ * z = Concat(the k_layers tapped hidden states of row r, the embedding of
+ * token y), r = the last row of d_result->path (the last accepted
+ * position) and y = d_result->next_token, through ReLU(W1 z + b1),
+ * ReLU(W2 . + b2), W3 . + b3.  Writes the three logits to d_logits3 and
+ * s_t = their argmax (lowest index on ties: 0 all reject, 1 use the
+ * draft's confidence, 2 all accept) to *d_class.  d_taps as filled by the
+ * forward that d_result's walk scored (k_layers, max_rows as given to
+ * sb_model_set_tap); a path row >= max_rows or a token outside the
+ * vocabulary yields class -1 and zero logits.  float32 arithmetic. */
+sb_status sb_hrad_predict(const sb_model *m, const float *d_taps, int32_t k_layers,
+                          int32_t max_rows, const sb_step_result *d_result,
+                          const sb_hrad_weights *w, float *d_logits3, int32_t *d_class,
+                          void *d_ws, size_t ws_bytes, hipStream_t stream);
+
 /* ---- measurement ---------------------------------------------------- */
 
 /* Kernel classes of the verify step, for sb_timer_start. */

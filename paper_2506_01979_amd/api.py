@@ -29,7 +29,10 @@ STATUS = {0: "SB_OK", 1: "SB_ERR_INVALID_ARG", 2: "SB_ERR_TREE", 3: "SB_ERR_CAPA
 EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight",
            "sb_model_create", "sb_model_destroy", "sb_workspace_bytes", "sb_verify_forward",
            "sb_softmax_stats", "sb_sample_workspace_bytes", "sb_select_branch",
-           "sb_accept_resample", "sb_kv_rollback", "sb_timer_start", "sb_timer_stop")
+           "sb_accept_resample", "sb_kv_rollback", "sb_timer_start", "sb_timer_stop",
+           "sb_model_set_tap", "sb_hrad_workspace_bytes", "sb_hrad_predict")
+
+SB_HRAD_H1, SB_HRAD_H2, SB_HRAD_CLASSES = 256, 64, 3
 
 KERNEL_CLASSES = {"qkv": 0, "o": 1, "gate_up": 2, "down": 3, "lm_head": 4, "attn": 5,
                   "attn_merge": 6, "norm": 7, "stats": 8}
@@ -61,6 +64,11 @@ class ModelWeights(C.Structure):
 
 class KVCache(C.Structure):
     _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("capacity", C.c_int32)]
+
+
+class HradWeights(C.Structure):
+    _fields_ = [("w1", C.c_void_p), ("b1", C.c_void_p), ("w2", C.c_void_p),
+                ("b2", C.c_void_p), ("w3", C.c_void_p), ("b3", C.c_void_p)]
 
 
 ROW_STATS_DTYPE = np.dtype([("zmax", "<f4"), ("argmax", "<i4"), ("total", "<f8")])
@@ -98,6 +106,13 @@ lib.sb_timer_stop.restype = _i32
 lib.sb_timer_stop.argtypes = [_vp, C.POINTER(C.c_double), C.POINTER(_i32)]
 lib.sb_kv_rollback.restype = _i32
 lib.sb_kv_rollback.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, _vp, _vp]
+lib.sb_model_set_tap.restype = _i32
+lib.sb_model_set_tap.argtypes = [_vp, _vp, _i32, _i32]
+lib.sb_hrad_workspace_bytes.restype = _sz
+lib.sb_hrad_workspace_bytes.argtypes = []
+lib.sb_hrad_predict.restype = _i32
+lib.sb_hrad_predict.argtypes = [_vp, _vp, _i32, _i32, _vp, C.POINTER(HradWeights), _vp, _vp,
+                                _vp, _sz, _vp]
 
 
 def _check(code: int, where: str) -> None:
@@ -387,6 +402,42 @@ class Model:
         n = C.c_int32()
         _check(lib.sb_timer_stop(self.handle, C.byref(ms), C.byref(n)), "sb_timer_stop")
         return ms.value, n.value
+
+    def sb_model_set_tap(self, taps, k_layers: int = 0, max_rows: int = 0) -> None:
+        """H-RAD feature tap: later forwards write the residual after each of
+        the last k_layers layers to taps, float32 [k_layers][max_rows][hidden]
+        (None clears it; the tensor must outlive its use)."""
+        if taps is None:
+            _check(lib.sb_model_set_tap(self.handle, None, 0, 0), "sb_model_set_tap")
+            self._tap = None
+            return
+        _need(taps, k_layers * max_rows * self.shape.hidden * 4, "taps", torch.float32)
+        _check(lib.sb_model_set_tap(self.handle, taps.data_ptr(), k_layers, max_rows),
+               "sb_model_set_tap")
+        self._tap = taps
+
+    def sb_hrad_predict(self, taps: torch.Tensor, k_layers: int, max_rows: int,
+                        result: torch.Tensor, w: dict, logits3: torch.Tensor,
+                        cls: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+        """H-RAD's class for the next round from the taps at the walk's last
+        accepted row and the embedding of its next token; w: float32 device
+        tensors w1 [256][(k+1)*hidden], b1, w2 [64][256], b2, w3 [3][64], b3."""
+        H = self.shape.hidden
+        _need(taps, k_layers * max_rows * H * 4, "taps", torch.float32)
+        _need(result, STEP_RESULT_INTS * 4, "result", torch.int32)
+        shapes = {"w1": SB_HRAD_H1 * (k_layers + 1) * H, "b1": SB_HRAD_H1,
+                  "w2": SB_HRAD_H2 * SB_HRAD_H1, "b2": SB_HRAD_H2,
+                  "w3": SB_HRAD_CLASSES * SB_HRAD_H2, "b3": SB_HRAD_CLASSES}
+        for nm, cnt in shapes.items():
+            _need(w[nm], cnt * 4, nm, torch.float32)
+        _need(logits3, SB_HRAD_CLASSES * 4, "logits3", torch.float32)
+        _need(cls, 4, "cls", torch.int32)
+        _need(ws, int(lib.sb_hrad_workspace_bytes()), "ws")
+        hw = HradWeights(*(w[nm].data_ptr() for nm in ("w1", "b1", "w2", "b2", "w3", "b3")))
+        _check(lib.sb_hrad_predict(self.handle, taps.data_ptr(), k_layers, max_rows,
+                                   result.data_ptr(), C.byref(hw), logits3.data_ptr(),
+                                   cls.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
+                                   _stream(stream)), "sb_hrad_predict")
 
     def sb_kv_rollback(self, k: torch.Tensor, v: torch.Tensor, kv_len: int,
                        result: torch.Tensor, new_len: torch.Tensor, stream=None) -> None:

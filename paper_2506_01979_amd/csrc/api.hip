@@ -23,6 +23,10 @@ struct sb_model {
   const float *final_norm;
   const void *lm_head;
   sb_timer timer;
+  // H-RAD feature tap: residual after each of the last tap_k layers,
+  // [tap_k][tap_rows][hidden] fp32 (null: no tap)
+  float *tap = nullptr;
+  int tap_k = 0, tap_rows = 0;
 };
 
 namespace sb {
@@ -232,6 +236,14 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   aa.part_o = (float *)(ws + L.part_o);
   aa.part_ml = (float *)(ws + L.part_ml);
 
+  // H-RAD tap: the norm that adds layer li's output to the residual also
+  // copies it when li is one of the last tap_k layers
+  auto tap_of = [&](int li) -> float * {
+    const int idx = li - (c.n_layers - m->tap_k);
+    if (!m->tap || li < 0 || idx < 0) return nullptr;
+    return m->tap + (size_t)idx * m->tap_rows * H;
+  };
+
   // The O projection also applies the post-attention RMSNorm when its
   // launch shape allows (RESID_NORM); gate/up then scales by 1 / rms.
   int o_groups = 0;
@@ -243,7 +255,7 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
     uint16_t *vc = (uint16_t *)kv->v + l * layer_kv;
     SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, split ? delta : nullptr, split ? split : 1,
                                              lw.attn_norm, H, L.ks_h, n, L.np, c.rms_eps, xa,
-                                             s));
+                                             s, tap_of(l - 1)));
     ga.W = (const uint16_t *)lw.qkv;
     ga.X = xa;
     ga.ks = gq.ks;
@@ -288,7 +300,8 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
     SB_TIMED(SB_KC_DOWN, launch_gemm(EPI_RESID, ga, gd.tiles, &split, s));
   }
   SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, split ? delta : nullptr, split ? split : 1,
-                                           m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s));
+                                           m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s,
+                                           tap_of(c.n_layers - 1)));
   ga.W = (const uint16_t *)m->lm_head;
   ga.X = xa;
   ga.ks = gl.ks;
@@ -531,6 +544,7 @@ sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
   if (m->cfg.dtype == SB_F32 && kv_len + n_rows > kF32MaxKeys) return SB_ERR_UNSUPPORTED;
   const Layout L = make_layout(m->cfg, n_rows, kv_len);
   if (ws_bytes < L.total) return SB_ERR_CAPACITY;
+  if (m->tap && n_rows > m->tap_rows) return SB_ERR_CAPACITY;
   if (m->cfg.dtype == SB_BF16)
     return forward_bf16(m, kv, kv_len, d_tokens, tree, n_rows, temperature, d_logits, d_stats,
                         (char *)d_ws, L, stream);
@@ -577,6 +591,55 @@ sb_status sb_accept_resample(int32_t vocab, int32_t n_rows, const int32_t *d_tok
   if (ws_bytes < sample_ws_bytes(vocab)) return SB_ERR_CAPACITY;
   return hip_status(launch_walk(vocab, tree, d_tokens, d_logits, d_stats, temperature, d_q, d_u,
                                 d_result, d_ws, stream));
+}
+
+sb_status sb_model_set_tap(sb_model *m, float *d_taps, int32_t k_layers, int32_t max_rows) {
+  if (!m) return SB_ERR_INVALID_ARG;
+  if (!d_taps) {
+    m->tap = nullptr;
+    m->tap_k = m->tap_rows = 0;
+    return SB_OK;
+  }
+  if (m->cfg.dtype != SB_BF16) return SB_ERR_DTYPE;
+  if (k_layers < 1 || k_layers > m->cfg.n_layers || max_rows < 1 || max_rows > SB_MAX_ROWS)
+    return SB_ERR_INVALID_ARG;
+  m->tap = d_taps;
+  m->tap_k = k_layers;
+  m->tap_rows = max_rows;
+  return SB_OK;
+}
+
+size_t sb_hrad_workspace_bytes(void) { return align_up(SB_HRAD_H1 * sizeof(float)); }
+
+sb_status sb_hrad_predict(const sb_model *m, const float *d_taps, int32_t k_layers,
+                          int32_t max_rows, const sb_step_result *d_result,
+                          const sb_hrad_weights *w, float *d_logits3, int32_t *d_class,
+                          void *d_ws, size_t ws_bytes, hipStream_t stream) {
+  if (!m || !d_taps || !d_result || !w || !d_logits3 || !d_class || !d_ws)
+    return SB_ERR_INVALID_ARG;
+  if (!w->w1 || !w->b1 || !w->w2 || !w->b2 || !w->w3 || !w->b3) return SB_ERR_INVALID_ARG;
+  if (m->cfg.dtype != SB_BF16) return SB_ERR_DTYPE;
+  if (k_layers < 1 || k_layers > m->cfg.n_layers || max_rows < 1 || max_rows > SB_MAX_ROWS)
+    return SB_ERR_INVALID_ARG;
+  if (ws_bytes < sb_hrad_workspace_bytes()) return SB_ERR_CAPACITY;
+  HradArgs a{};
+  a.taps = d_taps;
+  a.k = k_layers;
+  a.max_rows = max_rows;
+  a.hidden = m->cfg.hidden;
+  a.vocab = m->cfg.vocab;
+  a.embed = (const uint16_t *)m->embed;
+  a.res = d_result;
+  a.w1 = w->w1;
+  a.b1 = w->b1;
+  a.w2 = w->w2;
+  a.b2 = w->b2;
+  a.w3 = w->w3;
+  a.b3 = w->b3;
+  a.y1 = (float *)d_ws;
+  a.logits3 = d_logits3;
+  a.cls = d_class;
+  return hip_status(launch_hrad(a, stream));
 }
 
 sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_len,

@@ -192,7 +192,8 @@ __global__ __launch_bounds__(kNormThreads) void k_rmsnorm_pack(float *__restrict
                                                                const float *__restrict__ g,
                                                                int hidden, int ks, int n_tok,
                                                                float eps,
-                                                               uint16_t *__restrict__ out) {
+                                                               uint16_t *__restrict__ out,
+                                                               float *__restrict__ tap) {
   const int t = blockIdx.x;
   __shared__ float red[kNormThreads / 64];
   const int items = ks * 4;
@@ -240,6 +241,11 @@ __global__ __launch_bounds__(kNormThreads) void k_rmsnorm_pack(float *__restrict
         f32x4 *dst = (f32x4 *)(h + (size_t)t * hidden + k0);
         dst[0] = hv[j][0];
         dst[1] = hv[j][1];
+        if (tap) {  // the residual after the previous layer, for H-RAD
+          f32x4 *tp = (f32x4 *)(tap + (size_t)t * hidden + k0);
+          tp[0] = hv[j][0];
+          tp[1] = hv[j][1];
+        }
       }
     }
 #pragma unroll
@@ -309,14 +315,14 @@ hipError_t launch_embed_meta(const EmbedArgs &a, const TreeArg &tree, int blocks
 
 hipError_t launch_rmsnorm_pack(float *h, const float *delta, int n_delta, const float *g,
                                int hidden, int ks, int n_tok, int n_pad, float eps, uint16_t *out,
-                               hipStream_t s) {
+                               hipStream_t s, float *tap) {
   if (hidden % 8 != 0 || n_delta < 1 || n_delta > kMaxSplit) return hipErrorInvalidValue;
   const int ipt = (ks * 4 + kNormThreads - 1) / kNormThreads;
   switch (ipt) {
 #define SB_IPT(n)                                                                              \
   case n:                                                                                      \
     hipLaunchKernelGGL(k_rmsnorm_pack<n>, dim3(n_pad), dim3(kNormThreads), 0, s, h, delta,        \
-                       n_delta, g, hidden, ks, n_tok, eps, out);                               \
+                       n_delta, g, hidden, ks, n_tok, eps, out, tap);                          \
     break;
     SB_IPT(1) SB_IPT(2) SB_IPT(3) SB_IPT(4) SB_IPT(5) SB_IPT(6) SB_IPT(7) SB_IPT(8)
 #undef SB_IPT

@@ -143,9 +143,24 @@ hipError_t launch_pack_bf16(int kind, const sb_model_config &c, const void *src0
                             const void *src2, void *dst, hipStream_t s);
 hipError_t launch_embed_meta(const EmbedArgs &a, const TreeArg &tree, int blocks, int bf16,
                              hipStream_t s);
+// tap (nullable, [n_tok][hidden] fp32): also receives the residual rows
+// after the delta slices are added
 hipError_t launch_rmsnorm_pack(float *h, const float *delta, int n_delta, const float *g,
                                int hidden, int ks, int n_tok, int n_pad, float eps, uint16_t *out,
-                               hipStream_t s);
+                               hipStream_t s, float *tap = nullptr);
+// H-RAD (k_hrad.hip): y1 = ReLU(W1 z + b1) into ws, then the 64-unit layer,
+// the 3 logits and their argmax
+struct HradArgs {
+  const float *taps;  // [k][max_rows][hidden]
+  int k, max_rows, hidden, vocab;
+  const uint16_t *embed;  // bf16 [vocab][hidden]
+  const sb_step_result *res;
+  const float *w1, *b1, *w2, *b2, *w3, *b3;
+  float *y1;  // [SB_HRAD_H1] workspace
+  float *logits3;
+  int32_t *cls;
+};
+hipError_t launch_hrad(const HradArgs &a, hipStream_t s);
 // Launch geometry of a GEMM: token tiles (rounded up to a kernel's), tiles per
 // pass, K split, tile groups and grid.
 // Largest tiles per pass of the GEMM kernel per token-tile count (its

@@ -89,3 +89,32 @@ def test_host_validation_without_device(api):
     assert lib.sb_select_branch(10, 1, 1, 1.0, 0, 1, 1, 1, 1, 1, 1 << 20, None) == 1
     assert lib.sb_kv_rollback(None, C.byref(kv), 3, 1, 1, None) == 1
     assert lib.sb_sample_workspace_bytes(1000) == 16000
+
+
+def test_hrad_host_validation_without_device(api):
+    """H-RAD's tap and predictor reject bad arguments before any launch; a
+    model record needs no device (sb_model_create keeps the pointers)."""
+    lib = api.lib
+    w = api.ModelWeights(1, 1, 1, (api.LayerWeights * 2)(*[api.LayerWeights(1, 1, 1, 1, 1, 1)] * 2))
+    h16, h32 = C.c_void_p(), C.c_void_p()
+    assert lib.sb_model_create(C.byref(cfg(api, n_layers=2, dtype=api.SB_BF16)), C.byref(w), C.byref(h16)) == 0
+    assert lib.sb_model_create(C.byref(cfg(api, n_layers=2, dtype=api.SB_F32)), C.byref(w), C.byref(h32)) == 0
+    try:
+        assert lib.sb_model_set_tap(None, 1, 1, 4) == 1
+        assert lib.sb_model_set_tap(h32, 1, 1, 4) == 4          # float32 models: no tap
+        assert lib.sb_model_set_tap(h16, 1, 0, 4) == 1          # k outside 1..n_layers
+        assert lib.sb_model_set_tap(h16, 1, 3, 4) == 1
+        assert lib.sb_model_set_tap(h16, 1, 2, 257) == 1        # rows outside 1..SB_MAX_ROWS
+        assert lib.sb_model_set_tap(h16, 1, 2, 4) == 0
+        assert lib.sb_model_set_tap(h16, None, 0, 0) == 0       # cleared
+        assert lib.sb_hrad_workspace_bytes() == 1024
+        hw = api.HradWeights(1, 1, 1, 1, 1, 1)
+        args = lambda m, k=2, rows=4, ws=1024, hwp=C.byref(hw): (m, 1, k, rows, 1, hwp, 1, 1, 1, ws, None)
+        assert lib.sb_hrad_predict(*args(None)) == 1
+        assert lib.sb_hrad_predict(*args(h32)) == 4
+        assert lib.sb_hrad_predict(*args(h16, k=3)) == 1
+        assert lib.sb_hrad_predict(*args(h16, ws=512)) == 3
+        assert lib.sb_hrad_predict(*args(h16, hwp=C.byref(api.HradWeights(1, 1, 1, None, 1, 1)))) == 1
+    finally:
+        lib.sb_model_destroy(h16)
+        lib.sb_model_destroy(h32)

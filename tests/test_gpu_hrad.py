@@ -1,0 +1,132 @@
+"""GPU parity of H-RAD's feature tap and predictor (Section "H-RAD",
+equations for z_t and s_t) against the oracle.
+
+The tap: with sb_model_set_tap, the verify forward writes the residual
+stream after each of the last K layers; it must match the oracle's hidden
+states (bf16 emulation) to the logits' bound, 2e-2 per row.  The
+predictor: the GPU's three logits from its own taps and the embedding of
+the walk's next token against the oracle's float64 MLP on the same inputs
+(float32 accumulation over 768..1280 inputs: 1e-4 relative to the largest
+logit), and the class wherever the two largest logits differ by more than
+that bound.  A result naming no usable row or token yields class -1.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import row_relerr, say
+from oracle import decoder, hrad
+from paper_2506_01979_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+_W = {}
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2506_01979_amd import api as A
+    assert torch.cuda.is_available()
+    return A
+
+
+def weights(shape):
+    if shape.name not in _W:
+        _W[shape.name] = synth.model_weights(shape)
+    return _W[shape.name]
+
+
+def mlp_weights(din, seed):
+    g = np.random.default_rng(seed)
+    w = {"w1": g.standard_normal((256, din)) / np.sqrt(din), "b1": g.standard_normal(256) * 0.1,
+         "w2": g.standard_normal((64, 256)) / 16.0, "b2": g.standard_normal(64) * 0.1,
+         "w3": g.standard_normal((3, 64)) / 8.0, "b3": g.standard_normal(3) * 0.1}
+    return {k: v.astype(np.float32) for k, v in w.items()}
+
+
+def run_forward(api, shape, P, parents, K, max_rows):
+    W = weights(shape)
+    m = api.Model(shape, api.dict_tensors(W))
+    ptoks = synth.prefix_tokens(shape.vocab, P)
+    kv_len = P - 1
+    _, Kp, Vp = decoder.prefill(shape, W, ptoks[:-1], "bf16")
+    n = len(parents)
+    g = np.random.default_rng(P + n + K)
+    toks = g.integers(0, shape.vocab, n).astype(np.int32)
+    toks[0] = ptoks[-1]
+    k, v = m.new_kv(kv_len + n + 8)
+    m.load_kv(k, v, Kp, Vp, kv_len)
+    taps = torch.full((K, max_rows, shape.hidden), float("nan"), dtype=torch.float32, device="cuda")
+    m.sb_model_set_tap(taps, K, max_rows)
+    logits = torch.empty((n, shape.vocab), dtype=torch.float32, device="cuda")
+    stats = api.new_stats(n)
+    m.sb_verify_forward(k, v, kv_len, torch.from_numpy(toks).cuda(), parents, 1.0, logits, stats,
+                        m.workspace(n, kv_len))
+    torch.cuda.synchronize()
+    hidden = []
+    decoder.tree_forward(shape, W, Kp, Vp, kv_len, toks, parents, "bf16", hidden=hidden)
+    return m, W, taps, hidden, n
+
+
+@pytest.mark.parametrize("sname,P,K", [("small_bf16", 128, 2), ("small_bf16", 300, 1),
+                                       ("ragged_bf16", 90, 2), ("small_gqa_bf16", 200, 2)])
+def test_tap_matches_oracle_hidden_states(api, sname, P, K):
+    shape = synth.SHAPES[sname]
+    parents = synth.branch_parents(4, 8)
+    say(f"hrad tap {sname} P={P} K={K}")
+    m, W, taps, hidden, n = run_forward(api, shape, P, parents, K, 40)
+    got = taps.cpu().numpy()
+    for kk in range(K):
+        want = hidden[shape.n_layers - K + kk]
+        assert np.all(np.isfinite(got[kk, :n]))
+        err = row_relerr(got[kk, :n], want)
+        say(f"  tap {kk}: row-relative error {err:.3e}")
+        assert err < 2e-2
+    # rows past the call's rows are untouched
+    assert np.all(np.isnan(got[:, n:]))
+    m.sb_model_set_tap(None)
+
+
+def test_predict_matches_oracle(api):
+    shape = synth.SHAPES["small_bf16"]
+    K, rows = 2, 40
+    parents = synth.branch_parents(4, 8)
+    say("hrad predict small_bf16")
+    m, W, taps, hidden, n = run_forward(api, shape, 128, parents, K, rows)
+    m.sb_model_set_tap(None)
+    tap_h = taps.cpu().numpy().astype(np.float64)
+    emb = decoder.round_bf16(np.asarray(W["embed"], np.float32)).astype(np.float64)
+    ws = torch.empty(api.lib.sb_hrad_workspace_bytes(), dtype=torch.uint8, device="cuda")
+    logits3 = torch.empty(3, dtype=torch.float32, device="cuda")
+    cls = torch.empty(1, dtype=torch.int32, device="cuda")
+    checked = 0
+    for case in range(12):
+        w = mlp_weights((K + 1) * shape.hidden, 100 + case)
+        wd = {k: torch.from_numpy(v).cuda() for k, v in w.items()}
+        g = np.random.default_rng(case)
+        path = [0] + [1 + (case % 4) * 8 + j for j in range(case % 9)]
+        y = int(g.integers(0, shape.vocab))
+        a = np.full(api.STEP_RESULT_INTS, -1, np.int32)
+        a[:8] = [len(path) - 1, case % 4, y, len(path), 0, 0, 0, 0]
+        a[8:8 + len(path)] = path
+        res = torch.from_numpy(a).cuda()
+        m.sb_hrad_predict(taps, K, rows, res, wd, logits3, cls, ws)
+        torch.cuda.synchronize()
+        r = path[-1]
+        z = hrad.features([tap_h[kk, r] for kk in range(K)], emb[y])
+        want, s = hrad.predict(z, *(w[k].astype(np.float64) for k in ("w1", "b1", "w2", "b2", "w3", "b3")))
+        got = logits3.cpu().numpy().astype(np.float64)
+        scale = max(1e-30, float(np.max(np.abs(want))))
+        err = float(np.max(np.abs(got - want))) / scale
+        say(f"  case {case}: row {r} token {y} logits err {err:.2e} class {int(cls.item())} vs {s}")
+        assert err < 1e-4
+        top = np.sort(want)[::-1]
+        if (top[0] - top[1]) / scale > 1e-4:
+            assert int(cls.item()) == s
+            checked += 1
+    assert checked >= 8
+    # a result naming no usable token: class -1, zero logits
+    a[2] = shape.vocab
+    m.sb_hrad_predict(taps, K, rows, torch.from_numpy(a).cuda(), wd, logits3, cls, ws)
+    torch.cuda.synchronize()
+    assert int(cls.item()) == -1 and not np.any(logits3.cpu().numpy())
