@@ -12,6 +12,9 @@ MI355X path computes, written from the paper:
   (Preliminaries, "Speculative Decoding"), Branch Speculative Sampling
   (Appendix, Algorithm 1) at multi-child nodes, and inverse-CDF draws;
 * ``oracle.rollback`` -- KV compaction to the accepted path;
+* ``oracle.branching`` -- branch-point candidates (Section "Branch
+  Resampling"): B = max(1, floor(k_max (1 - q(x_b)))), TopK / i.i.d. /
+  without-replacement draws, each with the q row it carries;
 * ``oracle.hrad``     -- H-RAD's length predictor (Section "H-RAD"): the
   last K layers' hidden states and the new token's embedding through a
   256/64/3 ReLU MLP, s_t = argmax.
@@ -26,4 +29,4 @@ output distribution, closed forms printed in the paper, hand-worked golden
 cases).  Nothing here is "parity unpinned".
 """
 
-from . import tree, decoder, sampling, rollback, hrad  # noqa: F401
+from . import tree, decoder, sampling, rollback, hrad, branching  # noqa: F401
