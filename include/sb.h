@@ -276,6 +276,47 @@ sb_status sb_hrad_predict(const sb_model *m, const float *d_taps, int32_t k_laye
                           const sb_hrad_weights *w, float *d_logits3, int32_t *d_class,
                           void *d_ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- branch-point candidates (draft side) --------------------------- */
+
+/* Candidate rules of sb_branch_candidates. */
+typedef enum {
+  SB_BRANCH_TOPK = 0, /* the B largest entries of q, one-hot rows */
+  SB_BRANCH_IID = 1,  /* B independent inverse-CDF draws, each carrying q */
+  SB_BRANCH_WOR = 2   /* draws without replacement, each carrying its remainder */
+} sb_branch_mode;
+
+#define SB_BRANCH_MAX_K 16
+#define SB_BRANCH_MAX_VOCAB 1048576
+
+/* Workspace bytes of sb_branch_candidates. */
+size_t sb_branch_workspace_bytes(void);
+
+/* Sibling first tokens at a branch point (Section "Branch Resampling"):
+ * B = max(1, floor(k_max (1 - q[x_b]))) computed in float64 from the float32
+ * q[x_b], at most the number of tokens with q > 0 (B = 0 when there are
+ * none).  d_q: float32 [vocab], the draft's distribution at the branch
+ * position (finite, non-negative; other values give unspecified candidates,
+ * never a fault).  Each candidate carries the distribution it was drawn
+ * from, which verification (Algorithm 1) subtracts from p:
+ *  - SB_BRANCH_TOPK: the B largest entries, in descending order, lowest
+ *    index first among equal values; row i is one-hot at token i;
+ *  - SB_BRANCH_IID: token i is the first v whose float64 running sum of q
+ *    over 0..v exceeds d_u[i] times the total; row i is q;
+ *  - SB_BRANCH_WOR: the same draw over q with candidates 0..i-1 zeroed;
+ *    row i is that remainder r divided by its float64 mass, float32(r_v / Z).
+ * d_u: float32 [k_max] uniforms in [0, 1) (unused, may be NULL, for TOPK).
+ * Outputs: *d_count = B; d_tokens[k_max] (entries B.. set to -1);
+ * d_rows float32 [k_max][vocab], rows 0..B-1 written, the rest untouched.
+ * Draws sum in a tree order, so a u within rounding of a boundary of the
+ * running sum may pick the neighbouring token.  1 <= k_max <= SB_BRANCH_MAX_K,
+ * 0 <= x_b < vocab <= SB_BRANCH_MAX_VOCAB, else SB_ERR_INVALID_ARG;
+ * ws_bytes below sb_branch_workspace_bytes() gives SB_ERR_CAPACITY.  No
+ * model is involved. */
+sb_status sb_branch_candidates(const float *d_q, int32_t vocab, int32_t x_b, int32_t k_max,
+                               int32_t mode, const float *d_u, int32_t *d_count,
+                               int32_t *d_tokens, float *d_rows, void *d_ws, size_t ws_bytes,
+                               hipStream_t stream);
+
 /* ---- measurement ---------------------------------------------------- */
 
 /* Kernel classes of the verify step, for sb_timer_start. */

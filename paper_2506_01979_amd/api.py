@@ -30,9 +30,12 @@ EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight"
            "sb_model_create", "sb_model_destroy", "sb_workspace_bytes", "sb_verify_forward",
            "sb_softmax_stats", "sb_sample_workspace_bytes", "sb_select_branch",
            "sb_accept_resample", "sb_kv_rollback", "sb_timer_start", "sb_timer_stop",
-           "sb_model_set_tap", "sb_hrad_workspace_bytes", "sb_hrad_predict")
+           "sb_model_set_tap", "sb_hrad_workspace_bytes", "sb_hrad_predict",
+           "sb_branch_workspace_bytes", "sb_branch_candidates")
 
 SB_HRAD_H1, SB_HRAD_H2, SB_HRAD_CLASSES = 256, 64, 3
+BRANCH_MODES = {"topk": 0, "iid": 1, "wor": 2}
+SB_BRANCH_MAX_K, SB_BRANCH_MAX_VOCAB = 16, 1048576
 
 KERNEL_CLASSES = {"qkv": 0, "o": 1, "gate_up": 2, "down": 3, "lm_head": 4, "attn": 5,
                   "attn_merge": 6, "norm": 7, "stats": 8}
@@ -110,6 +113,11 @@ lib.sb_model_set_tap.restype = _i32
 lib.sb_model_set_tap.argtypes = [_vp, _vp, _i32, _i32]
 lib.sb_hrad_workspace_bytes.restype = _sz
 lib.sb_hrad_workspace_bytes.argtypes = []
+lib.sb_branch_workspace_bytes.restype = _sz
+lib.sb_branch_workspace_bytes.argtypes = []
+lib.sb_branch_candidates.restype = _i32
+lib.sb_branch_candidates.argtypes = [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz,
+                                     _vp]
 lib.sb_hrad_predict.restype = _i32
 lib.sb_hrad_predict.argtypes = [_vp, _vp, _i32, _i32, _vp, C.POINTER(HradWeights), _vp, _vp,
                                 _vp, _sz, _vp]
@@ -213,6 +221,29 @@ def sb_accept_resample(tokens: torch.Tensor, parents, logits: torch.Tensor, stat
                                   result.data_ptr(), ws.data_ptr(),
                                   ws.numel() * ws.element_size(), _stream(stream)),
            "sb_accept_resample")
+
+
+def sb_branch_workspace_bytes() -> int:
+    return int(lib.sb_branch_workspace_bytes())
+
+
+def sb_branch_candidates(q: torch.Tensor, x_b: int, k_max: int, mode: str, u, count: torch.Tensor,
+                         tokens: torch.Tensor, rows: torch.Tensor, ws: torch.Tensor,
+                         stream=None) -> None:
+    """q float32 [vocab]; u float32 [k_max] (None for "topk"); count int32 [1];
+    tokens int32 [k_max]; rows float32 [k_max][vocab]."""
+    v = q.shape[-1]
+    _need(q, v * 4, "q", torch.float32)
+    if u is not None:
+        _need(u, k_max * 4, "u", torch.float32)
+    _need(count, 4, "count", torch.int32)
+    _need(tokens, k_max * 4, "tokens", torch.int32)
+    _need(rows, k_max * v * 4, "rows", torch.float32)
+    _need(ws, sb_branch_workspace_bytes(), "ws")
+    _check(lib.sb_branch_candidates(q.data_ptr(), v, x_b, k_max, BRANCH_MODES[mode], _ptr(u),
+                                    count.data_ptr(), tokens.data_ptr(), rows.data_ptr(),
+                                    ws.data_ptr(), ws.numel() * ws.element_size(),
+                                    _stream(stream)), "sb_branch_candidates")
 
 
 def sb_sample_workspace_bytes(vocab: int) -> int:

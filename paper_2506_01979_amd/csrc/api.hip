@@ -642,6 +642,35 @@ sb_status sb_hrad_predict(const sb_model *m, const float *d_taps, int32_t k_laye
   return hip_status(launch_hrad(a, stream));
 }
 
+size_t sb_branch_workspace_bytes(void) { return 256; }
+
+sb_status sb_branch_candidates(const float *d_q, int32_t vocab, int32_t x_b, int32_t k_max,
+                               int32_t mode, const float *d_u, int32_t *d_count,
+                               int32_t *d_tokens, float *d_rows, void *d_ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  if (!d_q || !d_count || !d_tokens || !d_rows || !d_ws) return SB_ERR_INVALID_ARG;
+  if (mode != SB_BRANCH_TOPK && mode != SB_BRANCH_IID && mode != SB_BRANCH_WOR)
+    return SB_ERR_INVALID_ARG;
+  if (mode != SB_BRANCH_TOPK && !d_u) return SB_ERR_INVALID_ARG;
+  if (vocab < 1 || vocab > SB_BRANCH_MAX_VOCAB || x_b < 0 || x_b >= vocab || k_max < 1 ||
+      k_max > SB_BRANCH_MAX_K)
+    return SB_ERR_INVALID_ARG;
+  if (ws_bytes < sb_branch_workspace_bytes()) return SB_ERR_CAPACITY;
+  BranchArgs a{};
+  a.q = d_q;
+  a.vocab = vocab;
+  a.x_b = x_b;
+  a.k_max = k_max;
+  a.mode = mode;
+  a.vec4 = vocab % 4 == 0 && ((uintptr_t)d_q & 15) == 0 && ((uintptr_t)d_rows & 15) == 0;
+  a.u = d_u;
+  a.count = d_count;
+  a.tokens = d_tokens;
+  a.rows = d_rows;
+  a.znorm = (double *)d_ws;
+  return hip_status(launch_branch(a, stream));
+}
+
 sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
                          const sb_step_result *d_result, int32_t *d_new_len,
                          hipStream_t stream) {

@@ -161,6 +161,18 @@ struct HradArgs {
   int32_t *cls;
 };
 hipError_t launch_hrad(const HradArgs &a, hipStream_t s);
+// Branch-point candidates (k_branch.hip): the selection on one workgroup,
+// then the carried rows
+struct BranchArgs {
+  const float *q;  // [vocab]
+  int vocab, x_b, k_max, mode;
+  int vec4;        // vocab % 4 == 0 and q, rows 16-byte aligned
+  const float *u;  // [k_max]
+  int32_t *count, *tokens;
+  float *rows;     // [k_max][vocab]
+  double *znorm;   // [SB_BRANCH_MAX_K] workspace: the mass before each draw
+};
+hipError_t launch_branch(const BranchArgs &a, hipStream_t s);
 // Launch geometry of a GEMM: token tiles (rounded up to a kernel's), tiles per
 // pass, K split, tile groups and grid.
 // Largest tiles per pass of the GEMM kernel per token-tile count (its

@@ -118,3 +118,30 @@ def test_hrad_host_validation_without_device(api):
     finally:
         lib.sb_model_destroy(h16)
         lib.sb_model_destroy(h32)
+
+
+def test_branch_candidates_host_validation_without_device(api):
+    """Branch-point candidates reject bad arguments before any launch (the
+    pointers are never dereferenced on these paths)."""
+    lib = api.lib
+    assert lib.sb_branch_workspace_bytes() >= 8 * api.SB_BRANCH_MAX_K
+
+    def call(q=1, vocab=1000, x_b=3, k_max=6, mode=2, u=1, count=1, toks=1, rows=1, ws=1,
+             ws_bytes=None):
+        wb = lib.sb_branch_workspace_bytes() if ws_bytes is None else ws_bytes
+        return lib.sb_branch_candidates(q, vocab, x_b, k_max, mode, u, count, toks, rows, ws, wb,
+                                        None)
+    assert call(q=None) == 1
+    assert call(rows=None) == 1
+    assert call(ws=None) == 1
+    assert call(mode=3) == 1
+    assert call(mode=-1) == 1
+    assert call(u=None) == 1                      # draws need uniforms ...
+    assert call(mode=1, u=None) == 1
+    assert call(x_b=1000) == 1                    # x_b outside the vocabulary
+    assert call(x_b=-1) == 1
+    assert call(k_max=0) == 1
+    assert call(k_max=api.SB_BRANCH_MAX_K + 1) == 1
+    assert call(vocab=0, x_b=0) == 1
+    assert call(vocab=api.SB_BRANCH_MAX_VOCAB + 1) == 1
+    assert call(ws_bytes=8) == 3
