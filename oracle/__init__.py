@@ -15,6 +15,9 @@ MI355X path computes, written from the paper:
 * ``oracle.branching`` -- branch-point candidates (Section "Branch
   Resampling"): B = max(1, floor(k_max (1 - q(x_b)))), TopK / i.i.d. /
   without-replacement draws, each with the q row it carries;
+* ``oracle.drafting`` -- the draft side of a round: the draft's float32 q
+  rows and their draws, and a drafting phase with a branch point after the
+  root (Section "Branch Resampling") on the same decoder definition;
 * ``oracle.hrad``     -- H-RAD's length predictor (Section "H-RAD"): the
   last K layers' hidden states and the new token's embedding through a
   256/64/3 ReLU MLP, s_t = argmax.
@@ -29,4 +32,4 @@ output distribution, closed forms printed in the paper, hand-worked golden
 cases).  Nothing here is "parity unpinned".
 """
 
-from . import tree, decoder, sampling, rollback, hrad, branching  # noqa: F401
+from . import tree, decoder, sampling, rollback, hrad, branching, drafting  # noqa: F401
