@@ -143,7 +143,7 @@ def pmc_summary(fetch_dir: str, write_dir: str) -> str:
     cmd = ("cd /tmp && export TMPDIR=/tmp && "
            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <repo>/gpurun_out/pmc_fetch -o run -- "
            "python3 <repo>/bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-alpha-sweep "
-           "--no-hrad --no-graph --copy-calibration; the same with --pmc WRITE_SIZE into "
+           "--no-hrad --no-draft --no-graph --copy-calibration; the same with --pmc WRITE_SIZE into "
            "gpurun_out/pmc_write; then "
            "python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write")
     return "\n".join([
@@ -214,7 +214,7 @@ def trace_summary(trace_dir: str) -> str:
     out = [f"# Kernel trace of the verify step, {WORKLOAD}", "",
            "Command: `cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
            "--output-format csv -d <repo>/gpurun_out/prof_step -o run -- python3 <repo>/bench.py "
-           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-graph`, then "
+           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-draft --no-graph`, then "
            "`python3 bench.py --trace-summary gpurun_out/prof_step`", "",
            f"Last {len(steps)} complete steps (embed .. stats, then the accept walk and the rollback "
            f"when traced): span "
@@ -407,6 +407,8 @@ def main():
                     help="skip the HIP-graph replay measurement")
     ap.add_argument("--no-hrad", action="store_true",
                     help="skip the H-RAD measurement (feature tap + predictor)")
+    ap.add_argument("--no-draft", action="store_true",
+                    help="skip the draft-side measurement (68M draft round, candidates, sampler)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="end with a device copy of known size (for rocprofv3 --pmc runs)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -458,16 +460,19 @@ def main():
     m = api.Model(shape, tensor_fn, device=dev)
     log(f"weights generated, uploaded and packed in {time.time() - t0:.1f}s")
 
+    def fill_prefix(shp, kb_, vb_, keep=None):
+        for l in range(shp.n_layers):
+            kb = synth.synthetic_kv(shp, l, kv_len, kv_len, 0, as_bits=True)
+            vb = synth.synthetic_kv(shp, l, kv_len, kv_len, 1, as_bits=True)
+            kb_[l, :, :kv_len] = torch.from_numpy(kb.view(np.int16)).view(torch.bfloat16).to(dev)
+            vb_[l, :, :, :kv_len] = torch.from_numpy(vb.view(np.int16)).view(torch.bfloat16).to(dev).transpose(1, 2)
+            if keep is not None and l < args.cpu_layers:
+                keep[l] = (kb, vb)
+
     cap = kv_len + n + 16
     k_, v_ = m.new_kv(cap)
     kv_host = {}
-    for l in range(shape.n_layers):
-        kb = synth.synthetic_kv(shape, l, kv_len, kv_len, 0, as_bits=True)
-        vb = synth.synthetic_kv(shape, l, kv_len, kv_len, 1, as_bits=True)
-        k_[l, :, :kv_len] = torch.from_numpy(kb.view(np.int16)).view(torch.bfloat16).to(dev)
-        v_[l, :, :, :kv_len] = torch.from_numpy(vb.view(np.int16)).view(torch.bfloat16).to(dev).transpose(1, 2)
-        if l < args.cpu_layers:
-            kv_host[l] = (kb, vb)
+    fill_prefix(shape, k_, v_, kv_host)
     log(f"prefix KV ready ({kv_len} slots) at {time.time() - t0:.1f}s")
 
     root = int(synth.prefix_tokens(shape.vocab, P)[-1])
@@ -591,6 +596,79 @@ def main():
                     "w1_bytes": 256 * din * 4, "class": int(cls.item())}
         del taps
 
+    # The draft side (Section "Branch Resampling"): one drafting round of the
+    # 68M draft on its own prefix cache of the same length, k_max = B and
+    # depth k (a near-flat q at the branch point gives the verify step's B),
+    # then the branch-point candidates and the draft sampler on their own.
+    # Not part of `value`.
+    draft_out = None
+    if not args.no_draft:
+        dshape = synth.SHAPES["draft68m"]
+        dm = api.Model(dshape, api.synth_tensors(dshape, seed=1), device=dev)
+        DK, DD = B, kd
+        R = 1 + DK * DD
+        dk_, dv_ = dm.new_kv(kv_len + R + 8)
+        fill_prefix(dshape, dk_, dv_)
+        du = torch.from_numpy(synth.uniforms(R, 31)).to(dev)
+        dtok = torch.full((R,), root, dtype=torch.int32, device=dev)
+        dq = torch.empty((R, dshape.vocab), dtype=torch.float32, device=dev)
+        dws = dm.draft_round_workspace(DK, DD, kv_len)
+
+        def draft_round():
+            return dm.sb_draft_round(dk_, dv_, kv_len, DK, "wor", DD, 1.0, du, dtok, dq, dws, stream)
+        for _ in range(2):
+            draft_round()
+        torch.cuda.synchronize()
+        reps = 20
+        ev0.record(stream)
+        for _ in range(reps):
+            bd, _ = draft_round()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        round_ms = ev0.elapsed_time(ev1) / reps
+        V = dshape.vocab
+        cq = dq[0].contiguous()
+        cxb = dtok[1:2].clone()
+        ccount = torch.empty(1, dtype=torch.int32, device=dev)
+        ctok = torch.empty(16, dtype=torch.int32, device=dev)
+        crows = torch.empty((16, V), dtype=torch.float32, device=dev)
+        cws = torch.empty(api.sb_branch_workspace_bytes(), dtype=torch.uint8, device=dev)
+        cu = torch.from_numpy(synth.uniforms(16, 32)).to(dev)
+        cand_us = {}
+        for mode in ("topk", "iid", "wor"):
+            for _ in range(3):
+                api.sb_branch_candidates(cq, cxb, 6, mode, cu, ccount, ctok, crows, cws, stream)
+            torch.cuda.synchronize()
+            ev0.record(stream)
+            for _ in range(200):
+                api.sb_branch_candidates(cq, cxb, 6, mode, cu, ccount, ctok, crows, cws, stream)
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            cand_us[mode] = round(ev0.elapsed_time(ev1) * 1e3 / 200, 2)
+        cand_b = int(ccount.item())
+        src = list(range(1, 1 + B))
+        dst = list(range(1, 1 + B))
+        for _ in range(3):
+            api.sb_draft_sample(logits, stats, src, 1.0, du, dtok, dq, dst, stream)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(200):
+            api.sb_draft_sample(logits, stats, src, 1.0, du, dtok, dq, dst, stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        samp_us = ev0.elapsed_time(ev1) * 1e3 / 200
+        draft_out = {"shape": f"{dshape.name}: {dshape.n_layers} layers, hidden {dshape.hidden}, "
+                              f"{dshape.n_heads}x{dshape.head_dim} heads, ffn {dshape.ffn}, "
+                              f"vocab {V}, bf16",
+                     "round": f"k_max={DK}, depth={DD}, without replacement, T=1, prefix {P}",
+                     "round_ms": round(round_ms, 4), "branches": bd,
+                     "round_plus_verify_ms": round(round_ms + ms_per_step, 4),
+                     "candidates_us_k6": cand_us, "candidates_B": cand_b,
+                     "candidates_bytes_k6_wor": 4 * V * (1 + cand_b),
+                     "sample_us": round(samp_us, 2), "sample_rows": B,
+                     "sample_bytes": 2 * 4 * V * B}
+        del dm, dk_, dv_, dq, crows
+
     if args.copy_calibration:
         # a plain device copy of known size, for scaling the HBM byte counters
         src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
@@ -635,6 +713,8 @@ def main():
     }
     if hrad_out is not None:
         out["hrad"] = hrad_out
+    if draft_out is not None:
+        out["draft"] = draft_out
 
     if not args.no_alpha_sweep:
         sweep = {}

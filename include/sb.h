@@ -294,7 +294,9 @@ size_t sb_branch_workspace_bytes(void);
 /* Sibling first tokens at a branch point (Section "Branch Resampling"):
  * B = max(1, floor(k_max (1 - q[x_b]))) computed in float64 from the float32
  * q[x_b], at most the number of tokens with q > 0 (B = 0 when there are
- * none).  d_q: float32 [vocab], the draft's distribution at the branch
+ * none).  *d_x_b: the draft's token at the branch position, read on the
+ * device (a value outside the vocabulary counts as q[x_b] = 0).
+ * d_q: float32 [vocab], the draft's distribution at the branch
  * position (finite, non-negative; other values give unspecified candidates,
  * never a fault).  Each candidate carries the distribution it was drawn
  * from, which verification (Algorithm 1) subtracts from p:
@@ -309,13 +311,67 @@ size_t sb_branch_workspace_bytes(void);
  * d_rows float32 [k_max][vocab], rows 0..B-1 written, the rest untouched.
  * Draws sum in a tree order, so a u within rounding of a boundary of the
  * running sum may pick the neighbouring token.  1 <= k_max <= SB_BRANCH_MAX_K,
- * 0 <= x_b < vocab <= SB_BRANCH_MAX_VOCAB, else SB_ERR_INVALID_ARG;
+ * 1 <= vocab <= SB_BRANCH_MAX_VOCAB, else SB_ERR_INVALID_ARG;
  * ws_bytes below sb_branch_workspace_bytes() gives SB_ERR_CAPACITY.  No
  * model is involved. */
-sb_status sb_branch_candidates(const float *d_q, int32_t vocab, int32_t x_b, int32_t k_max,
+sb_status sb_branch_candidates(const float *d_q, int32_t vocab, const int32_t *d_x_b, int32_t k_max,
                                int32_t mode, const float *d_u, int32_t *d_count,
                                int32_t *d_tokens, float *d_rows, void *d_ws, size_t ws_bytes,
                                hipStream_t stream);
+
+/* ---- the draft side of a round ----------------------------------------- */
+
+#define SB_DRAFT_MAX_ROWS 64
+
+/* The draft's rows: for i < n, the distribution of logits row h_src_rows[i]
+ * at T -- the p(v) the verify step defines, stored as float32 because that
+ * row is what verification reads as q -- is written to row h_dst_rows[i] of
+ * d_q, and the token drawn from those float32 values with d_u[i] (the first
+ * v whose float64 running sum in vocabulary order exceeds d_u[i] times their
+ * total) to d_tokens[h_dst_rows[i]].  T = 0: q is one-hot at the row's
+ * argmax, which is the token.  d_logits: float32 [n_logit_rows][vocab] with
+ * d_stats their sb_row_stats at the same T (as sb_verify_forward and
+ * sb_softmax_stats write them; finite logits); d_tokens: int32
+ * [n_out_rows]; d_q: float32 [n_out_rows][vocab].  1 <= n <=
+ * SB_DRAFT_MAX_ROWS, 0 <= h_src_rows[i] < n_logit_rows, 0 <= h_dst_rows[i]
+ * < n_out_rows and distinct, T >= 0, else SB_ERR_INVALID_ARG. */
+sb_status sb_draft_sample(int32_t vocab, int32_t n, const float *d_logits,
+                          const sb_row_stats *d_stats, int32_t n_logit_rows,
+                          const int32_t *h_src_rows, float temperature, const float *d_u,
+                          int32_t *d_tokens, float *d_q, int32_t n_out_rows,
+                          const int32_t *h_dst_rows, hipStream_t stream);
+
+/* Workspace bytes of sb_draft_round (0 for arguments it rejects). */
+size_t sb_draft_round_workspace_bytes(const sb_model *draft, int32_t k_max, int32_t depth,
+                                      int32_t kv_len);
+
+/* One drafting phase of a SpecBranch round with its branch point right after
+ * the root (Section "Branch Resampling"; the drafting of Algorithm 2), on
+ * the draft model's prefix cache (kv_len slots):
+ *  1. the draft scores the root (d_tokens[0] on entry: the last committed
+ *     token, whose KV is not yet cached); x_b is drawn from its q with
+ *     d_u[0];
+ *  2. sb_branch_candidates spawns B first tokens from that q by `mode`,
+ *     with d_u[1 .. k_max];
+ *  3. each branch continues on its own path: its depth-d token (d = 2 ..
+ *     depth) is drawn by sb_draft_sample from the draft's distribution at
+ *     its depth d - 1 row, with d_u[1 + k_max (d - 1) + i] for branch i;
+ *     every step is one sb_verify_forward of the draft over the tree so far.
+ * The tree is depth-major: row 1 + (d - 1) B + i is branch i's depth-d
+ * token; its parent is row 0 at d = 1 and row - B after that.  Outputs:
+ * d_tokens[1 .. B depth] (int32 [1 + k_max depth]; later entries may be
+ * overwritten), d_q float32 [1 + k_max depth][vocab] (row i the
+ * distribution token i was drawn from; row 0 the root's, that of x_b),
+ * h_parents[0 .. B depth] (host, [1 + k_max depth]), *h_branches = B.  The
+ * draft's cache slots kv_len .. kv_len + B (depth - 1) are written
+ * (capacity at least kv_len + 1 + k_max depth).  d_u: float32
+ * [1 + k_max depth].
+ * Blocks the host once, to read B before sizing the tree.  1 <= k_max <=
+ * SB_BRANCH_MAX_K, depth >= 1, 1 + k_max depth <= SB_MAX_ROWS. */
+sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t k_max,
+                         int32_t mode, int32_t depth, float temperature, const float *d_u,
+                         int32_t *d_tokens, float *d_q, int32_t *h_parents, int32_t *h_branches,
+                         void *d_ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---- measurement ---------------------------------------------------- */
 

@@ -31,11 +31,13 @@ EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight"
            "sb_softmax_stats", "sb_sample_workspace_bytes", "sb_select_branch",
            "sb_accept_resample", "sb_kv_rollback", "sb_timer_start", "sb_timer_stop",
            "sb_model_set_tap", "sb_hrad_workspace_bytes", "sb_hrad_predict",
-           "sb_branch_workspace_bytes", "sb_branch_candidates")
+           "sb_branch_workspace_bytes", "sb_branch_candidates", "sb_draft_sample",
+           "sb_draft_round_workspace_bytes", "sb_draft_round")
 
 SB_HRAD_H1, SB_HRAD_H2, SB_HRAD_CLASSES = 256, 64, 3
 BRANCH_MODES = {"topk": 0, "iid": 1, "wor": 2}
 SB_BRANCH_MAX_K, SB_BRANCH_MAX_VOCAB = 16, 1048576
+SB_DRAFT_MAX_ROWS = 64
 
 KERNEL_CLASSES = {"qkv": 0, "o": 1, "gate_up": 2, "down": 3, "lm_head": 4, "attn": 5,
                   "attn_merge": 6, "norm": 7, "stats": 8}
@@ -116,8 +118,16 @@ lib.sb_hrad_workspace_bytes.argtypes = []
 lib.sb_branch_workspace_bytes.restype = _sz
 lib.sb_branch_workspace_bytes.argtypes = []
 lib.sb_branch_candidates.restype = _i32
-lib.sb_branch_candidates.argtypes = [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz,
+lib.sb_branch_candidates.argtypes = [_vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz,
                                      _vp]
+lib.sb_draft_sample.restype = _i32
+lib.sb_draft_sample.argtypes = [_i32, _i32, _vp, _vp, _i32, C.POINTER(_i32), _f, _vp, _vp, _vp,
+                                _i32, C.POINTER(_i32), _vp]
+lib.sb_draft_round_workspace_bytes.restype = _sz
+lib.sb_draft_round_workspace_bytes.argtypes = [_vp, _i32, _i32, _i32]
+lib.sb_draft_round.restype = _i32
+lib.sb_draft_round.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _i32, _i32, _f, _vp, _vp, _vp,
+                               C.POINTER(_i32), C.POINTER(_i32), _vp, _sz, _vp]
 lib.sb_hrad_predict.restype = _i32
 lib.sb_hrad_predict.argtypes = [_vp, _vp, _i32, _i32, _vp, C.POINTER(HradWeights), _vp, _vp,
                                 _vp, _sz, _vp]
@@ -227,23 +237,46 @@ def sb_branch_workspace_bytes() -> int:
     return int(lib.sb_branch_workspace_bytes())
 
 
-def sb_branch_candidates(q: torch.Tensor, x_b: int, k_max: int, mode: str, u, count: torch.Tensor,
-                         tokens: torch.Tensor, rows: torch.Tensor, ws: torch.Tensor,
-                         stream=None) -> None:
-    """q float32 [vocab]; u float32 [k_max] (None for "topk"); count int32 [1];
-    tokens int32 [k_max]; rows float32 [k_max][vocab]."""
+def sb_branch_candidates(q: torch.Tensor, x_b: torch.Tensor, k_max: int, mode: str, u,
+                         count: torch.Tensor, tokens: torch.Tensor, rows: torch.Tensor,
+                         ws: torch.Tensor, stream=None) -> None:
+    """q float32 [vocab]; x_b int32 [1] on the device; u float32 [k_max] (None
+    for "topk"); count int32 [1]; tokens int32 [k_max]; rows float32
+    [k_max][vocab]."""
     v = q.shape[-1]
     _need(q, v * 4, "q", torch.float32)
+    _need(x_b, 4, "x_b", torch.int32)
     if u is not None:
         _need(u, k_max * 4, "u", torch.float32)
     _need(count, 4, "count", torch.int32)
     _need(tokens, k_max * 4, "tokens", torch.int32)
     _need(rows, k_max * v * 4, "rows", torch.float32)
     _need(ws, sb_branch_workspace_bytes(), "ws")
-    _check(lib.sb_branch_candidates(q.data_ptr(), v, x_b, k_max, BRANCH_MODES[mode], _ptr(u),
+    _check(lib.sb_branch_candidates(q.data_ptr(), v, x_b.data_ptr(), k_max, BRANCH_MODES[mode], _ptr(u),
                                     count.data_ptr(), tokens.data_ptr(), rows.data_ptr(),
                                     ws.data_ptr(), ws.numel() * ws.element_size(),
                                     _stream(stream)), "sb_branch_candidates")
+
+
+def sb_draft_sample(logits: torch.Tensor, stats: torch.Tensor, src_rows, temperature: float,
+                    u: torch.Tensor, tokens: torch.Tensor, q: torch.Tensor, dst_rows,
+                    stream=None) -> None:
+    """logits float32 [n_logit_rows][vocab] with stats; tokens int32 [n_out];
+    q float32 [n_out][vocab]; u float32 [len(src_rows)]."""
+    nl, v = logits.shape
+    src, sp = _host_i32(src_rows)
+    dst, dp = _host_i32(dst_rows)
+    if len(src) != len(dst):
+        raise ValueError("src_rows and dst_rows differ in length")
+    n_out = tokens.numel()
+    _need(logits, nl * v * 4, "logits", torch.float32)
+    _need(stats, nl * 16, "stats")
+    _need(u, len(src) * 4, "u", torch.float32)
+    _need(tokens, n_out * 4, "tokens", torch.int32)
+    _need(q, n_out * v * 4, "q", torch.float32)
+    _check(lib.sb_draft_sample(v, len(src), logits.data_ptr(), stats.data_ptr(), nl, sp,
+                               temperature, u.data_ptr(), tokens.data_ptr(), q.data_ptr(), n_out,
+                               dp, _stream(stream)), "sb_draft_sample")
 
 
 def sb_sample_workspace_bytes(vocab: int) -> int:
@@ -469,6 +502,35 @@ class Model:
                                    result.data_ptr(), C.byref(hw), logits3.data_ptr(),
                                    cls.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
                                    _stream(stream)), "sb_hrad_predict")
+
+    def draft_round_workspace(self, k_max: int, depth: int, kv_len: int) -> torch.Tensor:
+        n = int(lib.sb_draft_round_workspace_bytes(self.handle, k_max, depth, kv_len))
+        if n == 0:
+            raise ValueError("sb_draft_round_workspace_bytes: arguments rejected")
+        return torch.empty(n, dtype=torch.uint8, device=self.device)
+
+    def sb_draft_round(self, k: torch.Tensor, v: torch.Tensor, kv_len: int, k_max: int, mode: str,
+                       depth: int, temperature: float, u: torch.Tensor, tokens: torch.Tensor,
+                       q: torch.Tensor, ws: torch.Tensor, stream=None):
+        """tokens int32 [1 + k_max*depth] with tokens[0] the root on entry;
+        q float32 [1 + k_max*depth][vocab]; u float32 [1 + k_max*depth].
+        Returns (B, parents as a numpy int32 array of 1 + B*depth entries)."""
+        self._check_kv(k, v)
+        R = 1 + k_max * depth
+        V = self.shape.vocab
+        _need(u, R * 4, "u", torch.float32)
+        _need(tokens, R * 4, "tokens", torch.int32)
+        _need(q, R * V * 4, "q", torch.float32)
+        par = np.zeros(R, dtype=np.int32)
+        nb = C.c_int32(0)
+        kv = KVCache(k.data_ptr(), v.data_ptr(), k.shape[2])
+        _check(lib.sb_draft_round(self.handle, C.byref(kv), kv_len, k_max, BRANCH_MODES[mode],
+                                  depth, temperature, u.data_ptr(), tokens.data_ptr(), q.data_ptr(),
+                                  par.ctypes.data_as(C.POINTER(C.c_int32)), C.byref(nb),
+                                  ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)),
+               "sb_draft_round")
+        B = int(nb.value)
+        return B, par[:1 + B * depth].copy()
 
     def sb_kv_rollback(self, k: torch.Tensor, v: torch.Tensor, kv_len: int,
                        result: torch.Tensor, new_len: torch.Tensor, stream=None) -> None:

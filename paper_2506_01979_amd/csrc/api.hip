@@ -644,22 +644,21 @@ sb_status sb_hrad_predict(const sb_model *m, const float *d_taps, int32_t k_laye
 
 size_t sb_branch_workspace_bytes(void) { return 256; }
 
-sb_status sb_branch_candidates(const float *d_q, int32_t vocab, int32_t x_b, int32_t k_max,
+sb_status sb_branch_candidates(const float *d_q, int32_t vocab, const int32_t *d_x_b, int32_t k_max,
                                int32_t mode, const float *d_u, int32_t *d_count,
                                int32_t *d_tokens, float *d_rows, void *d_ws, size_t ws_bytes,
                                hipStream_t stream) {
-  if (!d_q || !d_count || !d_tokens || !d_rows || !d_ws) return SB_ERR_INVALID_ARG;
+  if (!d_q || !d_x_b || !d_count || !d_tokens || !d_rows || !d_ws) return SB_ERR_INVALID_ARG;
   if (mode != SB_BRANCH_TOPK && mode != SB_BRANCH_IID && mode != SB_BRANCH_WOR)
     return SB_ERR_INVALID_ARG;
   if (mode != SB_BRANCH_TOPK && !d_u) return SB_ERR_INVALID_ARG;
-  if (vocab < 1 || vocab > SB_BRANCH_MAX_VOCAB || x_b < 0 || x_b >= vocab || k_max < 1 ||
-      k_max > SB_BRANCH_MAX_K)
+  if (vocab < 1 || vocab > SB_BRANCH_MAX_VOCAB || k_max < 1 || k_max > SB_BRANCH_MAX_K)
     return SB_ERR_INVALID_ARG;
   if (ws_bytes < sb_branch_workspace_bytes()) return SB_ERR_CAPACITY;
   BranchArgs a{};
   a.q = d_q;
   a.vocab = vocab;
-  a.x_b = x_b;
+  a.x_b = d_x_b;
   a.k_max = k_max;
   a.mode = mode;
   a.vec4 = vocab % 4 == 0 && ((uintptr_t)d_q & 15) == 0 && ((uintptr_t)d_rows & 15) == 0;
@@ -669,6 +668,120 @@ sb_status sb_branch_candidates(const float *d_q, int32_t vocab, int32_t x_b, int
   a.rows = d_rows;
   a.znorm = (double *)d_ws;
   return hip_status(launch_branch(a, stream));
+}
+
+sb_status sb_draft_sample(int32_t vocab, int32_t n, const float *d_logits,
+                          const sb_row_stats *d_stats, int32_t n_logit_rows,
+                          const int32_t *h_src_rows, float temperature, const float *d_u,
+                          int32_t *d_tokens, float *d_q, int32_t n_out_rows,
+                          const int32_t *h_dst_rows, hipStream_t stream) {
+  if (!d_logits || !d_stats || !h_src_rows || !d_u || !d_tokens || !d_q || !h_dst_rows)
+    return SB_ERR_INVALID_ARG;
+  if (vocab < 1 || n < 1 || n > SB_DRAFT_MAX_ROWS || !temperature_ok(temperature))
+    return SB_ERR_INVALID_ARG;
+  DraftRows rows{};
+  rows.n = n;
+  for (int i = 0; i < n; ++i) {
+    if (h_src_rows[i] < 0 || h_src_rows[i] >= n_logit_rows) return SB_ERR_INVALID_ARG;
+    if (h_dst_rows[i] < 0 || h_dst_rows[i] >= n_out_rows) return SB_ERR_INVALID_ARG;
+    for (int j = 0; j < i; ++j)
+      if (h_dst_rows[j] == h_dst_rows[i]) return SB_ERR_INVALID_ARG;
+    rows.src[i] = h_src_rows[i];
+    rows.dst[i] = h_dst_rows[i];
+  }
+  return hip_status(
+      launch_draft_sample(vocab, rows, d_logits, d_stats, temperature, d_u, d_tokens, d_q, stream));
+}
+
+// Workspace of a draft round: the forward's, the logits and statistics of
+// the largest tree, the candidates' workspace, x_b and B.
+struct RoundLayout {
+  size_t fwd, logits, stats, branch, ints, total;
+};
+static bool round_layout(const sb_model *m, int k_max, int depth, int kv_len, RoundLayout *o) {
+  if (!m || k_max < 1 || k_max > SB_BRANCH_MAX_K || depth < 1 || kv_len < 0) return false;
+  if (1 + (int64_t)k_max * depth > SB_MAX_ROWS) return false;
+  const int R = 1 + k_max * depth;
+  const size_t fw = sb_workspace_bytes(m, R, kv_len);
+  if (!fw) return false;
+  o->fwd = 0;
+  o->logits = align_up(fw);
+  o->stats = o->logits + align_up((size_t)R * m->cfg.vocab * 4);
+  o->branch = o->stats + align_up((size_t)R * sizeof(sb_row_stats));
+  o->ints = o->branch + align_up(sb_branch_workspace_bytes());
+  o->total = o->ints + align_up(2 * sizeof(int32_t));
+  return true;
+}
+
+size_t sb_draft_round_workspace_bytes(const sb_model *draft, int32_t k_max, int32_t depth,
+                                      int32_t kv_len) {
+  RoundLayout L;
+  return round_layout(draft, k_max, depth, kv_len, &L) ? L.total : 0;
+}
+
+sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t k_max,
+                         int32_t mode, int32_t depth, float temperature, const float *d_u,
+                         int32_t *d_tokens, float *d_q, int32_t *h_parents, int32_t *h_branches,
+                         void *d_ws, size_t ws_bytes, hipStream_t stream) {
+  if (!draft || !kv || !kv->k || !kv->v || !d_u || !d_tokens || !d_q || !h_parents ||
+      !h_branches || !d_ws)
+    return SB_ERR_INVALID_ARG;
+  if (mode != SB_BRANCH_TOPK && mode != SB_BRANCH_IID && mode != SB_BRANCH_WOR)
+    return SB_ERR_INVALID_ARG;
+  if (!temperature_ok(temperature) || draft->cfg.vocab > SB_BRANCH_MAX_VOCAB)
+    return SB_ERR_INVALID_ARG;
+  RoundLayout L;
+  if (!round_layout(draft, k_max, depth, kv_len, &L)) return SB_ERR_INVALID_ARG;
+  if (ws_bytes < L.total) return SB_ERR_CAPACITY;
+  const int R = 1 + k_max * depth;
+  if ((int64_t)kv_len + R > kv->capacity) return SB_ERR_CAPACITY;
+  const int V = draft->cfg.vocab;
+  char *ws = (char *)d_ws;
+  float *logits = (float *)(ws + L.logits);
+  sb_row_stats *stats = (sb_row_stats *)(ws + L.stats);
+  int32_t *xb = (int32_t *)(ws + L.ints);
+  int32_t *count = xb + 1;
+  const size_t fws = L.logits;
+
+  // 1. the root's row and x_b
+  int32_t par[SB_MAX_ROWS];
+  par[0] = -1;
+  sb_status st = sb_verify_forward(draft, kv, kv_len, d_tokens, par, 1, temperature, logits, stats,
+                                   ws, fws, stream);
+  if (st != SB_OK) return st;
+  const int32_t zero = 0;
+  st = sb_draft_sample(V, 1, logits, stats, 1, &zero, temperature, d_u, xb, d_q, 1, &zero, stream);
+  if (st != SB_OK) return st;
+  // 2. the branch-point candidates into rows 1 .. B
+  st = sb_branch_candidates(d_q, V, xb, k_max, mode, d_u + 1, count, d_tokens + 1, d_q + V,
+                            ws + L.branch, sb_branch_workspace_bytes(), stream);
+  if (st != SB_OK) return st;
+  int32_t B = 0;
+  if (hipMemcpyAsync(&B, count, sizeof(B), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
+    return SB_ERR_HIP;
+  if (B < 0 || B > k_max) return SB_ERR_HIP;
+  for (int i = 0; i < B; ++i) par[1 + i] = 0;
+  // 3. continuations, one depth per step
+  int32_t src[SB_BRANCH_MAX_K], dst[SB_BRANCH_MAX_K];
+  for (int d = 2; d <= depth && B > 0; ++d) {
+    const int n = 1 + (d - 1) * B;
+    st = sb_verify_forward(draft, kv, kv_len, d_tokens, par, n, temperature, logits, stats, ws, fws,
+                           stream);
+    if (st != SB_OK) return st;
+    for (int i = 0; i < B; ++i) {
+      src[i] = 1 + (d - 2) * B + i;
+      dst[i] = 1 + (d - 1) * B + i;
+      par[dst[i]] = src[i];
+    }
+    st = sb_draft_sample(V, B, logits, stats, n, src, temperature, d_u + 1 + k_max * (d - 1),
+                         d_tokens, d_q, R, dst, stream);
+    if (st != SB_OK) return st;
+  }
+  const int n_rows = 1 + B * depth;
+  for (int i = 0; i < n_rows; ++i) h_parents[i] = par[i];
+  *h_branches = B;
+  return SB_OK;
 }
 
 sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_len,

@@ -162,7 +162,8 @@ __global__ __launch_bounds__(kSelThreads) void k_branch_select(BranchArgs a) {
   // B = max(1, floor(k_max (1 - q(x_b)))), at most the tokens with mass and k_max
   int nnz = 0;
   for (int i = 0; i < kSelWaves; ++i) nnz += sh.cnt[i];
-  const float qxb = a.q[a.x_b];
+  const int xb = *a.x_b;
+  const float qxb = xb >= 0 && xb < a.vocab ? a.q[xb] : 0.0f;
   const double bf = floor((double)a.k_max * (1.0 - (double)qxb));
   int B = bf >= 1.0 ? (bf <= (double)a.k_max ? (int)bf : a.k_max) : 1;
   B = min(B, nnz);

@@ -860,6 +860,136 @@ __global__ __launch_bounds__(kWalkThreads) void k_select(int vocab, const float 
   }
 }
 
+// The draft's rows (the draft side of a round): q(v) = float32(p(v)) of a
+// logits row at T, written out as the row verification later reads as q,
+// and the token drawn from those float32 values: their float64 running sum
+// in vocabulary order, the first v whose sum exceeds u * W.  T = 0: q is
+// one-hot at the row's argmax, which is the token.  One workgroup per row;
+// each wave owns a contiguous segment of the vocabulary, as in draw_pass.
+__device__ __forceinline__ float draft_qv(const Dist &d, float raw) {
+  const float z = raw * d.inv_t;
+  const float e = expf(z - d.zmax);
+  return (float)((double)e / d.total);
+}
+
+__global__ __launch_bounds__(kWalkThreads) void k_draft_sample(int vocab, DraftRows rows,
+                                                               const float *__restrict__ logits,
+                                                               const sb_row_stats *__restrict__ stats,
+                                                               float inv_t, int greedy,
+                                                               const float *__restrict__ u,
+                                                               int32_t *__restrict__ tokens,
+                                                               float *__restrict__ q) {
+  __shared__ Shared sh;
+  const int i = blockIdx.x;
+  const int src = rows.src[i], dst = rows.dst[i];
+  const float *l = logits + (size_t)src * vocab;
+  const sb_row_stats st = stats[src];
+  float *qr = q + (size_t)dst * vocab;
+  if (greedy) {
+    for (int v = threadIdx.x; v < vocab; v += kWalkThreads) qr[v] = v == st.argmax ? 1.0f : 0.0f;
+    if (threadIdx.x == 0) tokens[dst] = st.argmax;
+    return;
+  }
+  const Dist d = row_dist(l, st, inv_t, 0);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int seg = ((vocab + kWaves - 1) / kWaves + 511) & ~511;
+  const int lo = w * seg;
+  const int hi = min(vocab, lo + seg);
+  const __amdgpu_buffer_rsrc_t rs = uniform_rsrc(l, vocab * 4);
+  // pass 1: write the row, sum it
+  double part = 0.0;
+  for (int v0 = lo + lane; v0 < hi; v0 += 64 * kBatch) {
+    float raw[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int v = v0 + 64 * j;
+      raw[j] = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(rs, v < hi ? v * 4 : vocab * 4, 0, 0));
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int v = v0 + 64 * j;
+      if (v < hi) {
+        const float f = draft_qv(d, raw[j]);
+        qr[v] = f;
+        part += (double)f;
+      }
+    }
+  }
+  part = wave_sum(part);
+  if (lane == 0) sh.red[w] = part;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double run = 0.0;
+    for (int k = 0; k < kWaves; ++k) {
+      const double t = sh.red[k];
+      sh.red[k] = run;
+      run += t;
+    }
+    sh.red[kWaves] = run;
+  }
+  __syncthreads();
+  // pass 2: the wave whose segment crosses u * W finds the token, lane l
+  // holding the 8 consecutive values 8l .. 8l + 7 of a block of 512
+  const double W = sh.red[kWaves];
+  const double thr = (double)u[i] * W;
+  const double seg_end = (w + 1 < kWaves) ? sh.red[w + 1] : W;
+  double run = sh.red[w];
+  int cand = INT_MAX;
+  if (lo < hi && seg_end > thr) {
+    for (int b0 = lo; b0 < hi && cand == INT_MAX; b0 += 512) {
+      const int e0 = b0 + 8 * lane;
+      float raw[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        raw[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                               rs, e0 + e < hi ? (e0 + e) * 4 : vocab * 4, 0, 0));
+      double x[8], ls = 0.0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        x[e] = e0 + e < hi ? (double)draft_qv(d, raw[e]) : 0.0;
+        ls += x[e];
+      }
+      double inc = ls;
+      for (int o = 1; o < 64; o <<= 1) {
+        const double y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+      }
+      const double lane_start = run + (inc - ls);
+      const unsigned long long hit = __ballot(e0 < hi && lane_start + ls > thr);
+      if (hit) {
+        const int first = __ffsll((long long)hit) - 1;
+        int found = INT_MAX;
+        if (lane == first) {
+          double c = lane_start;
+          for (int e = 0; e < 8; ++e) {
+            c += x[e];
+            if (e0 + e < hi && x[e] > 0.0 && c > thr) {
+              found = e0 + e;
+              break;
+            }
+          }
+          if (found == INT_MAX)  // rounding: the lane's last token with mass
+            for (int e = 0; e < 8; ++e)
+              if (e0 + e < hi && x[e] > 0.0) found = e0 + e;
+        }
+        cand = __shfl(found, first, 64);
+      }
+      run += __shfl(inc, 63, 64);
+    }
+  }
+  int y = block_min<kWaves>(cand, sh.ired);
+  if (y == INT_MAX) {
+    // rounding left no crossing: the last token with mass
+    int lp = -1;
+    for (int v = threadIdx.x; v < vocab; v += kWalkThreads)
+      if (draft_qv(d, l[v]) > 0.0f) lp = v;
+    y = block_max<kWaves>(lp, sh.ired);
+    if (y < 0) y = st.argmax;
+  }
+  if (threadIdx.x == 0) tokens[dst] = y;
+}
+
 }  // namespace
 
 size_t sample_ws_bytes(int vocab) { return (size_t)2 * (size_t)vocab * sizeof(double); }
@@ -898,6 +1028,17 @@ hipError_t launch_walk(int vocab, const TreeArg &tree, const int32_t *tokens, co
   temp_args(temperature, &inv_t, &greedy);
   hipLaunchKernelGGL(k_walk, dim3(1), dim3(kWalkThreads), 0, s, vocab, tree, tokens, logits, stats,
                      inv_t, greedy, q, u, result, (double *)ws);
+  return hipGetLastError();
+}
+
+hipError_t launch_draft_sample(int vocab, const DraftRows &rows, const float *logits,
+                               const sb_row_stats *stats, float temperature, const float *u,
+                               int32_t *tokens, float *q, hipStream_t s) {
+  float inv_t;
+  int greedy;
+  temp_args(temperature, &inv_t, &greedy);
+  hipLaunchKernelGGL(k_draft_sample, dim3(rows.n), dim3(kWalkThreads), 0, s, vocab, rows, logits,
+                     stats, inv_t, greedy, u, tokens, q);
   return hipGetLastError();
 }
 

@@ -24,6 +24,14 @@ hipError_t launch_select(int vocab, const float *logits_row, const sb_row_stats 
                          float temperature, int n_cand, const int32_t *cand_tokens,
                          const float *q, const float *u, int32_t *out, void *ws, hipStream_t s);
 size_t sample_ws_bytes(int vocab);
+// Rows of a draft sample call: logits/stats row src[i] -> token and q row dst[i].
+struct DraftRows {
+  int32_t n;
+  int32_t src[SB_DRAFT_MAX_ROWS], dst[SB_DRAFT_MAX_ROWS];
+};
+hipError_t launch_draft_sample(int vocab, const DraftRows &rows, const float *logits,
+                               const sb_row_stats *stats, float temperature, const float *u,
+                               int32_t *tokens, float *q, hipStream_t s);
 
 // ---- rollback (k_rollback.hip) ---------------------------------------------
 hipError_t launch_rollback(int n_layers, int n_kv, int capacity, int head_dim, int elem_bytes,

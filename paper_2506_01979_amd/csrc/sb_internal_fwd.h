@@ -165,7 +165,8 @@ hipError_t launch_hrad(const HradArgs &a, hipStream_t s);
 // then the carried rows
 struct BranchArgs {
   const float *q;  // [vocab]
-  int vocab, x_b, k_max, mode;
+  const int32_t *x_b;
+  int vocab, k_max, mode;
   int vec4;        // vocab % 4 == 0 and q, rows 16-byte aligned
   const float *u;  // [k_max]
   int32_t *count, *tokens;

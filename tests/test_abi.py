@@ -126,7 +126,7 @@ def test_branch_candidates_host_validation_without_device(api):
     lib = api.lib
     assert lib.sb_branch_workspace_bytes() >= 8 * api.SB_BRANCH_MAX_K
 
-    def call(q=1, vocab=1000, x_b=3, k_max=6, mode=2, u=1, count=1, toks=1, rows=1, ws=1,
+    def call(q=1, vocab=1000, x_b=1, k_max=6, mode=2, u=1, count=1, toks=1, rows=1, ws=1,
              ws_bytes=None):
         wb = lib.sb_branch_workspace_bytes() if ws_bytes is None else ws_bytes
         return lib.sb_branch_candidates(q, vocab, x_b, k_max, mode, u, count, toks, rows, ws, wb,
@@ -138,10 +138,56 @@ def test_branch_candidates_host_validation_without_device(api):
     assert call(mode=-1) == 1
     assert call(u=None) == 1                      # draws need uniforms ...
     assert call(mode=1, u=None) == 1
-    assert call(x_b=1000) == 1                    # x_b outside the vocabulary
-    assert call(x_b=-1) == 1
+    assert call(x_b=None) == 1
     assert call(k_max=0) == 1
     assert call(k_max=api.SB_BRANCH_MAX_K + 1) == 1
-    assert call(vocab=0, x_b=0) == 1
+    assert call(vocab=0) == 1
     assert call(vocab=api.SB_BRANCH_MAX_VOCAB + 1) == 1
     assert call(ws_bytes=8) == 3
+
+
+def test_draft_host_validation_without_device(api):
+    """The draft sampler and the draft round reject bad arguments before any
+    launch; the round's workspace size is host arithmetic."""
+    lib = api.lib
+    I = lambda *a: (C.c_int32 * len(a))(*a)
+
+    def samp(n=2, src=(0, 1), dst=(0, 1), nl=2, no=2, T=1.0, logits=1, u=1):
+        return lib.sb_draft_sample(100, n, logits, 1, nl, I(*src), T, u, 1, 1, no, I(*dst), None)
+    assert samp(logits=None) == 1
+    assert samp(u=None) == 1
+    assert samp(n=0) == 1
+    assert samp(n=api.SB_DRAFT_MAX_ROWS + 1, src=(0,) * 65, dst=tuple(range(65)), no=65) == 1
+    assert samp(src=(0, 2)) == 1                       # source row past the logits
+    assert samp(dst=(0, 2)) == 1                       # destination past the outputs
+    assert samp(dst=(1, 1)) == 1                       # two rows into one destination
+    assert samp(T=-1.0) == 1
+    assert samp(T=float("nan")) == 1
+    w = api.ModelWeights(1, 1, 1, (api.LayerWeights * 2)(*[api.LayerWeights(1, 1, 1, 1, 1, 1)] * 2))
+    h = C.c_void_p()
+    assert lib.sb_model_create(C.byref(cfg(api, n_layers=2, dtype=api.SB_BF16)), C.byref(w), C.byref(h)) == 0
+    try:
+        assert lib.sb_draft_round_workspace_bytes(None, 6, 4, 100) == 0
+        assert lib.sb_draft_round_workspace_bytes(h, 0, 4, 100) == 0
+        assert lib.sb_draft_round_workspace_bytes(h, 17, 4, 100) == 0
+        assert lib.sb_draft_round_workspace_bytes(h, 16, 16, 100) == 0   # 257 rows
+        wb = lib.sb_draft_round_workspace_bytes(h, 6, 4, 100)
+        assert wb > 0
+        kv = api.KVCache(1, 1, 128)
+        par = (C.c_int32 * 25)()
+        nb = C.c_int32(0)
+
+        def rnd(m=h, mode=2, k_max=6, depth=4, cap=128, ws=wb, T=1.0, u=1):
+            kv.capacity = cap
+            return lib.sb_draft_round(m, C.byref(kv), 100, k_max, mode, depth, T, u, 1, 1, par,
+                                      C.byref(nb), 1, ws, None)
+        assert rnd(m=None) == 1
+        assert rnd(u=None) == 1
+        assert rnd(mode=5) == 1
+        assert rnd(k_max=0) == 1
+        assert rnd(depth=0) == 1
+        assert rnd(T=-0.5) == 1
+        assert rnd(ws=wb - 1) == 3
+        assert rnd(cap=120) == 3                        # 100 + 25 slots needed
+    finally:
+        lib.sb_model_destroy(h)

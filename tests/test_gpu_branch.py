@@ -76,7 +76,8 @@ def run(api, q, x_b, k_max, mode, u, offset=0):
     toks = torch.full((k_max,), -7, dtype=torch.int32, device=dev)
     rows = torch.full((k_max, V), 7.0, dtype=torch.float32, device=dev)
     ws = torch.empty(api.sb_branch_workspace_bytes(), dtype=torch.uint8, device=dev)
-    api.sb_branch_candidates(qd, x_b, k_max, mode, ud, count, toks, rows, ws)
+    xb = torch.tensor([x_b], dtype=torch.int32, device=dev)
+    api.sb_branch_candidates(qd, xb, k_max, mode, ud, count, toks, rows, ws)
     torch.cuda.synchronize()
     return int(count.item()), toks.cpu().numpy(), rows.cpu().numpy()
 
@@ -143,3 +144,9 @@ def test_branch_count_follows_q_of_x_b(api):
         say(f"branch count q(x_b)={qx}")
         B, _, _ = run(api, q, 9, 6, "topk", None)
         assert B == branching.branch_count(q[9], 6, int(np.count_nonzero(q > 0)))
+    # a token outside the vocabulary counts as q(x_b) = 0: B = k_max
+    q = np.full(V, 1.0 / V, dtype=np.float32)
+    for xb in (-1, V):
+        say(f"branch count x_b={xb}")
+        B, _, _ = run(api, q, xb, 6, "topk", None)
+        assert B == 6

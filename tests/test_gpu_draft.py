@@ -1,0 +1,220 @@
+"""GPU parity of the draft side of a round (Section "Branch Resampling")
+against the oracle, through the C ABI.
+
+sb_draft_sample: on the same synthetic logits, each q row within 5e-7
+relative of the oracle's (both take float32 exp of the same float32 z and
+divide by a float64 total; the two exp implementations and summation
+orders differ by a few float32 ulps), T = 0 rows exactly one-hot, and each
+token bit-exact unless its uniform lies within 1e-6 (relative to the total)
+of a boundary of the oracle's running sum.
+
+sb_draft_round on float32 draft models (float32 GEMMs over K <= 688 put
+the logits about 1e-6 from the float64 oracle's): the branch count, the
+tree and the tokens bit-exact, the q rows within 2e-5 relative, up to the
+first decision the oracle takes within 2e-5 of its threshold (a draw's
+uniform against a running sum, B's floor(k_max (1 - q(x_b))) against an
+integer, a greedy argmax against the runner-up), where the comparison
+stops; the seeds are ones whose rounds have few such ties.  The 68M draft shape in bfloat16
+(2 layers, hidden 768, 12 heads of 64, FFN 3072, vocabulary 32000) is
+checked by the properties every round has, since its logits carry the
+bfloat16 bound.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import say
+from oracle import branching, decoder, drafting
+from paper_2506_01979_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+_W = {}
+_M = {}
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2506_01979_amd import api as A
+    assert torch.cuda.is_available()
+    return A
+
+
+def weights(shape):
+    if shape.name not in _W:
+        _W[shape.name] = synth.model_weights(shape)
+    return _W[shape.name]
+
+
+def model(api, shape):
+    if shape.name not in _M:
+        _M[shape.name] = api.Model(shape, api.dict_tensors(weights(shape)))
+    return _M[shape.name]
+
+
+def cum_margin(q_row, u):
+    C = np.cumsum(np.asarray(q_row, dtype=np.float64))
+    W = C[-1]
+    return float(np.min(np.abs(C - np.float64(u) * W))) / W if W > 0 else np.inf
+
+
+@pytest.mark.parametrize("V,T,n", [(32000, 0.7, 6), (32000, 1.0, 16), (1003, 1.3, 5), (16, 0.9, 9),
+                                   (32000, 0.0, 4), (128256, 0.8, 3)])
+def test_draft_sample_matches_oracle(api, V, T, n):
+    seed = V % 97 + n
+    logits = synth.random_logits(n + 2, V, scale=3.0, seed=seed)
+    g = np.random.default_rng(seed)
+    src = g.permutation(n + 2)[:n].astype(np.int32)
+    n_out = n + 3
+    dst = g.permutation(n_out)[:n].astype(np.int32)
+    u = synth.uniforms(n, seed=seed)
+    dev = "cuda"
+    ld = torch.from_numpy(logits).to(dev)
+    stats = api.new_stats(n + 2)
+    api.sb_softmax_stats(ld, T, stats)
+    toks = torch.full((n_out,), -5, dtype=torch.int32, device=dev)
+    q = torch.full((n_out, V), 7.0, dtype=torch.float32, device=dev)
+    say(f"draft sample V={V} T={T} n={n}")
+    api.sb_draft_sample(ld, stats, src, T, torch.from_numpy(u).to(dev), toks, q, dst)
+    torch.cuda.synchronize()
+    toks, q = toks.cpu().numpy(), q.cpu().numpy()
+    for i in range(n):
+        qo, to = drafting.sample(logits[src[i]], T, u[i])
+        if T > 0:
+            np.testing.assert_allclose(q[dst[i]], qo, rtol=5e-7, atol=0)
+        else:
+            assert np.array_equal(q[dst[i]], qo)
+        if T == 0 or cum_margin(qo, u[i]) >= 1e-6:
+            assert toks[dst[i]] == to, (i, toks[dst[i]], to)
+    rest = np.setdiff1d(np.arange(n_out), dst)
+    assert np.all(toks[rest] == -5) and np.all(q[rest] == 7.0)
+
+
+def gpu_round(api, shape, K, V, P, root, k_max, mode, depth, T, u):
+    m = model(api, shape)
+    R = 1 + k_max * depth
+    k, v = m.new_kv(P + R)
+    if P:
+        m.load_kv(k, v, K, V, P)
+    toks = torch.full((R,), -5, dtype=torch.int32, device="cuda")
+    toks[0] = int(root)
+    q = torch.full((R, shape.vocab), 7.0, dtype=torch.float32, device="cuda")
+    ws = m.draft_round_workspace(k_max, depth, P)
+    B, par = m.sb_draft_round(k, v, P, k_max, mode, depth, T, torch.from_numpy(u).cuda(), toks, q,
+                              ws)
+    torch.cuda.synchronize()
+    return B, par, toks.cpu().numpy(), q.cpu().numpy()
+
+
+def first_tie(shape, W, K, V, P, ref, k_max, mode, depth, T, u, thr=2e-5):
+    """Row order index of the first oracle decision within thr of its
+    threshold (len(tokens) if none; 0 if the branch point itself is one)."""
+    lg, _, _ = decoder.tree_forward(shape, W, K, V, P, ref.tokens, ref.parents, "f64")
+    B = ref.branches
+    if T == 0:
+        for r in range(len(ref.tokens)):
+            s = np.sort(lg[r].astype(np.float64))
+            if s[-1] - s[-2] < thr * max(1.0, abs(s[-1])):
+                return 0 if r == 0 else r + B
+        return len(ref.tokens)
+    if cum_margin(ref.q[0], u[0]) < thr:
+        return 0
+    x = k_max * (1.0 - float(ref.q[0][ref.x_b]))
+    if abs(x - round(x)) < thr * k_max:
+        return 0
+    if mode != "topk":
+        rem = ref.q[0].astype(np.float64).copy()
+        for i in range(B):
+            if cum_margin(rem, u[1 + i]) < thr:
+                return 1 + i
+            if mode == "wor":
+                rem[ref.tokens[1 + i]] = 0.0
+    elif B > 1:
+        s = np.sort(ref.q[0])[::-1]
+        if np.min(np.abs(np.diff(s[:B + 1]))) < thr * s[0]:
+            return 1
+    for d in range(2, depth + 1):
+        for i in range(B):
+            r = 1 + (d - 1) * B + i
+            if cum_margin(ref.q[r], u[1 + k_max * (d - 1) + i]) < thr:
+                return r
+    return len(ref.tokens)
+
+
+ROUND_CASES = [
+    # shape, prefix, k_max, depth, T, seed
+    ("exact", 8, 6, 4, 0.9, 1),
+    ("exact", 8, 16, 3, 1.0, 2),
+    ("tiny", 96, 6, 4, 0.8, 7),
+    ("tiny", 40, 4, 8, 1.2, 7),
+    ("tiny", 96, 6, 4, 0.8, 5),
+    ("exact", 8, 6, 5, 0.0, 5),
+]
+
+
+@pytest.mark.parametrize("mode", branching.MODES)
+@pytest.mark.parametrize("name,P,k_max,depth,T,seed", ROUND_CASES)
+def test_draft_round_matches_oracle(api, mode, name, P, k_max, depth, T, seed):
+    shape = synth.SHAPES[name]
+    W = weights(shape)
+    ptoks = synth.prefix_tokens(shape.vocab, P + 1, seed=seed)
+    _, K, V = decoder.prefill(shape, W, ptoks[:-1], "f64")
+    u = synth.uniforms(drafting.uniforms_needed(k_max, depth), seed=seed)
+    ref = drafting.draft_round(shape, W, K, V, P, int(ptoks[-1]), k_max, mode, depth, T, u)
+    say(f"draft round {name} P={P} k_max={k_max} depth={depth} T={T} {mode}")
+    B, par, toks, q = gpu_round(api, shape, K, V, P, ptoks[-1], k_max, mode, depth, T, u)
+    stop = first_tie(shape, W, K, V, P, ref, k_max, mode, depth, T, u)
+    if stop == 0:
+        return                              # the branch point itself is a rounding tie
+    assert B == ref.branches
+    assert par.tolist() == ref.parents.tolist()
+    n = min(stop, len(ref.tokens))
+    assert toks[:n].tolist() == ref.tokens[:n].tolist()
+    np.testing.assert_allclose(q[:n], ref.q[:n], rtol=2e-5, atol=1e-12)
+    if n == len(ref.tokens):
+        assert np.all(q[n:] == 7.0)
+
+
+def test_draft_round_properties_68m_bf16(api):
+    shape = synth.SHAPES["draft68m"]
+    P, k_max, depth, T = 256, 6, 5, 1.0
+    m = api.Model(shape, api.synth_tensors(shape, seed=7))
+    R = 1 + k_max * depth
+    k, v = m.new_kv(P + R)
+    Kp = np.stack([synth.synthetic_kv(shape, li, P, P, 0, as_bits=True)
+                   for li in range(shape.n_layers)])
+    Vp = np.stack([synth.synthetic_kv(shape, li, P, P, 1, as_bits=True)
+                   for li in range(shape.n_layers)])
+    m.load_kv(k, v, Kp, Vp, P)
+    for mode in branching.MODES:
+        u = synth.uniforms(R, seed=11)
+        toks = torch.full((R,), -5, dtype=torch.int32, device="cuda")
+        toks[0] = 17
+        q = torch.full((R, shape.vocab), 7.0, dtype=torch.float32, device="cuda")
+        ws = m.draft_round_workspace(k_max, depth, P)
+        say(f"draft round 68m bf16 {mode}")
+        B, par = m.sb_draft_round(k, v, P, k_max, mode, depth, T, torch.from_numpy(u).cuda(), toks,
+                                  q, ws)
+        torch.cuda.synchronize()
+        tk, qq = toks.cpu().numpy(), q.cpu().numpy().astype(np.float64)
+        assert 1 <= B <= k_max
+        assert par.tolist() == [-1] + [0] * B + [1 + (d - 2) * B + i for d in range(2, depth + 1)
+                                                for i in range(B)]
+        n = 1 + B * depth
+        assert np.all((tk[1:n] >= 0) & (tk[1:n] < shape.vocab))
+        assert np.all(np.abs(qq[:n].sum(axis=1) - 1.0) < 1e-5)
+        assert np.all(qq[np.arange(1, n), tk[1:n]] > 0)
+        first = tk[1:1 + B]
+        assert len(set(first.tolist())) == B or mode == "iid"
+        if mode == "topk":
+            assert np.array_equal(qq[1:1 + B], np.eye(shape.vocab)[first])
+            assert np.min(qq[0][first]) >= np.sort(qq[0])[-B]
+        elif mode == "iid":
+            assert np.all(qq[1:1 + B] == qq[0])
+        else:
+            for i in range(B):
+                live = np.ones(shape.vocab, bool)
+                live[first[:i]] = False
+                assert np.all(qq[1 + i][~live] == 0)
+                ratio = qq[1 + i][live] / qq[0][live]
+                assert np.allclose(ratio, ratio[0], rtol=1e-6)
