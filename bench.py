@@ -601,7 +601,7 @@ def main():
     # depth k (a near-flat q at the branch point gives the verify step's B),
     # then the branch-point candidates and the draft sampler on their own.
     # Not part of `value`.
-    draft_out = None
+    draft_out = overlap_out = None
     if not args.no_draft:
         dshape = synth.SHAPES["draft68m"]
         dm = api.Model(dshape, api.synth_tensors(dshape, seed=1), device=dev)
@@ -634,29 +634,84 @@ def main():
         crows = torch.empty((16, V), dtype=torch.float32, device=dev)
         cws = torch.empty(api.sb_branch_workspace_bytes(), dtype=torch.uint8, device=dev)
         cu = torch.from_numpy(synth.uniforms(16, 32)).to(dev)
-        cand_us = {}
-        for mode in ("topk", "iid", "wor"):
-            for _ in range(3):
-                api.sb_branch_candidates(cq, cxb, 6, mode, cu, ccount, ctok, crows, cws, stream)
+        # device time per call: 50 calls captured in a HIP graph and replayed
+        # (the Python binding's own cost per call is larger than the kernels')
+        def graph_us(call, reps=50, replays=10):
+            gs = torch.cuda.Stream()
+            gs.wait_stream(stream)
+            with torch.cuda.stream(gs):
+                call(gs)
+            gs.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=gs):
+                for _ in range(reps):
+                    call(gs)
+            g.replay()
             torch.cuda.synchronize()
             ev0.record(stream)
-            for _ in range(200):
-                api.sb_branch_candidates(cq, cxb, 6, mode, cu, ccount, ctok, crows, cws, stream)
+            for _ in range(replays):
+                g.replay()
             ev1.record(stream)
             torch.cuda.synchronize()
-            cand_us[mode] = round(ev0.elapsed_time(ev1) * 1e3 / 200, 2)
+            return round(ev0.elapsed_time(ev1) * 1e3 / (reps * replays), 2)
+        cand_us = {}
+        for mode in ("topk", "iid", "wor"):
+            cand_us[mode] = graph_us(lambda st, mode=mode: api.sb_branch_candidates(
+                cq, cxb, 6, mode, cu, ccount, ctok, crows, cws, st))
         cand_b = int(ccount.item())
         src = list(range(1, 1 + B))
         dst = list(range(1, 1 + B))
-        for _ in range(3):
-            api.sb_draft_sample(logits, stats, src, 1.0, du, dtok, dq, dst, stream)
-        torch.cuda.synchronize()
-        ev0.record(stream)
-        for _ in range(200):
-            api.sb_draft_sample(logits, stats, src, 1.0, du, dtok, dq, dst, stream)
-        ev1.record(stream)
-        torch.cuda.synchronize()
-        samp_us = ev0.elapsed_time(ev1) * 1e3 / 200
+        dsws = torch.empty(api.sb_draft_sample_workspace_bytes(V, B), dtype=torch.uint8, device=dev)
+        samp_us = graph_us(lambda st: api.sb_draft_sample(logits, stats, src, 1.0, du, dtok, dq, dst,
+                                                          dsws, st))
+        # Algorithm 2's overlap on one GPU: the target's verify step on one
+        # stream while the draft builds the next round's branches on another
+        # (default priorities), then Algorithm 1 over the branches' first
+        # tokens at the verified tree's first leaf row.  Serial first, then
+        # overlapped; the results must not change.
+        sv, sd = torch.cuda.Stream(), torch.cuda.Stream()
+        sel_out = torch.empty(3, dtype=torch.int32, device=dev)
+        su = torch.from_numpy(synth.uniforms(DK + 1, 41)).to(dev)
+        leaf = n - 1
+
+        def select(st):
+            api.sb_select_branch(logits[leaf], stats[leaf], 1.0, dtok[1:1 + bd], dq[1:1 + bd], su,
+                                 sel_out, sws_sel, st)
+        sws_sel = torch.empty(api.sb_sample_workspace_bytes(V), dtype=torch.uint8, device=dev)
+
+        def serial():
+            step(stream)
+            draft_round()
+            select(stream)
+
+        def overlapped():
+            sv.wait_stream(stream)
+            sd.wait_stream(stream)
+            step(sv)
+            dm.sb_draft_round(dk_, dv_, kv_len, DK, "wor", DD, 1.0, du, dtok, dq, dws, sd)
+            stream.wait_stream(sv)
+            stream.wait_stream(sd)
+            select(stream)
+        times = {}
+        outs = {}
+        for name, fn in (("serial", serial), ("overlapped", overlapped)):
+            for _ in range(2):
+                fn()
+            torch.cuda.synchronize()
+            ev0.record(stream)
+            for _ in range(reps):
+                fn()
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            times[name] = ev0.elapsed_time(ev1) / reps
+            outs[name] = (api.decode_result(res), sel_out.cpu().tolist(), dtok.cpu().tolist())
+        if outs["serial"] != outs["overlapped"]:
+            raise RuntimeError("the overlapped round changed a result")
+        overlap_out = {"verify_ms": round(ms_per_step, 4), "draft_round_ms": round(round_ms, 4),
+                       "serial_ms": round(times["serial"], 4),
+                       "overlapped_ms": round(times["overlapped"], 4),
+                       "hidden_frac_of_draft": round((times["serial"] - times["overlapped"])
+                                                     / round_ms, 3)}
         draft_out = {"shape": f"{dshape.name}: {dshape.n_layers} layers, hidden {dshape.hidden}, "
                               f"{dshape.n_heads}x{dshape.head_dim} heads, ffn {dshape.ffn}, "
                               f"vocab {V}, bf16",
@@ -665,7 +720,7 @@ def main():
                      "round_plus_verify_ms": round(round_ms + ms_per_step, 4),
                      "candidates_us_k6": cand_us, "candidates_B": cand_b,
                      "candidates_bytes_k6_wor": 4 * V * (1 + cand_b),
-                     "sample_us": round(samp_us, 2), "sample_rows": B,
+                     "sample_us": samp_us, "sample_rows": B,
                      "sample_bytes": 2 * 4 * V * B}
         del dm, dk_, dv_, dq, crows
 
@@ -715,6 +770,7 @@ def main():
         out["hrad"] = hrad_out
     if draft_out is not None:
         out["draft"] = draft_out
+        out["overlap"] = overlap_out
 
     if not args.no_alpha_sweep:
         sweep = {}

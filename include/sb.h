@@ -332,14 +332,21 @@ sb_status sb_branch_candidates(const float *d_q, int32_t vocab, const int32_t *d
  * argmax, which is the token.  d_logits: float32 [n_logit_rows][vocab] with
  * d_stats their sb_row_stats at the same T (as sb_verify_forward and
  * sb_softmax_stats write them; finite logits); d_tokens: int32
- * [n_out_rows]; d_q: float32 [n_out_rows][vocab].  1 <= n <=
- * SB_DRAFT_MAX_ROWS, 0 <= h_src_rows[i] < n_logit_rows, 0 <= h_dst_rows[i]
- * < n_out_rows and distinct, T >= 0, else SB_ERR_INVALID_ARG. */
+ * [n_out_rows]; d_q: float32 [n_out_rows][vocab]; d_ws of at least
+ * sb_draft_sample_workspace_bytes(vocab, n) bytes (SB_ERR_CAPACITY).
+ * 1 <= n <= SB_DRAFT_MAX_ROWS, 0 <= h_src_rows[i] < n_logit_rows,
+ * 0 <= h_dst_rows[i] < n_out_rows and distinct, T >= 0, else
+ * SB_ERR_INVALID_ARG.  The draw sums in blocks of 2048 tokens, so a u within
+ * rounding of a boundary of the running sum may pick the neighbouring token. */
 sb_status sb_draft_sample(int32_t vocab, int32_t n, const float *d_logits,
                           const sb_row_stats *d_stats, int32_t n_logit_rows,
                           const int32_t *h_src_rows, float temperature, const float *d_u,
                           int32_t *d_tokens, float *d_q, int32_t n_out_rows,
-                          const int32_t *h_dst_rows, hipStream_t stream);
+                          const int32_t *h_dst_rows, void *d_ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+/* Workspace bytes of sb_draft_sample (per-block sums of each row). */
+size_t sb_draft_sample_workspace_bytes(int32_t vocab, int32_t n);
 
 /* Workspace bytes of sb_draft_round (0 for arguments it rejects). */
 size_t sb_draft_round_workspace_bytes(const sb_model *draft, int32_t k_max, int32_t depth,

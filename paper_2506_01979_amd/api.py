@@ -32,6 +32,7 @@ EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight"
            "sb_accept_resample", "sb_kv_rollback", "sb_timer_start", "sb_timer_stop",
            "sb_model_set_tap", "sb_hrad_workspace_bytes", "sb_hrad_predict",
            "sb_branch_workspace_bytes", "sb_branch_candidates", "sb_draft_sample",
+           "sb_draft_sample_workspace_bytes",
            "sb_draft_round_workspace_bytes", "sb_draft_round")
 
 SB_HRAD_H1, SB_HRAD_H2, SB_HRAD_CLASSES = 256, 64, 3
@@ -122,7 +123,9 @@ lib.sb_branch_candidates.argtypes = [_vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, 
                                      _vp]
 lib.sb_draft_sample.restype = _i32
 lib.sb_draft_sample.argtypes = [_i32, _i32, _vp, _vp, _i32, C.POINTER(_i32), _f, _vp, _vp, _vp,
-                                _i32, C.POINTER(_i32), _vp]
+                                _i32, C.POINTER(_i32), _vp, _sz, _vp]
+lib.sb_draft_sample_workspace_bytes.restype = _sz
+lib.sb_draft_sample_workspace_bytes.argtypes = [_i32, _i32]
 lib.sb_draft_round_workspace_bytes.restype = _sz
 lib.sb_draft_round_workspace_bytes.argtypes = [_vp, _i32, _i32, _i32]
 lib.sb_draft_round.restype = _i32
@@ -258,9 +261,13 @@ def sb_branch_candidates(q: torch.Tensor, x_b: torch.Tensor, k_max: int, mode: s
                                     _stream(stream)), "sb_branch_candidates")
 
 
+def sb_draft_sample_workspace_bytes(vocab: int, n: int) -> int:
+    return int(lib.sb_draft_sample_workspace_bytes(vocab, n))
+
+
 def sb_draft_sample(logits: torch.Tensor, stats: torch.Tensor, src_rows, temperature: float,
                     u: torch.Tensor, tokens: torch.Tensor, q: torch.Tensor, dst_rows,
-                    stream=None) -> None:
+                    ws: torch.Tensor, stream=None) -> None:
     """logits float32 [n_logit_rows][vocab] with stats; tokens int32 [n_out];
     q float32 [n_out][vocab]; u float32 [len(src_rows)]."""
     nl, v = logits.shape
@@ -274,9 +281,11 @@ def sb_draft_sample(logits: torch.Tensor, stats: torch.Tensor, src_rows, tempera
     _need(u, len(src) * 4, "u", torch.float32)
     _need(tokens, n_out * 4, "tokens", torch.int32)
     _need(q, n_out * v * 4, "q", torch.float32)
+    _need(ws, sb_draft_sample_workspace_bytes(v, len(src)), "ws")
     _check(lib.sb_draft_sample(v, len(src), logits.data_ptr(), stats.data_ptr(), nl, sp,
                                temperature, u.data_ptr(), tokens.data_ptr(), q.data_ptr(), n_out,
-                               dp, _stream(stream)), "sb_draft_sample")
+                               dp, ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)),
+           "sb_draft_sample")
 
 
 def sb_sample_workspace_bytes(vocab: int) -> int:

@@ -674,11 +674,13 @@ sb_status sb_draft_sample(int32_t vocab, int32_t n, const float *d_logits,
                           const sb_row_stats *d_stats, int32_t n_logit_rows,
                           const int32_t *h_src_rows, float temperature, const float *d_u,
                           int32_t *d_tokens, float *d_q, int32_t n_out_rows,
-                          const int32_t *h_dst_rows, hipStream_t stream) {
-  if (!d_logits || !d_stats || !h_src_rows || !d_u || !d_tokens || !d_q || !h_dst_rows)
+                          const int32_t *h_dst_rows, void *d_ws, size_t ws_bytes,
+                          hipStream_t stream) {
+  if (!d_logits || !d_stats || !h_src_rows || !d_u || !d_tokens || !d_q || !h_dst_rows || !d_ws)
     return SB_ERR_INVALID_ARG;
   if (vocab < 1 || n < 1 || n > SB_DRAFT_MAX_ROWS || !temperature_ok(temperature))
     return SB_ERR_INVALID_ARG;
+  if (ws_bytes < draft_ws_bytes(vocab, n)) return SB_ERR_CAPACITY;
   DraftRows rows{};
   rows.n = n;
   for (int i = 0; i < n; ++i) {
@@ -689,14 +691,19 @@ sb_status sb_draft_sample(int32_t vocab, int32_t n, const float *d_logits,
     rows.src[i] = h_src_rows[i];
     rows.dst[i] = h_dst_rows[i];
   }
-  return hip_status(
-      launch_draft_sample(vocab, rows, d_logits, d_stats, temperature, d_u, d_tokens, d_q, stream));
+  return hip_status(launch_draft_sample(vocab, rows, d_logits, d_stats, temperature, d_u, d_tokens,
+                                       d_q, d_ws, stream));
+}
+
+size_t sb_draft_sample_workspace_bytes(int32_t vocab, int32_t n) {
+  if (vocab < 1 || n < 1 || n > SB_DRAFT_MAX_ROWS) return 0;
+  return draft_ws_bytes(vocab, n);
 }
 
 // Workspace of a draft round: the forward's, the logits and statistics of
 // the largest tree, the candidates' workspace, x_b and B.
 struct RoundLayout {
-  size_t fwd, logits, stats, branch, ints, total;
+  size_t fwd, logits, stats, branch, sample, ints, total;
 };
 static bool round_layout(const sb_model *m, int k_max, int depth, int kv_len, RoundLayout *o) {
   if (!m || k_max < 1 || k_max > SB_BRANCH_MAX_K || depth < 1 || kv_len < 0) return false;
@@ -708,7 +715,8 @@ static bool round_layout(const sb_model *m, int k_max, int depth, int kv_len, Ro
   o->logits = align_up(fw);
   o->stats = o->logits + align_up((size_t)R * m->cfg.vocab * 4);
   o->branch = o->stats + align_up((size_t)R * sizeof(sb_row_stats));
-  o->ints = o->branch + align_up(sb_branch_workspace_bytes());
+  o->sample = o->branch + align_up(sb_branch_workspace_bytes());
+  o->ints = o->sample + align_up(draft_ws_bytes(m->cfg.vocab, k_max));
   o->total = o->ints + align_up(2 * sizeof(int32_t));
   return true;
 }
@@ -750,7 +758,10 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
                                    ws, fws, stream);
   if (st != SB_OK) return st;
   const int32_t zero = 0;
-  st = sb_draft_sample(V, 1, logits, stats, 1, &zero, temperature, d_u, xb, d_q, 1, &zero, stream);
+  void *sws = ws + L.sample;
+  const size_t swb = draft_ws_bytes(V, k_max);
+  st = sb_draft_sample(V, 1, logits, stats, 1, &zero, temperature, d_u, xb, d_q, 1, &zero, sws, swb,
+                       stream);
   if (st != SB_OK) return st;
   // 2. the branch-point candidates into rows 1 .. B
   st = sb_branch_candidates(d_q, V, xb, k_max, mode, d_u + 1, count, d_tokens + 1, d_q + V,
@@ -775,7 +786,7 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
       par[dst[i]] = src[i];
     }
     st = sb_draft_sample(V, B, logits, stats, n, src, temperature, d_u + 1 + k_max * (d - 1),
-                         d_tokens, d_q, R, dst, stream);
+                         d_tokens, d_q, R, dst, sws, swb, stream);
     if (st != SB_OK) return st;
   }
   const int n_rows = 1 + B * depth;

@@ -864,130 +864,197 @@ __global__ __launch_bounds__(kWalkThreads) void k_select(int vocab, const float 
 // logits row at T, written out as the row verification later reads as q,
 // and the token drawn from those float32 values: their float64 running sum
 // in vocabulary order, the first v whose sum exceeds u * W.  T = 0: q is
-// one-hot at the row's argmax, which is the token.  One workgroup per row;
-// each wave owns a contiguous segment of the vocabulary, as in draw_pass.
-__device__ __forceinline__ float draft_qv(const Dist &d, float raw) {
-  const float z = raw * d.inv_t;
-  const float e = expf(z - d.zmax);
-  return (float)((double)e / d.total);
+// one-hot at the row's argmax, which is the token.
+//   k_draft_q:    grid (blocks of kDraftSpan tokens, rows); writes q and the
+//                 float64 sum of each block's q to the workspace;
+//   k_draft_draw: one workgroup per row; the crossing block from the block
+//                 sums, then the token from that block's q.
+constexpr int kDraftThreads = 256;
+constexpr int kDraftSpan = kDraftThreads * 8;
+
+__device__ __forceinline__ float draft_qv(float raw, float inv_t, float zmax, double total) {
+  const float z = raw * inv_t;
+  const float e = expf(z - zmax);
+  return (float)((double)e / total);
 }
 
-__global__ __launch_bounds__(kWalkThreads) void k_draft_sample(int vocab, DraftRows rows,
-                                                               const float *__restrict__ logits,
-                                                               const sb_row_stats *__restrict__ stats,
-                                                               float inv_t, int greedy,
-                                                               const float *__restrict__ u,
-                                                               int32_t *__restrict__ tokens,
-                                                               float *__restrict__ q) {
-  __shared__ Shared sh;
-  const int i = blockIdx.x;
+__global__ __launch_bounds__(kDraftThreads) void k_draft_q(int vocab, int vec8, DraftRows rows,
+                                                           const float *__restrict__ logits,
+                                                           const sb_row_stats *__restrict__ stats,
+                                                           float inv_t, int greedy,
+                                                           float *__restrict__ q,
+                                                           double *__restrict__ bsum) {
+  __shared__ double red[kDraftThreads / 64];
+  const int i = blockIdx.y, blk = blockIdx.x, nblk = gridDim.x;
   const int src = rows.src[i], dst = rows.dst[i];
   const float *l = logits + (size_t)src * vocab;
   const sb_row_stats st = stats[src];
   float *qr = q + (size_t)dst * vocab;
-  if (greedy) {
-    for (int v = threadIdx.x; v < vocab; v += kWalkThreads) qr[v] = v == st.argmax ? 1.0f : 0.0f;
-    if (threadIdx.x == 0) tokens[dst] = st.argmax;
-    return;
+  // thread t: the 8 consecutive tokens v0 .. v0 + 7 of the block (whole
+  // 16-byte pairs when vocab % 8 == 0 and the rows are 16-byte aligned)
+  const int v0 = blk * kDraftSpan + (int)threadIdx.x * 8;
+  float raw[8];
+  if (vec8 && v0 < vocab) {
+    const f32x4 a = *(const f32x4 *)(l + v0), b = *(const f32x4 *)(l + v0 + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      raw[e] = a[e];
+      raw[4 + e] = b[e];
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) raw[e] = v0 + e < vocab ? l[v0 + e] : 0.0f;
   }
-  const Dist d = row_dist(l, st, inv_t, 0);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int seg = ((vocab + kWaves - 1) / kWaves + 511) & ~511;
-  const int lo = w * seg;
-  const int hi = min(vocab, lo + seg);
-  const __amdgpu_buffer_rsrc_t rs = uniform_rsrc(l, vocab * 4);
-  // pass 1: write the row, sum it
+  float f[8];
   double part = 0.0;
-  for (int v0 = lo + lane; v0 < hi; v0 += 64 * kBatch) {
-    float raw[kBatch];
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int v = v0 + 64 * j;
-      raw[j] = __builtin_bit_cast(
-          float, __builtin_amdgcn_raw_buffer_load_b32(rs, v < hi ? v * 4 : vocab * 4, 0, 0));
-    }
+  for (int e = 0; e < 8; ++e) {
+    const int v = v0 + e;
+    f[e] = greedy ? (v == st.argmax ? 1.0f : 0.0f) : draft_qv(raw[e], inv_t, st.zmax, st.total);
+    if (v < vocab) part += (double)f[e];
+  }
+  if (vec8 && v0 < vocab) {
+    *(f32x4 *)(qr + v0) = f32x4{f[0], f[1], f[2], f[3]};
+    *(f32x4 *)(qr + v0 + 4) = f32x4{f[4], f[5], f[6], f[7]};
+  } else {
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int v = v0 + 64 * j;
-      if (v < hi) {
-        const float f = draft_qv(d, raw[j]);
-        qr[v] = f;
-        part += (double)f;
-      }
-    }
+    for (int e = 0; e < 8; ++e)
+      if (v0 + e < vocab) qr[v0 + e] = f[e];
   }
   part = wave_sum(part);
-  if (lane == 0) sh.red[w] = part;
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
   __syncthreads();
   if (threadIdx.x == 0) {
-    double run = 0.0;
-    for (int k = 0; k < kWaves; ++k) {
-      const double t = sh.red[k];
-      sh.red[k] = run;
-      run += t;
+    double t = red[0];
+    for (int w = 1; w < kDraftThreads / 64; ++w) t += red[w];
+    bsum[(size_t)i * nblk + blk] = t;
+  }
+}
+
+// Inclusive 64-lane scan of a double.
+__device__ __forceinline__ double wave_scan(double x) {
+  const int lane = threadIdx.x & 63;
+  for (int o = 1; o < 64; o <<= 1) {
+    const double y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+__global__ __launch_bounds__(kDraftThreads) void k_draft_draw(int vocab, int nblk, DraftRows rows,
+                                                              const sb_row_stats *__restrict__ stats,
+                                                              int greedy, const float *__restrict__ u,
+                                                              int32_t *__restrict__ tokens,
+                                                              const float *__restrict__ q,
+                                                              const double *__restrict__ bsum) {
+  __shared__ double s_base, s_thr, wsum[kDraftThreads / 64];
+  __shared__ int s_blk, s_tok;
+  const int i = blockIdx.x;
+  const int src = rows.src[i], dst = rows.dst[i];
+  if (greedy) {
+    if (threadIdx.x == 0) tokens[dst] = stats[src].argmax;
+    return;
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const double *bs = bsum + (size_t)i * nblk;
+  // wave 0: lane l sums the block sums l*per .. l*per + per - 1 in order,
+  // scans the lane sums, and finds the first block whose running sum
+  // exceeds u * W (else the last block with mass)
+  if (w == 0) {
+    const int per = (nblk + 63) / 64;
+    double ls = 0.0;
+    for (int j = 0; j < per; ++j) {
+      const int b = lane * per + j;
+      if (b < nblk) ls += bs[b];
     }
-    sh.red[kWaves] = run;
+    const double inc = wave_scan(ls);
+    const double W = __shfl(inc, 63, 64);
+    const double thr = (double)u[i] * W;
+    const unsigned long long hit = __ballot(ls > 0.0 && inc > thr);
+    int sel_lane;
+    if (hit) {
+      sel_lane = __ffsll((long long)hit) - 1;
+    } else {
+      const unsigned long long pos = __ballot(ls > 0.0);
+      sel_lane = pos ? 63 - __clzll((long long)pos) : 0;
+    }
+    if (lane == sel_lane) {
+      double run = inc - ls;
+      int blk = -1, last = -1;
+      double base_at = run, base_last = run;
+      for (int j = 0; j < per; ++j) {
+        const int b = lane * per + j;
+        if (b >= nblk) break;
+        const double x = bs[b];
+        if (x > 0.0) {
+          last = b;
+          base_last = run;
+          if (blk < 0 && run + x > thr) {
+            blk = b;
+            base_at = run;
+          }
+        }
+        run += x;
+      }
+      if (blk < 0) {
+        blk = last < 0 ? 0 : last;
+        base_at = base_last;
+      }
+      s_blk = blk;
+      s_base = base_at;
+      s_thr = thr;
+    }
   }
   __syncthreads();
-  // pass 2: the wave whose segment crosses u * W finds the token, lane l
-  // holding the 8 consecutive values 8l .. 8l + 7 of a block of 512
-  const double W = sh.red[kWaves];
-  const double thr = (double)u[i] * W;
-  const double seg_end = (w + 1 < kWaves) ? sh.red[w + 1] : W;
-  double run = sh.red[w];
-  int cand = INT_MAX;
-  if (lo < hi && seg_end > thr) {
-    for (int b0 = lo; b0 < hi && cand == INT_MAX; b0 += 512) {
-      const int e0 = b0 + 8 * lane;
-      float raw[8];
+  // the crossing block: thread t holds its 8 consecutive values, a block-wide
+  // scan of the thread sums finds the thread, that thread finds the token
+  const int blk = s_blk;
+  const double thr = s_thr - s_base;
+  const int v0 = blk * kDraftSpan + (int)threadIdx.x * 8;
+  const float *qr = q + (size_t)dst * vocab;
+  double x[8], ts = 0.0;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        raw[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                               rs, e0 + e < hi ? (e0 + e) * 4 : vocab * 4, 0, 0));
-      double x[8], ls = 0.0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        x[e] = e0 + e < hi ? (double)draft_qv(d, raw[e]) : 0.0;
-        ls += x[e];
+  for (int e = 0; e < 8; ++e) {
+    x[e] = v0 + e < vocab ? (double)qr[v0 + e] : 0.0;
+    ts += x[e];
+  }
+  const double inc = wave_scan(ts);
+  if (lane == 63) wsum[w] = inc;
+  if (threadIdx.x == 0) s_tok = INT_MAX;
+  __syncthreads();
+  double off = 0.0;
+  for (int k = 0; k < w; ++k) off += wsum[k];
+  const double start = off + inc - ts;
+  const unsigned long long hit = __ballot(ts > 0.0 && start + ts > thr);
+  int found = INT_MAX;
+  if (hit && lane == __ffsll((long long)hit) - 1) {
+    double c = start;
+    for (int e = 0; e < 8; ++e) {
+      c += x[e];
+      if (x[e] > 0.0 && c > thr) {
+        found = v0 + e;
+        break;
       }
-      double inc = ls;
-      for (int o = 1; o < 64; o <<= 1) {
-        const double y = __shfl_up(inc, o, 64);
-        if (lane >= o) inc += y;
-      }
-      const double lane_start = run + (inc - ls);
-      const unsigned long long hit = __ballot(e0 < hi && lane_start + ls > thr);
-      if (hit) {
-        const int first = __ffsll((long long)hit) - 1;
-        int found = INT_MAX;
-        if (lane == first) {
-          double c = lane_start;
-          for (int e = 0; e < 8; ++e) {
-            c += x[e];
-            if (e0 + e < hi && x[e] > 0.0 && c > thr) {
-              found = e0 + e;
-              break;
-            }
-          }
-          if (found == INT_MAX)  // rounding: the lane's last token with mass
-            for (int e = 0; e < 8; ++e)
-              if (e0 + e < hi && x[e] > 0.0) found = e0 + e;
-        }
-        cand = __shfl(found, first, 64);
-      }
-      run += __shfl(inc, 63, 64);
     }
+    if (found == INT_MAX)  // rounding: the thread's last token with mass
+      for (int e = 0; e < 8; ++e)
+        if (x[e] > 0.0) found = v0 + e;
   }
-  int y = block_min<kWaves>(cand, sh.ired);
-  if (y == INT_MAX) {
-    // rounding left no crossing: the last token with mass
-    int lp = -1;
-    for (int v = threadIdx.x; v < vocab; v += kWalkThreads)
-      if (draft_qv(d, l[v]) > 0.0f) lp = v;
-    y = block_max<kWaves>(lp, sh.ired);
-    if (y < 0) y = st.argmax;
+  if (found != INT_MAX) atomicMin(&s_tok, found);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int y = s_tok;
+    if (y == INT_MAX) {
+      // rounding left no crossing in the block: its last token with mass
+      for (int v = min(vocab, (blk + 1) * kDraftSpan) - 1; v >= blk * kDraftSpan; --v)
+        if (qr[v] > 0.0f) {
+          y = v;
+          break;
+        }
+      if (y == INT_MAX) y = stats[src].argmax;
+    }
+    tokens[dst] = y;
   }
-  if (threadIdx.x == 0) tokens[dst] = y;
 }
 
 }  // namespace
@@ -1031,14 +1098,24 @@ hipError_t launch_walk(int vocab, const TreeArg &tree, const int32_t *tokens, co
   return hipGetLastError();
 }
 
+size_t draft_ws_bytes(int vocab, int n) {
+  return (size_t)n * ((vocab + kDraftSpan - 1) / kDraftSpan) * sizeof(double);
+}
+
 hipError_t launch_draft_sample(int vocab, const DraftRows &rows, const float *logits,
                                const sb_row_stats *stats, float temperature, const float *u,
-                               int32_t *tokens, float *q, hipStream_t s) {
+                               int32_t *tokens, float *q, void *ws, hipStream_t s) {
   float inv_t;
   int greedy;
   temp_args(temperature, &inv_t, &greedy);
-  hipLaunchKernelGGL(k_draft_sample, dim3(rows.n), dim3(kWalkThreads), 0, s, vocab, rows, logits,
-                     stats, inv_t, greedy, u, tokens, q);
+  const int nblk = (vocab + kDraftSpan - 1) / kDraftSpan;
+  const int vec8 = vocab % 8 == 0 && ((uintptr_t)logits & 15) == 0 && ((uintptr_t)q & 15) == 0;
+  hipLaunchKernelGGL(k_draft_q, dim3(nblk, rows.n), dim3(kDraftThreads), 0, s, vocab, vec8, rows,
+                     logits, stats, inv_t, greedy, q, (double *)ws);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_draft_draw, dim3(rows.n), dim3(kDraftThreads), 0, s, vocab, nblk, rows,
+                     stats, greedy, u, tokens, q, (const double *)ws);
   return hipGetLastError();
 }
 

@@ -152,8 +152,15 @@ def test_draft_host_validation_without_device(api):
     lib = api.lib
     I = lambda *a: (C.c_int32 * len(a))(*a)
 
-    def samp(n=2, src=(0, 1), dst=(0, 1), nl=2, no=2, T=1.0, logits=1, u=1):
-        return lib.sb_draft_sample(100, n, logits, 1, nl, I(*src), T, u, 1, 1, no, I(*dst), None)
+    def samp(n=2, src=(0, 1), dst=(0, 1), nl=2, no=2, T=1.0, logits=1, u=1, ws=1, wb=None):
+        wb = lib.sb_draft_sample_workspace_bytes(100, n) if wb is None else wb
+        return lib.sb_draft_sample(100, n, logits, 1, nl, I(*src), T, u, 1, 1, no, I(*dst), ws, wb,
+                                   None)
+    assert lib.sb_draft_sample_workspace_bytes(100, 2) == 2 * 8
+    assert lib.sb_draft_sample_workspace_bytes(4097, 3) == 3 * 3 * 8     # blocks of 2048
+    assert lib.sb_draft_sample_workspace_bytes(100, 0) == 0
+    assert samp(ws=None) == 1
+    assert samp(wb=15) == 3
     assert samp(logits=None) == 1
     assert samp(u=None) == 1
     assert samp(n=0) == 1

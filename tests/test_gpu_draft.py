@@ -75,7 +75,8 @@ def test_draft_sample_matches_oracle(api, V, T, n):
     toks = torch.full((n_out,), -5, dtype=torch.int32, device=dev)
     q = torch.full((n_out, V), 7.0, dtype=torch.float32, device=dev)
     say(f"draft sample V={V} T={T} n={n}")
-    api.sb_draft_sample(ld, stats, src, T, torch.from_numpy(u).to(dev), toks, q, dst)
+    ws = torch.empty(api.sb_draft_sample_workspace_bytes(V, n), dtype=torch.uint8, device=dev)
+    api.sb_draft_sample(ld, stats, src, T, torch.from_numpy(u).to(dev), toks, q, dst, ws)
     torch.cuda.synchronize()
     toks, q = toks.cpu().numpy(), q.cpu().numpy()
     for i in range(n):
