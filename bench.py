@@ -237,6 +237,57 @@ def trace_summary(trace_dir: str) -> str:
     return "\n".join(out) + "\n"
 
 
+def draft_trace_summary(trace_dir: str) -> str:
+    """Markdown summary of the draft side in a rocprofv3 --kernel-trace
+    --stats run of bench.py: the draft-side kernels' whole-run stats, then one
+    drafting round broken down by kernel (the windows between consecutive
+    branch-point launches of the timed rounds, each holding one round's
+    continuation steps and the next round's root step)."""
+    import collections
+    import csv
+    import glob
+    import re
+    stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)[0]
+    trace = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
+    rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
+    short = lambda n: (re.search(r"(k_[A-Za-z0-9_]+)", n) or re.search(r"(\S+)", n)).group(1)
+    sel = [i for i, r in enumerate(rows) if "k_branch_select" in r["Kernel_Name"]]
+    # the timed rounds: the 3rd .. 22nd branch-point launches (two warmup rounds first)
+    wins = [(sel[j], sel[j + 1]) for j in range(2, min(21, len(sel) - 1))]
+    agg = collections.defaultdict(list)
+    spans, busy = [], []
+    for a, b in wins:
+        per = collections.Counter()
+        for r in rows[a:b]:
+            per[short(r["Kernel_Name"])] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        for k, v in per.items():
+            agg[k].append(v)
+        spans.append((int(rows[b]["Start_Timestamp"]) - int(rows[a]["Start_Timestamp"])) / 1e3)
+        busy.append(sum(per.values()))
+    counts = collections.Counter(short(r["Kernel_Name"]) for r in rows[wins[0][0]:wins[0][1]])
+    out = ["# Kernel trace of the draft side: 68M draft round (k_max 4, depth 8, prefix 2048), "
+           "branch-point candidates and draft sampler", "",
+           "Command: `cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
+           "--output-format csv -d <repo>/gpurun_out/prof_draft -o run -- python3 <repo>/bench.py "
+           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-graph`, then "
+           "`python3 bench.py --draft-trace-summary gpurun_out/prof_draft`", "",
+           f"One round ({len(wins)} rounds): kernel time {sum(busy) / len(busy):.1f} us, "
+           f"span under the tracer {sum(spans) / len(spans):.1f} us", "",
+           "| kernel | launches/round | us/round | avg us |", "|---|---|---|---|"]
+    for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        per = sum(v) / len(wins)
+        out.append(f"| `{k}` | {counts[k]} | {per:.1f} | {per / max(1, counts[k]):.2f} |")
+    out += ["", "Whole-run `--stats` of the draft-side kernels (rounds, the candidate and sampler "
+            "timing loops, the overlap runs):", "",
+            "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+    for r in csv.DictReader(open(stats)):
+        if re.search(r"k_branch_|k_draft_", r["Name"]):
+            out.append(f"| `{short(r['Name'])}` | {r['Calls']} | "
+                       f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                       f"{float(r['MaxNs']) / 1e3:.2f} |")
+    return "\n".join(out) + "\n"
+
+
 def algorithmic_bytes(shape, P_kv: int, n: int) -> dict:
     """Bytes the verify step must move at least once (bf16 weights read once,
     prefix KV read once, tree KV written, fp32 logits written and read)."""
@@ -413,6 +464,8 @@ def main():
                     help="end with a device copy of known size (for rocprofv3 --pmc runs)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs of this script and exit")
+    ap.add_argument("--draft-trace-summary", metavar="TRACE_DIR",
+                    help="print the draft-side summary of a rocprofv3 kernel trace and exit")
     ap.add_argument("--trace-summary", metavar="TRACE_DIR",
                     help="summarise a rocprofv3 --kernel-trace --stats run of this script and exit")
     args = ap.parse_args()
@@ -421,6 +474,9 @@ def main():
         return
     if args.trace_summary:
         print(trace_summary(args.trace_summary))
+        return
+    if args.draft_trace_summary:
+        print(draft_trace_summary(args.draft_trace_summary), end="")
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
