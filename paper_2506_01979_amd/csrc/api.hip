@@ -30,6 +30,7 @@ struct sb_model {
 };
 
 namespace sb {
+thread_local LaunchEvents g_launch_events;
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -161,21 +162,29 @@ EmbedArgs embed_args(const sb_model *m, const int32_t *tokens, float *h, int n, 
   return ea;
 }
 
-// Brackets one launch of kernel class kc with the model's timer events.
+// Times one launch of kernel class kc with the model's timer events: a GEMM
+// class hands them to its dispatch (which records the kernel's own start and
+// end), any other class records them before and after its launch.
 struct TimedLaunch {
   sb_timer &t;
   hipStream_t s;
-  bool on;
+  bool on, gemm;
   TimedLaunch(sb_model *m, int kc, hipStream_t st)
       : t(m->timer), s(st), on(m->timer.active && m->timer.kernel_class == kc &&
-                               m->timer.used < (int)m->timer.start.size()) {
-    if (on) hipEventRecord(t.start[t.used], s);
+                               m->timer.used < (int)m->timer.start.size()),
+        gemm(kc == SB_KC_QKV || kc == SB_KC_O || kc == SB_KC_GATE_UP || kc == SB_KC_DOWN ||
+             kc == SB_KC_LM_HEAD) {
+    if (!on) return;
+    if (gemm)
+      g_launch_events = LaunchEvents{t.start[t.used], t.stop[t.used], false};
+    else
+      hipEventRecord(t.start[t.used], s);
   }
   ~TimedLaunch() {
-    if (on) {
-      hipEventRecord(t.stop[t.used], s);
-      ++t.used;
-    }
+    if (!on) return;
+    if (!gemm) hipEventRecord(t.stop[t.used], s);
+    g_launch_events.taken = true;
+    ++t.used;
   }
 };
 

@@ -13,6 +13,8 @@
 
 #include <math.h>
 
+#include <hip/hip_ext.h>
+
 #include "sb_device.h"
 #include "sb_internal_fwd.h"
 
@@ -448,7 +450,14 @@ hipError_t launch_tt_nt(const GemmArgs &a, int grid, hipStream_t s) {
   if constexpr (NT > gemm_nt_cap(TT)) {
     return hipErrorInvalidValue;
   } else {
-    hipLaunchKernelGGL((k_gemm<EPI, TT, NT>), dim3(grid), dim3(kGemmThreads), 0, s, a);
+    LaunchEvents &ev = g_launch_events;
+    if (!ev.taken) {
+      ev.taken = true;
+      hipExtLaunchKernelGGL((k_gemm<EPI, TT, NT>), dim3(grid), dim3(kGemmThreads), 0, s, ev.start,
+                            ev.stop, 0, a);
+    } else {
+      hipLaunchKernelGGL((k_gemm<EPI, TT, NT>), dim3(grid), dim3(kGemmThreads), 0, s, a);
+    }
     return hipGetLastError();
   }
 }

@@ -195,6 +195,14 @@ hipError_t launch_gemm_logits(const GemmArgs &a, const GemmPlan &p, hipStream_t 
 hipError_t launch_gemm_resid_norm(const GemmArgs &a, const GemmPlan &p, hipStream_t s);
 // *split receives the K split used (the number of delta slices for RESID).
 hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int *split, hipStream_t s);
+// Timing events a measured launch hands to the next GEMM dispatch, which
+// passes them to hipExtLaunchKernelGGL so that the dispatch itself records
+// the kernel's start and end; taken once, then ignored.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+  bool taken = true;
+};
+extern thread_local LaunchEvents g_launch_events;
 // Whether a residual projection of `tiles` tiles over n_tok rows can run as
 // RESID_NORM (one pass, one reduction round, at most kSsGroups groups,
 // n_tok <= kNormFuseRows); *groups receives its group count.
