@@ -36,8 +36,9 @@ def branch_count(q_xb: float, k_max: int, n_positive: int | None = None) -> int:
     return min(b, n_positive) if n_positive is not None else b
 
 
-def candidates(q_row, x_b: int, k_max: int, mode: str, u):
-    """(tokens [B] int32, rows [B][V] float32)."""
+def candidates(q_row, x_b: int, k_max: int, mode: str, u, trace: list | None = None):
+    """(tokens [B] int32, rows [B][V] float32).  With `trace`, each draw is
+    recorded as sampling.draw records it (uniform index i for candidate i)."""
     q = np.asarray(q_row, dtype=np.float32)
     V = len(q)
     nnz = int(np.count_nonzero(q > 0))
@@ -51,14 +52,14 @@ def candidates(q_row, x_b: int, k_max: int, mode: str, u):
             rows[i, toks[i]] = 1.0
     elif mode == "iid":
         for i in range(B):
-            toks[i] = draw(q.astype(np.float64), float(u[i]))
+            toks[i] = draw(q.astype(np.float64), float(u[i]), trace, i)
             rows[i] = q
     elif mode == "wor":
         rem = q.astype(np.float64).copy()
         for i in range(B):
             Z = float(np.sum(rem))
             rows[i] = (rem / Z).astype(np.float32)
-            toks[i] = draw(rem, float(u[i]))
+            toks[i] = draw(rem, float(u[i]), trace, i)
             rem[toks[i]] = 0.0
     else:
         raise ValueError(mode)

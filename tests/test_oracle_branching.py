@@ -76,3 +76,52 @@ def test_without_replacement_pair_law_by_enumeration():
     want = np.array([[0.0 if a == b else qd[a] * qd[b] / (1 - qd[a]) for b in range(4)]
                      for a in range(4)])
     assert np.abs(freq - want).max() < 2.0 / n
+
+
+@pytest.mark.parametrize("mode", branching.MODES)
+def test_candidates_through_algorithm1_emit_the_target_distribution(mode):
+    """R1 end to end: the candidates and the rows they carry, tested by
+    Algorithm 1 at the root (sampling.accept_resample over the root and B
+    children), emit a first token distributed exactly as p.  Exact
+    enumeration over the candidate draws' uniforms and the walk's together."""
+    from oracle import sampling
+    from walk_enum import enumerate_outcomes
+    V = 6
+    k = np.array([9, 3, 7, 2, 6, 5], dtype=np.int64)          # dyadic q: draws and rows agree
+    q = (k / k.sum()).astype(np.float32)
+    q = (np.round(q.astype(np.float64) * 2 ** 20) / 2 ** 20).astype(np.float32)
+    q[0] += np.float32(1.0) - q.sum(dtype=np.float32)
+    p = np.array([0.05, 0.3, 0.1, 0.25, 0.2, 0.1])
+    x_b, k_max = 3, 4                                           # B = floor(4 (1 - q_3)) = 3
+    B = branching.branch_count(q[x_b], k_max, V)
+    assert B == 3
+    logits = np.zeros((1 + B, V), dtype=np.float32)
+    logits[0] = np.log(p).astype(np.float32)
+    p_used = sampling.target_probs(logits[0], 1.0)
+    parents = [-1] + [0] * B
+
+    def run(u):
+        tr = []
+        toks, rows = branching.candidates(q, x_b, k_max, mode, u[:B], trace=tr)
+        qa = np.zeros((1 + B, V), dtype=np.float32)
+        qa[1:] = rows
+        wt = []
+        r = sampling.accept_resample([0] + [int(t) for t in toks], parents, logits, 1.0, qa,
+                                     u[B:], trace=wt)
+        tr += [(ev[0], ev[1] + B) + tuple(ev[2:]) for ev in wt]
+        r.first = int(toks[r.path[1] - 1]) if r.n_accepted else r.next_token
+        return r, tr
+
+    def relevant(r, tr):
+        # after an accepted child the bonus draw no longer moves the first token
+        return len(tr) - 1 if r.n_accepted else len(tr)
+
+    out = enumerate_outcomes(run, 2 * B + 1, lambda r: r.first, relevant)
+    dist = np.zeros(V)
+    for v, pr in out.items():
+        dist[v] += pr
+    # rows without replacement are float32 roundings of the remainders the
+    # draws use, ~1e-8 apart
+    tol = 1e-6 if mode == "wor" else 1e-9
+    assert abs(dist.sum() - 1.0) < tol
+    assert np.max(np.abs(dist - p_used)) < tol
