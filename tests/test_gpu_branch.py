@@ -94,6 +94,10 @@ CASES = [
     ("sparse", 32000, 16, 18, 0),
     ("tied", 4096, 16, 19, 0),
     ("peaked", 32000, 6, 20, 0),
+    ("softmax", 1, 16, 21, 0),                # one token: B = 1, that token
+    ("softmax", 2, 16, 22, 0),
+    ("softmax", 32768, 16, 23, 0),            # the largest vocabulary kept in LDS
+    ("softmax", 32769, 16, 24, 0),            # the smallest one read from memory
 ]
 
 

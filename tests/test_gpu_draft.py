@@ -59,7 +59,8 @@ def cum_margin(q_row, u):
 
 
 @pytest.mark.parametrize("V,T,n", [(32000, 0.7, 6), (32000, 1.0, 16), (1003, 1.3, 5), (16, 0.9, 9),
-                                   (32000, 0.0, 4), (128256, 0.8, 3)])
+                                   (32000, 0.0, 4), (128256, 0.8, 3), (1000, 1.0, 64), (1, 1.0, 2),
+                                   (2052, 0.9, 3)])
 def test_draft_sample_matches_oracle(api, V, T, n):
     seed = V % 97 + n
     logits = synth.random_logits(n + 2, V, scale=3.0, seed=seed)
@@ -150,6 +151,9 @@ ROUND_CASES = [
     ("tiny", 40, 4, 8, 1.2, 7),
     ("tiny", 96, 6, 4, 0.8, 5),
     ("exact", 8, 6, 5, 0.0, 5),
+    ("exact", 8, 6, 1, 0.9, 6),               # depth 1: the candidates alone
+    ("exact", 8, 1, 6, 0.9, 7),               # k_max 1: one branch, a chain
+    ("exact", 8, 16, 15, 1.0, 8),             # 241 rows, near the 256-row limit
 ]
 
 
