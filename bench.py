@@ -657,7 +657,7 @@ def main():
     # depth k (a near-flat q at the branch point gives the verify step's B),
     # then the branch-point candidates and the draft sampler on their own.
     # Not part of `value`.
-    draft_out = overlap_out = None
+    draft_out = overlap_out = spec_out = None
     if not args.no_draft:
         dshape = synth.SHAPES["draft68m"]
         dm = api.Model(dshape, api.synth_tensors(dshape, seed=1), device=dev)
@@ -720,6 +720,35 @@ def main():
         dsws = torch.empty(api.sb_draft_sample_workspace_bytes(V, B), dtype=torch.uint8, device=dev)
         samp_us = graph_us(lambda st: api.sb_draft_sample(logits, stats, src, 1.0, du, dtok, dq, dst,
                                                           dsws, st))
+        # One whole round on the draft's own output: the 7B target verifies
+        # the draft's tree with the q rows its tokens were drawn from, then
+        # the walk and the rollback (random weights on both sides, so few
+        # drafts are accepted; the mechanics and the time are the point).
+        rtok = torch.empty(R, dtype=torch.int32, device=dev)
+        rq = torch.empty((R, V), dtype=torch.float32, device=dev)
+
+        def spec_round():
+            nb, par_d = dm.sb_draft_round(dk_, dv_, kv_len, DK, "wor", DD, 1.0, du, rtok, rq, dws,
+                                          stream)
+            m.sb_verify_forward(k_, v_, kv_len, rtok, par_d, 1.0, logits, stats, ws, stream)
+            api.sb_accept_resample(rtok, par_d, logits, stats, 1.0, rq, d_u, res, sws, stream)
+            m.sb_kv_rollback(k_, v_, kv_len, res, new_len, stream)
+            return nb, par_d
+        rtok[0] = root
+        for _ in range(2):
+            spec_round()
+        torch.cuda.synchronize()
+        committed = []
+        ev0.record(stream)
+        for _ in range(reps):
+            nb_r, par_r = spec_round()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        spec_ms = ev0.elapsed_time(ev1) / reps
+        rr = api.decode_result(res)
+        spec_out = {"round_ms": round(spec_ms, 4), "tree_rows": int(len(par_r)), "branches": nb_r,
+                    "committed": rr["n_accepted"] + 1, "kept_branch": rr["branch"]}
+
         # Algorithm 2's overlap on one GPU: the target's verify step on one
         # stream while the draft builds the next round's branches on another
         # (default priorities), then Algorithm 1 over the branches' first
@@ -827,6 +856,7 @@ def main():
     if draft_out is not None:
         out["draft"] = draft_out
         out["overlap"] = overlap_out
+        out["spec_round"] = spec_out
 
     if not args.no_alpha_sweep:
         sweep = {}
