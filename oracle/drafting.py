@@ -8,19 +8,28 @@ the token is the inverse-CDF draw (sampling.draw) over that float32 row with
 the row's uniform.  T = 0: q is one-hot at the argmax (lowest index on
 ties) and the token is the argmax.
 
-``draft_round`` -- one drafting phase with its branch point right after the
-root (Section "Branch Resampling", the drafting of Algorithm 2):
+``draft_round`` -- one drafting phase (Section "Branch Resampling", the
+drafting of Algorithm 2), with the branch point at the draft's first
+unconfident token:
   1. the draft scores the root (the last committed token, not yet cached)
-     on its prefix cache; x_b is drawn from that row's q with u[0];
-  2. B sibling first tokens come from the same q by branching.candidates,
-     with u[1 .. k_max], each carrying its own q row (reading R1);
+     on its prefix cache and drafts a chain: x_t (t = 1, 2, ...) is drawn
+     from the distribution at row t - 1 with u[t - 1].  The branch point is
+     the first x_t whose own probability q(x_t) is below the confidence
+     threshold epsilon (both float32), or x_trunk_max; the confident tokens
+     before it, c = t - 1 of them, stay in the tree as a chain (rows 1 .. c);
+  2. x_b = that token sets B, and B sibling first tokens come from the
+     distribution it was drawn from by branching.candidates, with
+     u[trunk_max .. trunk_max + k_max - 1], each carrying its own q row
+     (reading R1);
   3. each branch then continues on its own prefix: its depth-d token
      (d = 2 .. depth) is drawn from the draft's distribution at its depth
-     d - 1 row, with u[1 + k_max (d - 1) + i] for branch i.
-The tree is depth-major: row 1 + (d - 1) B + i holds branch i's depth-d
-token; its parent is row 0 at d = 1 and row - B after that.  Row i of the
-returned q is the distribution token i was drawn from (row 0: the root's
-distribution, the one x_b came from).  Every step scores the whole tree so
+     d - 1 row, with u[trunk_max + k_max (d - 1) + i] for branch i.
+trunk_max = 1 puts the branch point right after the root (x_b = x_1).
+The branches are depth-major: row c + 1 + (d - 1) B + i holds branch i's
+depth-d token; its parent is row c at d = 1 and row - B after that.  Row i
+of the returned q is the distribution token i was drawn from, and row 0
+(the root, which verification does not test) holds the branch position's
+distribution, the one x_b came from.  Every step scores the whole tree so
 far with decoder.tree_forward; a row's logits do not depend on later rows.
 """
 from __future__ import annotations
@@ -40,38 +49,54 @@ def sample(logits_row, T: float, u: float):
 
 @dataclass
 class DraftRound:
-    tokens: np.ndarray    # int32 [1 + B depth], row 0 the root
-    parents: np.ndarray   # int32 [1 + B depth]
-    q: np.ndarray         # float32 [1 + B depth][V]
+    tokens: np.ndarray    # int32 [1 + c + B depth], row 0 the root
+    parents: np.ndarray   # int32, same length
+    q: np.ndarray         # float32 [rows][V]
     branches: int         # B
     x_b: int
+    chain: int = 0        # c, the confident drafts before the branch point
 
 
-def uniforms_needed(k_max: int, depth: int) -> int:
-    return 1 + k_max * depth
+def uniforms_needed(k_max: int, depth: int, trunk_max: int = 1) -> int:
+    return trunk_max + k_max * depth
 
 
 def draft_round(shape, weights: dict, prefix_k, prefix_v, kv_len: int, root_token: int,
-                k_max: int, mode: str, depth: int, T: float, u, prec: str = "f64") -> DraftRound:
+                k_max: int, mode: str, depth: int, T: float, u, prec: str = "f64",
+                trunk_max: int = 1, epsilon: float = float("inf")) -> DraftRound:
     u = np.asarray(u, dtype=np.float32)
-    assert depth >= 1 and len(u) >= uniforms_needed(k_max, depth)
+    assert depth >= 1 and trunk_max >= 1
+    assert len(u) >= uniforms_needed(k_max, depth, trunk_max)
+    eps = np.float32(epsilon)
     toks = [int(root_token)]
     parents = [-1]
-    lg, _, _ = decoder.tree_forward(shape, weights, prefix_k, prefix_v, kv_len, toks, parents, prec)
-    q_root, x_b = sample(lg[0], T, u[0])
-    cand, rows = branching.candidates(q_root, x_b, k_max, mode, u[1:1 + k_max])
+    q = [None]
+    for t in range(1, trunk_max + 1):
+        lg, _, _ = decoder.tree_forward(shape, weights, prefix_k, prefix_v, kv_len, toks, parents,
+                                        prec)
+        q_t, x_t = sample(lg[t - 1], T, u[t - 1])
+        if t == trunk_max or q_t[x_t] < eps:
+            q_b, x_b = q_t, x_t
+            break
+        toks.append(x_t)
+        parents.append(t - 1)
+        q.append(q_t)
+    c = len(toks) - 1
+    q[0] = q_b
+    u0 = trunk_max
+    cand, rows = branching.candidates(q_b, x_b, k_max, mode, u[u0:u0 + k_max])
     B = len(cand)
-    q = [q_root] + list(rows)
+    q += list(rows)
     toks += [int(t) for t in cand]
-    parents += [0] * B
+    parents += [c] * B
     for d in range(2, depth + 1 if B else 0):
         lg, _, _ = decoder.tree_forward(shape, weights, prefix_k, prefix_v, kv_len, toks, parents,
                                         prec)
         for i in range(B):
-            r = 1 + (d - 2) * B + i
-            qi, t = sample(lg[r], T, u[1 + k_max * (d - 1) + i])
+            r = c + 1 + (d - 2) * B + i
+            qi, t = sample(lg[r], T, u[u0 + k_max * (d - 1) + i])
             toks.append(t)
             parents.append(r)
             q.append(qi)
     return DraftRound(np.asarray(toks, dtype=np.int32), np.asarray(parents, dtype=np.int32),
-                      np.stack(q).astype(np.float32), B, int(x_b))
+                      np.stack(q).astype(np.float32), B, int(x_b), c)

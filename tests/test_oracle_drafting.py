@@ -114,3 +114,48 @@ def test_greedy_round_is_one_branch_of_greedy_decoding():
             lg = m(torch.tensor(np.asarray(seq, dtype=np.int64))[None]).logits[0, -1].numpy()
         seq.append(int(np.argmax(lg)))
     assert r.tokens[1:].tolist() == seq[len(ptoks):]
+
+
+@pytest.mark.parametrize("mode", branching.MODES)
+def test_round_with_a_confident_chain(mode):
+    """The branch point is the first drafted token below the confidence
+    threshold: the chain before it holds the library model's draws (each
+    token at or above the threshold), x_b is below it (or the last allowed),
+    and every branch continues after the chain."""
+    k_max, depth, T, trunk_max, eps = 4, 3, 0.9, 6, 0.07
+    seed = 8
+    W = synth.model_weights(SHAPE, seed=seed)
+    ptoks = synth.prefix_tokens(SHAPE.vocab, 9, seed=seed)
+    _, K, V = decoder.prefill(SHAPE, W, ptoks[:-1], "f64")
+    u = synth.uniforms(drafting.uniforms_needed(k_max, depth, trunk_max), seed=seed)
+    r = drafting.draft_round(SHAPE, W, K, V, len(ptoks) - 1, int(ptoks[-1]), k_max, mode, depth, T,
+                             u, trunk_max=trunk_max, epsilon=eps)
+    c, B = r.chain, r.branches
+    assert 1 <= c < trunk_max                      # this seed drafts a chain, then branches
+    assert len(r.tokens) == 1 + c + B * depth
+    assert r.parents.tolist() == ([-1] + list(range(c)) + [c] * B +
+                                  [c + 1 + (d - 2) * B + i for d in range(2, depth + 1)
+                                   for i in range(B)])
+    m = hf_model(SHAPE, W, exact_rope=True)
+    chain = r.tokens[1:1 + c]
+    with torch.no_grad():
+        lg = m(torch.tensor(np.concatenate([ptoks, chain]).astype(np.int64))[None]).logits[0]
+    lg = lg.double().numpy()
+    for t in range(1, c + 2):                      # chain tokens, then x_b
+        ref = scipy.special.softmax(lg[len(ptoks) + t - 2] / np.float64(np.float32(T)))
+        row = r.q[t] if t <= c else r.q[0]
+        assert np.max(np.abs(row - ref)) < 1e-6
+        C = np.cumsum(row.astype(np.float64))
+        tok = r.tokens[t] if t <= c else r.x_b
+        assert tok == int(np.searchsorted(C, np.float64(u[t - 1]) * C[-1], side="right"))
+        assert (row[tok] >= np.float32(eps)) == (t <= c)
+    ct, cr = branching.candidates(r.q[0], r.x_b, k_max, mode, u[trunk_max:trunk_max + k_max])
+    assert r.tokens[1 + c:1 + c + B].tolist() == ct.tolist()
+    for i in range(B):                             # each branch continues after the chain
+        rows = [1 + c + (d - 1) * B + i for d in range(1, depth + 1)]
+        seq = np.concatenate([ptoks, chain, r.tokens[rows]]).astype(np.int64)
+        with torch.no_grad():
+            lb = m(torch.tensor(seq)[None]).logits[0].double().numpy()
+        for d in range(2, depth + 1):
+            ref = scipy.special.softmax(lb[len(ptoks) + c + d - 2] / np.float64(np.float32(T)))
+            assert np.max(np.abs(r.q[rows[d - 1]] - ref)) < 1e-6
