@@ -678,7 +678,7 @@ def main():
         reps = 20
         ev0.record(stream)
         for _ in range(reps):
-            bd, _ = draft_round()
+            bd, _, _ = draft_round()
         ev1.record(stream)
         torch.cuda.synchronize()
         round_ms = ev0.elapsed_time(ev1) / reps
@@ -728,7 +728,7 @@ def main():
         rq = torch.empty((R, V), dtype=torch.float32, device=dev)
 
         def spec_round():
-            nb, par_d = dm.sb_draft_round(dk_, dv_, kv_len, DK, "wor", DD, 1.0, du, rtok, rq, dws,
+            nb, par_d, _ = dm.sb_draft_round(dk_, dv_, kv_len, DK, "wor", DD, 1.0, du, rtok, rq, dws,
                                           stream)
             m.sb_verify_forward(k_, v_, kv_len, rtok, par_d, 1.0, logits, stats, ws, stream)
             api.sb_accept_resample(rtok, par_d, logits, stats, 1.0, rq, d_u, res, sws, stream)

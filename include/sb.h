@@ -350,35 +350,44 @@ size_t sb_draft_sample_workspace_bytes(int32_t vocab, int32_t n);
 
 /* Workspace bytes of sb_draft_round (0 for arguments it rejects). */
 size_t sb_draft_round_workspace_bytes(const sb_model *draft, int32_t k_max, int32_t depth,
-                                      int32_t kv_len);
+                                      int32_t trunk_max, int32_t kv_len);
 
-/* One drafting phase of a SpecBranch round with its branch point right after
- * the root (Section "Branch Resampling"; the drafting of Algorithm 2), on
- * the draft model's prefix cache (kv_len slots):
+/* One drafting phase of a SpecBranch round (Section "Branch Resampling";
+ * the drafting of Algorithm 2, which marks a drafted token whose own
+ * probability is below a threshold) on the draft model's prefix cache
+ * (kv_len slots):
  *  1. the draft scores the root (d_tokens[0] on entry: the last committed
- *     token, whose KV is not yet cached); x_b is drawn from its q with
- *     d_u[0];
- *  2. sb_branch_candidates spawns B first tokens from that q by `mode`,
- *     with d_u[1 .. k_max];
+ *     token, whose KV is not yet cached) and drafts a chain: x_t (t = 1,
+ *     2, ...) is drawn from the distribution at row t - 1 with d_u[t - 1].
+ *     The branch point x_b is the first x_t with q(x_t) < confidence (both
+ *     float32), or x_trunk_max; the c = t - 1 confident drafts before it
+ *     stay as a chain in rows 1 .. c.  trunk_max = 1: x_b = x_1, c = 0;
+ *  2. sb_branch_candidates spawns B first tokens by `mode` from the
+ *     distribution x_b was drawn from, with d_u[trunk_max .. trunk_max +
+ *     k_max - 1]; they replace x_b;
  *  3. each branch continues on its own path: its depth-d token (d = 2 ..
  *     depth) is drawn by sb_draft_sample from the draft's distribution at
- *     its depth d - 1 row, with d_u[1 + k_max (d - 1) + i] for branch i;
- *     every step is one sb_verify_forward of the draft over the tree so far.
- * The tree is depth-major: row 1 + (d - 1) B + i is branch i's depth-d
- * token; its parent is row 0 at d = 1 and row - B after that.  Outputs:
- * d_tokens[1 .. B depth] (int32 [1 + k_max depth]; later entries may be
- * overwritten), d_q float32 [1 + k_max depth][vocab] (row i the
- * distribution token i was drawn from; row 0 the root's, that of x_b),
- * h_parents[0 .. B depth] (host, [1 + k_max depth]), *h_branches = B.  The
- * draft's cache slots kv_len .. kv_len + B (depth - 1) are written
- * (capacity at least kv_len + 1 + k_max depth).  d_u: float32
- * [1 + k_max depth].
- * Blocks the host once, to read B before sizing the tree.  1 <= k_max <=
- * SB_BRANCH_MAX_K, depth >= 1, 1 + k_max depth <= SB_MAX_ROWS. */
+ *     its depth d - 1 row, with d_u[trunk_max + k_max (d - 1) + i] for
+ *     branch i; every step is one sb_verify_forward of the draft over the
+ *     tree so far.
+ * Rows: 0 the root, 1 .. c the chain (parent t - 1), then the branches
+ * depth-major: row c + 1 + (d - 1) B + i is branch i's depth-d token, its
+ * parent row c at d = 1 and row - B after that.  Outputs: d_tokens[1 .. c +
+ * B depth] (int32 [trunk_max + k_max depth]; later entries may be
+ * overwritten), d_q float32 [trunk_max + k_max depth][vocab] (row i the
+ * distribution token i was drawn from; row 0 the branch position's, that of
+ * x_b), h_parents[0 .. c + B depth] (host, [trunk_max + k_max depth]),
+ * *h_branches = B, *h_chain = c.  The draft's cache slots kv_len .. are
+ * written (capacity at least kv_len + trunk_max + k_max depth).  d_u:
+ * float32 [trunk_max + k_max depth].  Blocks the host once per chain draft
+ * before the last allowed one (to read its probability) and once to read B.
+ * 1 <= k_max <= SB_BRANCH_MAX_K, depth >= 1, trunk_max >= 1, trunk_max +
+ * k_max depth <= SB_MAX_ROWS, confidence not NaN. */
 sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t k_max,
-                         int32_t mode, int32_t depth, float temperature, const float *d_u,
-                         int32_t *d_tokens, float *d_q, int32_t *h_parents, int32_t *h_branches,
-                         void *d_ws, size_t ws_bytes, hipStream_t stream);
+                         int32_t mode, int32_t depth, int32_t trunk_max, float confidence,
+                         float temperature, const float *d_u, int32_t *d_tokens, float *d_q,
+                         int32_t *h_parents, int32_t *h_branches, int32_t *h_chain, void *d_ws,
+                         size_t ws_bytes, hipStream_t stream);
 
 /* ---- measurement ---------------------------------------------------- */
 

@@ -127,10 +127,11 @@ lib.sb_draft_sample.argtypes = [_i32, _i32, _vp, _vp, _i32, C.POINTER(_i32), _f,
 lib.sb_draft_sample_workspace_bytes.restype = _sz
 lib.sb_draft_sample_workspace_bytes.argtypes = [_i32, _i32]
 lib.sb_draft_round_workspace_bytes.restype = _sz
-lib.sb_draft_round_workspace_bytes.argtypes = [_vp, _i32, _i32, _i32]
+lib.sb_draft_round_workspace_bytes.argtypes = [_vp, _i32, _i32, _i32, _i32]
 lib.sb_draft_round.restype = _i32
-lib.sb_draft_round.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _i32, _i32, _f, _vp, _vp, _vp,
-                               C.POINTER(_i32), C.POINTER(_i32), _vp, _sz, _vp]
+lib.sb_draft_round.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _i32, _i32, _i32, _f, _f, _vp,
+                               _vp, _vp, C.POINTER(_i32), C.POINTER(_i32), C.POINTER(_i32), _vp,
+                               _sz, _vp]
 lib.sb_hrad_predict.restype = _i32
 lib.sb_hrad_predict.argtypes = [_vp, _vp, _i32, _i32, _vp, C.POINTER(HradWeights), _vp, _vp,
                                 _vp, _sz, _vp]
@@ -512,34 +513,37 @@ class Model:
                                    cls.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
                                    _stream(stream)), "sb_hrad_predict")
 
-    def draft_round_workspace(self, k_max: int, depth: int, kv_len: int) -> torch.Tensor:
-        n = int(lib.sb_draft_round_workspace_bytes(self.handle, k_max, depth, kv_len))
+    def draft_round_workspace(self, k_max: int, depth: int, kv_len: int,
+                              trunk_max: int = 1) -> torch.Tensor:
+        n = int(lib.sb_draft_round_workspace_bytes(self.handle, k_max, depth, trunk_max, kv_len))
         if n == 0:
             raise ValueError("sb_draft_round_workspace_bytes: arguments rejected")
         return torch.empty(n, dtype=torch.uint8, device=self.device)
 
     def sb_draft_round(self, k: torch.Tensor, v: torch.Tensor, kv_len: int, k_max: int, mode: str,
                        depth: int, temperature: float, u: torch.Tensor, tokens: torch.Tensor,
-                       q: torch.Tensor, ws: torch.Tensor, stream=None):
-        """tokens int32 [1 + k_max*depth] with tokens[0] the root on entry;
-        q float32 [1 + k_max*depth][vocab]; u float32 [1 + k_max*depth].
-        Returns (B, parents as a numpy int32 array of 1 + B*depth entries)."""
+                       q: torch.Tensor, ws: torch.Tensor, stream=None, trunk_max: int = 1,
+                       confidence: float = float("inf")):
+        """tokens int32 [trunk_max + k_max*depth] with tokens[0] the root on
+        entry; q float32 [same][vocab]; u float32 [same].  Returns (B,
+        parents as a numpy int32 array of 1 + c + B*depth entries, c)."""
         self._check_kv(k, v)
-        R = 1 + k_max * depth
+        R = trunk_max + k_max * depth
         V = self.shape.vocab
         _need(u, R * 4, "u", torch.float32)
         _need(tokens, R * 4, "tokens", torch.int32)
         _need(q, R * V * 4, "q", torch.float32)
         par = np.zeros(R, dtype=np.int32)
-        nb = C.c_int32(0)
+        nb, nc = C.c_int32(0), C.c_int32(0)
         kv = KVCache(k.data_ptr(), v.data_ptr(), k.shape[2])
         _check(lib.sb_draft_round(self.handle, C.byref(kv), kv_len, k_max, BRANCH_MODES[mode],
-                                  depth, temperature, u.data_ptr(), tokens.data_ptr(), q.data_ptr(),
+                                  depth, trunk_max, confidence, temperature, u.data_ptr(),
+                                  tokens.data_ptr(), q.data_ptr(),
                                   par.ctypes.data_as(C.POINTER(C.c_int32)), C.byref(nb),
-                                  ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)),
-               "sb_draft_round")
-        B = int(nb.value)
-        return B, par[:1 + B * depth].copy()
+                                  C.byref(nc), ws.data_ptr(), ws.numel() * ws.element_size(),
+                                  _stream(stream)), "sb_draft_round")
+        B, c = int(nb.value), int(nc.value)
+        return B, par[:1 + c + B * depth].copy(), c
 
     def sb_kv_rollback(self, k: torch.Tensor, v: torch.Tensor, kv_len: int,
                        result: torch.Tensor, new_len: torch.Tensor, stream=None) -> None:

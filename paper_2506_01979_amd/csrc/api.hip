@@ -710,14 +710,17 @@ size_t sb_draft_sample_workspace_bytes(int32_t vocab, int32_t n) {
 }
 
 // Workspace of a draft round: the forward's, the logits and statistics of
-// the largest tree, the candidates' workspace, x_b and B.
+// the largest tree, the candidates' and the sampler's workspaces, x_b, B and
+// the drawn token's probability.
 struct RoundLayout {
   size_t fwd, logits, stats, branch, sample, ints, total;
 };
-static bool round_layout(const sb_model *m, int k_max, int depth, int kv_len, RoundLayout *o) {
-  if (!m || k_max < 1 || k_max > SB_BRANCH_MAX_K || depth < 1 || kv_len < 0) return false;
-  if (1 + (int64_t)k_max * depth > SB_MAX_ROWS) return false;
-  const int R = 1 + k_max * depth;
+static bool round_layout(const sb_model *m, int k_max, int depth, int trunk_max, int kv_len,
+                         RoundLayout *o) {
+  if (!m || k_max < 1 || k_max > SB_BRANCH_MAX_K || depth < 1 || trunk_max < 1 || kv_len < 0)
+    return false;
+  if ((int64_t)trunk_max + (int64_t)k_max * depth > SB_MAX_ROWS) return false;
+  const int R = trunk_max + k_max * depth;
   const size_t fw = sb_workspace_bytes(m, R, kv_len);
   if (!fw) return false;
   o->fwd = 0;
@@ -726,31 +729,32 @@ static bool round_layout(const sb_model *m, int k_max, int depth, int kv_len, Ro
   o->branch = o->stats + align_up((size_t)R * sizeof(sb_row_stats));
   o->sample = o->branch + align_up(sb_branch_workspace_bytes());
   o->ints = o->sample + align_up(draft_ws_bytes(m->cfg.vocab, k_max));
-  o->total = o->ints + align_up(2 * sizeof(int32_t));
+  o->total = o->ints + align_up(4 * sizeof(int32_t));
   return true;
 }
 
 size_t sb_draft_round_workspace_bytes(const sb_model *draft, int32_t k_max, int32_t depth,
-                                      int32_t kv_len) {
+                                      int32_t trunk_max, int32_t kv_len) {
   RoundLayout L;
-  return round_layout(draft, k_max, depth, kv_len, &L) ? L.total : 0;
+  return round_layout(draft, k_max, depth, trunk_max, kv_len, &L) ? L.total : 0;
 }
 
 sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t k_max,
-                         int32_t mode, int32_t depth, float temperature, const float *d_u,
-                         int32_t *d_tokens, float *d_q, int32_t *h_parents, int32_t *h_branches,
-                         void *d_ws, size_t ws_bytes, hipStream_t stream) {
+                         int32_t mode, int32_t depth, int32_t trunk_max, float confidence,
+                         float temperature, const float *d_u, int32_t *d_tokens, float *d_q,
+                         int32_t *h_parents, int32_t *h_branches, int32_t *h_chain, void *d_ws,
+                         size_t ws_bytes, hipStream_t stream) {
   if (!draft || !kv || !kv->k || !kv->v || !d_u || !d_tokens || !d_q || !h_parents ||
-      !h_branches || !d_ws)
+      !h_branches || !h_chain || !d_ws)
     return SB_ERR_INVALID_ARG;
   if (mode != SB_BRANCH_TOPK && mode != SB_BRANCH_IID && mode != SB_BRANCH_WOR)
     return SB_ERR_INVALID_ARG;
-  if (!temperature_ok(temperature) || draft->cfg.vocab > SB_BRANCH_MAX_VOCAB)
+  if (!temperature_ok(temperature) || isnan(confidence) || draft->cfg.vocab > SB_BRANCH_MAX_VOCAB)
     return SB_ERR_INVALID_ARG;
   RoundLayout L;
-  if (!round_layout(draft, k_max, depth, kv_len, &L)) return SB_ERR_INVALID_ARG;
+  if (!round_layout(draft, k_max, depth, trunk_max, kv_len, &L)) return SB_ERR_INVALID_ARG;
   if (ws_bytes < L.total) return SB_ERR_CAPACITY;
-  const int R = 1 + k_max * depth;
+  const int R = trunk_max + k_max * depth;
   if ((int64_t)kv_len + R > kv->capacity) return SB_ERR_CAPACITY;
   const int V = draft->cfg.vocab;
   char *ws = (char *)d_ws;
@@ -758,49 +762,91 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
   sb_row_stats *stats = (sb_row_stats *)(ws + L.stats);
   int32_t *xb = (int32_t *)(ws + L.ints);
   int32_t *count = xb + 1;
+  float *conf = (float *)(xb + 2);
+  void *sws = ws + L.sample;
   const size_t fws = L.logits;
+  auto sample = [&](int n_logit_rows, int n, const int32_t *src, const int32_t *dst, int n_out,
+                    const float *u, int32_t *toks, float *cf) -> sb_status {
+    DraftRows rows{};
+    rows.n = n;
+    for (int i = 0; i < n; ++i) {
+      if (src[i] < 0 || src[i] >= n_logit_rows || dst[i] < 0 || dst[i] >= n_out)
+        return SB_ERR_INVALID_ARG;
+      rows.src[i] = src[i];
+      rows.dst[i] = dst[i];
+    }
+    return hip_status(
+        launch_draft_sample(V, rows, logits, stats, temperature, u, toks, d_q, sws, stream, cf));
+  };
 
-  // 1. the root's row and x_b
+  // 1. the chain: x_t from row t - 1, until the first token below the
+  //    confidence threshold or x_trunk_max, which becomes x_b
   int32_t par[SB_MAX_ROWS];
   par[0] = -1;
-  sb_status st = sb_verify_forward(draft, kv, kv_len, d_tokens, par, 1, temperature, logits, stats,
-                                   ws, fws, stream);
-  if (st != SB_OK) return st;
-  const int32_t zero = 0;
-  void *sws = ws + L.sample;
-  const size_t swb = draft_ws_bytes(V, k_max);
-  st = sb_draft_sample(V, 1, logits, stats, 1, &zero, temperature, d_u, xb, d_q, 1, &zero, sws, swb,
-                       stream);
-  if (st != SB_OK) return st;
-  // 2. the branch-point candidates into rows 1 .. B
-  st = sb_branch_candidates(d_q, V, xb, k_max, mode, d_u + 1, count, d_tokens + 1, d_q + V,
-                            ws + L.branch, sb_branch_workspace_bytes(), stream);
+  int c = 0;
+  const int32_t *d_xb = xb;
+  for (int t = 1; t <= trunk_max; ++t) {
+    sb_status st = sb_verify_forward(draft, kv, kv_len, d_tokens, par, t, temperature, logits,
+                                     stats, ws, fws, stream);
+    if (st != SB_OK) return st;
+    const int32_t src = t - 1;
+    if (t == trunk_max) {
+      // the last allowed draft is the branch point: its row goes straight
+      // to row 0, its token to x_b
+      const int32_t zero = 0;
+      st = sample(t, 1, &src, &zero, R, d_u + (t - 1), xb, nullptr);
+      if (st != SB_OK) return st;
+      c = t - 1;
+      break;
+    }
+    const int32_t dst = t;
+    st = sample(t, 1, &src, &dst, R, d_u + (t - 1), d_tokens, conf);
+    if (st != SB_OK) return st;
+    float cf = 0.0f;
+    if (hipMemcpyAsync(&cf, conf, sizeof(cf), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+      return SB_ERR_HIP;
+    if (cf < confidence) {
+      // an unconfident draft: the branch point; its distribution to row 0
+      if (hipMemcpyAsync(d_q, d_q + (size_t)t * V, (size_t)V * sizeof(float),
+                         hipMemcpyDeviceToDevice, stream) != hipSuccess)
+        return SB_ERR_HIP;
+      d_xb = d_tokens + t;
+      c = t - 1;
+      break;
+    }
+    par[t] = t - 1;
+  }
+  // 2. the branch-point candidates into rows c + 1 .. c + B
+  sb_status st = sb_branch_candidates(d_q, V, d_xb, k_max, mode, d_u + trunk_max, count,
+                                      d_tokens + c + 1, d_q + (size_t)(c + 1) * V, ws + L.branch,
+                                      sb_branch_workspace_bytes(), stream);
   if (st != SB_OK) return st;
   int32_t B = 0;
   if (hipMemcpyAsync(&B, count, sizeof(B), hipMemcpyDeviceToHost, stream) != hipSuccess ||
       hipStreamSynchronize(stream) != hipSuccess)
     return SB_ERR_HIP;
   if (B < 0 || B > k_max) return SB_ERR_HIP;
-  for (int i = 0; i < B; ++i) par[1 + i] = 0;
+  for (int i = 0; i < B; ++i) par[c + 1 + i] = c;
   // 3. continuations, one depth per step
   int32_t src[SB_BRANCH_MAX_K], dst[SB_BRANCH_MAX_K];
   for (int d = 2; d <= depth && B > 0; ++d) {
-    const int n = 1 + (d - 1) * B;
+    const int n = 1 + c + (d - 1) * B;
     st = sb_verify_forward(draft, kv, kv_len, d_tokens, par, n, temperature, logits, stats, ws, fws,
                            stream);
     if (st != SB_OK) return st;
     for (int i = 0; i < B; ++i) {
-      src[i] = 1 + (d - 2) * B + i;
-      dst[i] = 1 + (d - 1) * B + i;
+      src[i] = c + 1 + (d - 2) * B + i;
+      dst[i] = c + 1 + (d - 1) * B + i;
       par[dst[i]] = src[i];
     }
-    st = sb_draft_sample(V, B, logits, stats, n, src, temperature, d_u + 1 + k_max * (d - 1),
-                         d_tokens, d_q, R, dst, sws, swb, stream);
+    st = sample(n, B, src, dst, R, d_u + trunk_max + k_max * (d - 1), d_tokens, nullptr);
     if (st != SB_OK) return st;
   }
-  const int n_rows = 1 + B * depth;
+  const int n_rows = 1 + c + B * depth;
   for (int i = 0; i < n_rows; ++i) h_parents[i] = par[i];
   *h_branches = B;
+  *h_chain = c;
   return SB_OK;
 }
 

@@ -946,13 +946,17 @@ __global__ __launch_bounds__(kDraftThreads) void k_draft_draw(int vocab, int nbl
                                                               int greedy, const float *__restrict__ u,
                                                               int32_t *__restrict__ tokens,
                                                               const float *__restrict__ q,
-                                                              const double *__restrict__ bsum) {
+                                                              const double *__restrict__ bsum,
+                                                              float *__restrict__ conf) {
   __shared__ double s_base, s_thr, wsum[kDraftThreads / 64];
   __shared__ int s_blk, s_tok;
   const int i = blockIdx.x;
   const int src = rows.src[i], dst = rows.dst[i];
   if (greedy) {
-    if (threadIdx.x == 0) tokens[dst] = stats[src].argmax;
+    if (threadIdx.x == 0) {
+      tokens[dst] = stats[src].argmax;
+      if (conf) conf[i] = 1.0f;
+    }
     return;
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -1054,6 +1058,7 @@ __global__ __launch_bounds__(kDraftThreads) void k_draft_draw(int vocab, int nbl
       if (y == INT_MAX) y = stats[src].argmax;
     }
     tokens[dst] = y;
+    if (conf) conf[i] = qr[y];  // the drawn token's own probability
   }
 }
 
@@ -1104,7 +1109,7 @@ size_t draft_ws_bytes(int vocab, int n) {
 
 hipError_t launch_draft_sample(int vocab, const DraftRows &rows, const float *logits,
                                const sb_row_stats *stats, float temperature, const float *u,
-                               int32_t *tokens, float *q, void *ws, hipStream_t s) {
+                               int32_t *tokens, float *q, void *ws, hipStream_t s, float *conf) {
   float inv_t;
   int greedy;
   temp_args(temperature, &inv_t, &greedy);
@@ -1115,7 +1120,7 @@ hipError_t launch_draft_sample(int vocab, const DraftRows &rows, const float *lo
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_draft_draw, dim3(rows.n), dim3(kDraftThreads), 0, s, vocab, nblk, rows,
-                     stats, greedy, u, tokens, q, (const double *)ws);
+                     stats, greedy, u, tokens, q, (const double *)ws, conf);
   return hipGetLastError();
 }
 

@@ -32,7 +32,8 @@ struct DraftRows {
 size_t draft_ws_bytes(int vocab, int n);
 hipError_t launch_draft_sample(int vocab, const DraftRows &rows, const float *logits,
                                const sb_row_stats *stats, float temperature, const float *u,
-                               int32_t *tokens, float *q, void *ws, hipStream_t s);
+                               int32_t *tokens, float *q, void *ws, hipStream_t s,
+                               float *conf = nullptr);
 
 // ---- rollback (k_rollback.hip) ---------------------------------------------
 hipError_t launch_rollback(int n_layers, int n_kv, int capacity, int head_dim, int elem_bytes,

@@ -174,25 +174,29 @@ def test_draft_host_validation_without_device(api):
     h = C.c_void_p()
     assert lib.sb_model_create(C.byref(cfg(api, n_layers=2, dtype=api.SB_BF16)), C.byref(w), C.byref(h)) == 0
     try:
-        assert lib.sb_draft_round_workspace_bytes(None, 6, 4, 100) == 0
-        assert lib.sb_draft_round_workspace_bytes(h, 0, 4, 100) == 0
-        assert lib.sb_draft_round_workspace_bytes(h, 17, 4, 100) == 0
-        assert lib.sb_draft_round_workspace_bytes(h, 16, 16, 100) == 0   # 257 rows
-        wb = lib.sb_draft_round_workspace_bytes(h, 6, 4, 100)
+        assert lib.sb_draft_round_workspace_bytes(None, 6, 4, 1, 100) == 0
+        assert lib.sb_draft_round_workspace_bytes(h, 0, 4, 1, 100) == 0
+        assert lib.sb_draft_round_workspace_bytes(h, 17, 4, 1, 100) == 0
+        assert lib.sb_draft_round_workspace_bytes(h, 6, 4, 0, 100) == 0
+        assert lib.sb_draft_round_workspace_bytes(h, 16, 16, 1, 100) == 0   # 257 rows
+        assert lib.sb_draft_round_workspace_bytes(h, 16, 15, 17, 100) == 0  # 257 rows
+        wb = lib.sb_draft_round_workspace_bytes(h, 6, 4, 1, 100)
         assert wb > 0
         kv = api.KVCache(1, 1, 128)
-        par = (C.c_int32 * 25)()
-        nb = C.c_int32(0)
+        par = (C.c_int32 * 32)()
+        nb, nc = C.c_int32(0), C.c_int32(0)
 
-        def rnd(m=h, mode=2, k_max=6, depth=4, cap=128, ws=wb, T=1.0, u=1):
+        def rnd(m=h, mode=2, k_max=6, depth=4, trunk=1, conf=0.5, cap=128, ws=wb, T=1.0, u=1):
             kv.capacity = cap
-            return lib.sb_draft_round(m, C.byref(kv), 100, k_max, mode, depth, T, u, 1, 1, par,
-                                      C.byref(nb), 1, ws, None)
+            return lib.sb_draft_round(m, C.byref(kv), 100, k_max, mode, depth, trunk, conf, T, u, 1,
+                                      1, par, C.byref(nb), C.byref(nc), 1, ws, None)
         assert rnd(m=None) == 1
         assert rnd(u=None) == 1
         assert rnd(mode=5) == 1
         assert rnd(k_max=0) == 1
         assert rnd(depth=0) == 1
+        assert rnd(trunk=0) == 1
+        assert rnd(conf=float("nan")) == 1
         assert rnd(T=-0.5) == 1
         assert rnd(ws=wb - 1) == 3
         assert rnd(cap=120) == 3                        # 100 + 25 slots needed

@@ -92,90 +92,111 @@ def test_draft_sample_matches_oracle(api, V, T, n):
     assert np.all(toks[rest] == -5) and np.all(q[rest] == 7.0)
 
 
-def gpu_round(api, shape, K, V, P, root, k_max, mode, depth, T, u):
+def gpu_round(api, shape, K, V, P, root, k_max, mode, depth, T, u, trunk=1, eps=float("inf")):
     m = model(api, shape)
-    R = 1 + k_max * depth
+    R = trunk + k_max * depth
     k, v = m.new_kv(P + R)
     if P:
         m.load_kv(k, v, K, V, P)
     toks = torch.full((R,), -5, dtype=torch.int32, device="cuda")
     toks[0] = int(root)
     q = torch.full((R, shape.vocab), 7.0, dtype=torch.float32, device="cuda")
-    ws = m.draft_round_workspace(k_max, depth, P)
-    B, par = m.sb_draft_round(k, v, P, k_max, mode, depth, T, torch.from_numpy(u).cuda(), toks, q,
-                              ws)
+    ws = m.draft_round_workspace(k_max, depth, P, trunk)
+    B, par, c = m.sb_draft_round(k, v, P, k_max, mode, depth, T, torch.from_numpy(u).cuda(), toks,
+                                 q, ws, trunk_max=trunk, confidence=eps)
     torch.cuda.synchronize()
-    return B, par, toks.cpu().numpy(), q.cpu().numpy()
+    return B, par, c, toks.cpu().numpy(), q.cpu().numpy()
 
 
-def first_tie(shape, W, K, V, P, ref, k_max, mode, depth, T, u, thr=2e-5):
-    """Row order index of the first oracle decision within thr of its
-    threshold (len(tokens) if none; 0 if the branch point itself is one)."""
+def first_tie(shape, W, K, V, P, ref, k_max, mode, depth, T, u, trunk=1, eps=float("inf"),
+              thr=2e-5):
+    """(rows, whole): the oracle's rows before its first decision within thr
+    of its threshold, and whether the branch point (B, the tree) is past
+    every such decision.  Decisions in the oracle's order: the chain's draws
+    and confidence tests, x_b's draw, B's floor(k_max (1 - q(x_b))) against
+    an integer, the candidates' draws (or top-k order), the continuations'
+    draws; at T = 0 each argmax against the runner-up."""
     lg, _, _ = decoder.tree_forward(shape, W, K, V, P, ref.tokens, ref.parents, "f64")
-    B = ref.branches
+    B, c = ref.branches, ref.chain
+    n = len(ref.tokens)
     if T == 0:
-        for r in range(len(ref.tokens)):
+        for r in range(n):
             s = np.sort(lg[r].astype(np.float64))
             if s[-1] - s[-2] < thr * max(1.0, abs(s[-1])):
-                return 0 if r == 0 else r + B
-        return len(ref.tokens)
-    if cum_margin(ref.q[0], u[0]) < thr:
-        return 0
+                kids = [j for j in range(n) if ref.parents[j] == r]
+                return (min(kids) if kids else n), r >= c + 1
+        return n, True
+    for t in range(1, c + 2):                   # chain drafts, then x_b
+        row = ref.q[t] if t <= c else ref.q[0]
+        tok = ref.tokens[t] if t <= c else ref.x_b
+        if cum_margin(row, u[t - 1]) < thr:
+            return t, False
+        if t < trunk and abs(float(row[tok]) - float(np.float32(eps))) < thr * float(np.float32(eps)):
+            return t, False
     x = k_max * (1.0 - float(ref.q[0][ref.x_b]))
     if abs(x - round(x)) < thr * k_max:
-        return 0
+        return c + 1, False
     if mode != "topk":
         rem = ref.q[0].astype(np.float64).copy()
         for i in range(B):
-            if cum_margin(rem, u[1 + i]) < thr:
-                return 1 + i
+            if cum_margin(rem, u[trunk + i]) < thr:
+                return c + 1 + i, True
             if mode == "wor":
-                rem[ref.tokens[1 + i]] = 0.0
+                rem[ref.tokens[c + 1 + i]] = 0.0
     elif B > 1:
-        s = np.sort(ref.q[0])[::-1]
-        if np.min(np.abs(np.diff(s[:B + 1]))) < thr * s[0]:
-            return 1
+        srt = np.sort(ref.q[0])[::-1]
+        if np.min(np.abs(np.diff(srt[:B + 1]))) < thr * srt[0]:
+            return c + 1, True
     for d in range(2, depth + 1):
         for i in range(B):
-            r = 1 + (d - 1) * B + i
-            if cum_margin(ref.q[r], u[1 + k_max * (d - 1) + i]) < thr:
-                return r
-    return len(ref.tokens)
+            r = c + 1 + (d - 1) * B + i
+            if cum_margin(ref.q[r], u[trunk + k_max * (d - 1) + i]) < thr:
+                return r, True
+    return n, True
 
 
 ROUND_CASES = [
-    # shape, prefix, k_max, depth, T, seed
-    ("exact", 8, 6, 4, 0.9, 1),
-    ("exact", 8, 16, 3, 1.0, 2),
-    ("tiny", 96, 6, 4, 0.8, 7),
-    ("tiny", 40, 4, 8, 1.2, 7),
-    ("tiny", 96, 6, 4, 0.8, 5),
-    ("exact", 8, 6, 5, 0.0, 5),
-    ("exact", 8, 6, 1, 0.9, 6),               # depth 1: the candidates alone
-    ("exact", 8, 1, 6, 0.9, 7),               # k_max 1: one branch, a chain
-    ("exact", 8, 16, 15, 1.0, 8),             # 241 rows, near the 256-row limit
+    # shape, prefix, k_max, depth, T, seed, trunk_max, confidence
+    ("exact", 8, 6, 4, 0.9, 1, 1, None),
+    ("exact", 8, 16, 3, 1.0, 2, 1, None),
+    ("tiny", 96, 6, 4, 0.8, 7, 1, None),
+    ("tiny", 40, 4, 8, 1.2, 7, 1, None),
+    ("tiny", 96, 6, 4, 0.8, 5, 1, None),
+    ("exact", 8, 6, 5, 0.0, 5, 1, None),
+    ("exact", 8, 6, 1, 0.9, 6, 1, None),      # depth 1: the candidates alone
+    ("exact", 8, 1, 6, 0.9, 7, 1, None),      # k_max 1: one branch, a chain
+    ("exact", 8, 16, 15, 1.0, 8, 1, None),    # 211 rows, near the 256-row limit
+    ("exact", 8, 4, 3, 0.9, 28, 6, 0.07),     # a confident chain of 3, then the fork
+    ("exact", 8, 4, 3, 0.9, 21, 6, 0.07),     # a chain of 2
+    ("exact", 8, 4, 3, 0.9, 8, 6, 0.07),      # a chain of 1
+    ("exact", 8, 4, 3, 0.9, 9, 4, 0.0),       # never below 0: the fork after trunk_max - 1
+    ("exact", 8, 4, 3, 0.0, 5, 3, 0.5),       # greedy: q(x) = 1, a chain to the end
 ]
 
 
 @pytest.mark.parametrize("mode", branching.MODES)
-@pytest.mark.parametrize("name,P,k_max,depth,T,seed", ROUND_CASES)
-def test_draft_round_matches_oracle(api, mode, name, P, k_max, depth, T, seed):
+@pytest.mark.parametrize("name,P,k_max,depth,T,seed,trunk,conf", ROUND_CASES)
+def test_draft_round_matches_oracle(api, mode, name, P, k_max, depth, T, seed, trunk, conf):
     shape = synth.SHAPES[name]
     W = weights(shape)
+    eps = float("inf") if conf is None else conf
     ptoks = synth.prefix_tokens(shape.vocab, P + 1, seed=seed)
     _, K, V = decoder.prefill(shape, W, ptoks[:-1], "f64")
-    u = synth.uniforms(drafting.uniforms_needed(k_max, depth), seed=seed)
-    ref = drafting.draft_round(shape, W, K, V, P, int(ptoks[-1]), k_max, mode, depth, T, u)
-    say(f"draft round {name} P={P} k_max={k_max} depth={depth} T={T} {mode}")
-    B, par, toks, q = gpu_round(api, shape, K, V, P, ptoks[-1], k_max, mode, depth, T, u)
-    stop = first_tie(shape, W, K, V, P, ref, k_max, mode, depth, T, u)
-    if stop == 0:
-        return                              # the branch point itself is a rounding tie
-    assert B == ref.branches
-    assert par.tolist() == ref.parents.tolist()
+    u = synth.uniforms(drafting.uniforms_needed(k_max, depth, trunk), seed=seed)
+    ref = drafting.draft_round(shape, W, K, V, P, int(ptoks[-1]), k_max, mode, depth, T, u,
+                               trunk_max=trunk, epsilon=eps)
+    say(f"draft round {name} P={P} k_max={k_max} depth={depth} T={T} {mode} trunk={trunk}")
+    B, par, c, toks, q = gpu_round(api, shape, K, V, P, ptoks[-1], k_max, mode, depth, T, u,
+                                   trunk, eps)
+    stop, whole = first_tie(shape, W, K, V, P, ref, k_max, mode, depth, T, u, trunk, eps)
     n = min(stop, len(ref.tokens))
-    assert toks[:n].tolist() == ref.tokens[:n].tolist()
-    np.testing.assert_allclose(q[:n], ref.q[:n], rtol=2e-5, atol=1e-12)
+    lo = 0 if whole else 1                     # row 0 is the branch position's row
+    assert toks[1:n].tolist() == ref.tokens[1:n].tolist()
+    np.testing.assert_allclose(q[lo:n], ref.q[lo:n], rtol=2e-5, atol=1e-12)
+    if not whole:
+        return
+    assert (B, c) == (ref.branches, ref.chain)
+    assert par.tolist() == ref.parents.tolist()
     if n == len(ref.tokens):
         assert np.all(q[n:] == 7.0)
 
@@ -198,8 +219,8 @@ def test_draft_round_properties_68m_bf16(api):
         q = torch.full((R, shape.vocab), 7.0, dtype=torch.float32, device="cuda")
         ws = m.draft_round_workspace(k_max, depth, P)
         say(f"draft round 68m bf16 {mode}")
-        B, par = m.sb_draft_round(k, v, P, k_max, mode, depth, T, torch.from_numpy(u).cuda(), toks,
-                                  q, ws)
+        B, par, _ = m.sb_draft_round(k, v, P, k_max, mode, depth, T, torch.from_numpy(u).cuda(),
+                                     toks, q, ws)
         torch.cuda.synchronize()
         tk, qq = toks.cpu().numpy(), q.cpu().numpy().astype(np.float64)
         assert 1 <= B <= k_max

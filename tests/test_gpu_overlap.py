@@ -80,7 +80,7 @@ def test_overlapped_round_equals_serial(api):
 
     say("overlap: serial round")
     verify(cur)
-    nb, _ = dm.sb_draft_round(dk, dv, P, K_MAX, "wor", DEPTH, 1.0, du, dtok, dq, dws, cur)
+    nb, _, _ = dm.sb_draft_round(dk, dv, P, K_MAX, "wor", DEPTH, 1.0, du, dtok, dq, dws, cur)
     api.sb_select_branch(logits[n - 1], stats[n - 1], 1.0, dtok[1:1 + nb], dq[1:1 + nb], su, sel,
                          sws, cur)
     torch.cuda.synchronize()
@@ -94,7 +94,7 @@ def test_overlapped_round_equals_serial(api):
         sv.wait_stream(cur)
         sd.wait_stream(cur)
         verify(sv)
-        nb2, _ = dm.sb_draft_round(dk, dv, P, K_MAX, "wor", DEPTH, 1.0, du, dtok, dq, dws, sd)
+        nb2, _, _ = dm.sb_draft_round(dk, dv, P, K_MAX, "wor", DEPTH, 1.0, du, dtok, dq, dws, sd)
         cur.wait_stream(sv)
         cur.wait_stream(sd)
         api.sb_select_branch(logits[n - 1], stats[n - 1], 1.0, dtok[1:1 + nb2], dq[1:1 + nb2], su,
