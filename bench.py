@@ -164,16 +164,17 @@ def pmc_summary(fetch_dir: str, write_dir: str) -> str:
         ""])
 
 
-def measured_traffic():
+def measured_traffic(workload: str):
     """HBM bytes per dominant launch from the committed counter summary, or
-    None when there is none or the kernel sources changed since."""
+    None when there is none, it measured another workload, or the kernel
+    sources changed since."""
     try:
         with open(TRAFFIC_FILE) as fh:
             line = [l for l in fh if l.startswith("{")][-1]
         rec = json.loads(line)
     except (OSError, IndexError, ValueError):
         return None
-    if rec.get("gemm_source_sha256") != gemm_source_sha():
+    if rec.get("gemm_source_sha256") != gemm_source_sha() or rec.get("workload") != workload:
         return None
     return rec["traffic_bytes"]
 
@@ -842,7 +843,7 @@ def main():
                    "alpha": args.alpha},
         "roofline": {"bound": "hbm", "kernel": f"k_gemm (gate/up + SwiGLU), {k_launches} launches",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.workload),
                      "avg_us": round(k_avg_ms * 1e3, 2)},
         "step_hbm": {"bytes": nbytes["step"],
                      "achieved_gbs": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9, 1),
