@@ -8,7 +8,11 @@
  * target forward; Section "Branch Resampling" keeps the surviving branch and
  * drops the others with their KV), row softmax statistics, the lossless
  * accept/resample walk (Preliminaries, "Speculative Decoding"; Appendix,
- * Algorithm 1 "Branch Speculative Sampling") and KV rollback.
+ * Algorithm 1 "Branch Speculative Sampling") and KV rollback.  Around it:
+ * H-RAD's feature tap and length predictor (Section "H-RAD") and the draft
+ * side of a round -- branch-point candidates, the draft's q rows and
+ * draws, and a whole drafting round on the draft model (Section "Branch
+ * Resampling"; Algorithm 2's drafting).
  *
  * Conventions shared by every entry point:
  *  - "d_" pointers are device pointers, "h_" pointers host pointers.  The
@@ -16,7 +20,8 @@
  *    workspace, results); the library keeps only the pointers it is given
  *    and, in sb_model_create, a small host-side model record.
  *  - Every call is asynchronous on the given HIP stream and allocates no
- *    device memory.  A model handle must not be used from two streams at
+ *    device memory (sb_draft_round alone blocks the host, to read back the
+ *    few values that shape its tree).  A model handle must not be used from two streams at
  *    once, and two calls that share a workspace must not overlap.
  *  - Errors a host can detect (null pointers, bad sizes, a malformed tree,
  *    too little KV capacity or workspace, unsupported shapes) return an
