@@ -141,11 +141,11 @@ def pmc_summary(fetch_dir: str, write_dir: str) -> str:
            "algorithmic_bytes": nb["gate_up_launch"],
            "gemm_source_sha256": gemm_source_sha()}
     cmd = ("cd /tmp && export TMPDIR=/tmp && "
-           "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <repo>/gpurun_out/pmc_fetch -o run -- "
+           "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <repo>/out/pmc_fetch -o run -- "
            "python3 <repo>/bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-alpha-sweep "
            "--no-hrad --no-draft --no-graph --copy-calibration; the same with --pmc WRITE_SIZE into "
-           "gpurun_out/pmc_write; then "
-           "python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write")
+           "out/pmc_write; then "
+           "python3 bench.py --pmc-summary out/pmc_fetch out/pmc_write")
     return "\n".join([
         f"# HBM traffic of the gate/up GEMM launch, {WORKLOAD}",
         "",
@@ -214,9 +214,9 @@ def trace_summary(trace_dir: str) -> str:
             a["us"].append(d)
     out = [f"# Kernel trace of the verify step, {WORKLOAD}", "",
            "Command: `cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
-           "--output-format csv -d <repo>/gpurun_out/prof_step -o run -- python3 <repo>/bench.py "
+           "--output-format csv -d <repo>/out/prof_step -o run -- python3 <repo>/bench.py "
            "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-draft --no-graph`, then "
-           "`python3 bench.py --trace-summary gpurun_out/prof_step`", "",
+           "`python3 bench.py --trace-summary out/prof_step`", "",
            f"Last {len(steps)} complete steps (embed .. stats, then the accept walk and the rollback "
            f"when traced): span "
            + ", ".join(f"{x:.1f}" for x in span) + " us", "",
@@ -269,9 +269,9 @@ def draft_trace_summary(trace_dir: str) -> str:
     out = ["# Kernel trace of the draft side: 68M draft round (k_max 4, depth 8, prefix 2048), "
            "branch-point candidates and draft sampler", "",
            "Command: `cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
-           "--output-format csv -d <repo>/gpurun_out/prof_draft -o run -- python3 <repo>/bench.py "
+           "--output-format csv -d <repo>/out/prof_draft -o run -- python3 <repo>/bench.py "
            "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-graph`, then "
-           "`python3 bench.py --draft-trace-summary gpurun_out/prof_draft`", "",
+           "`python3 bench.py --draft-trace-summary out/prof_draft`", "",
            f"One round ({len(wins)} rounds): kernel time {sum(busy) / len(busy):.1f} us, "
            f"span under the tracer {sum(spans) / len(spans):.1f} us", "",
            "| kernel | launches/round | us/round | avg us |", "|---|---|---|---|"]
