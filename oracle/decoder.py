@@ -26,14 +26,29 @@ prefix + path(i) would use, so each branch's rows equal a plain causal
 forward of that branch (the paper keeps the branch that survives and drops
 the others, Section "Branch Resampling", "Branch Verification").
 
+Every RMSNorm feeds a projection, and the oracle applies it in the
+factored form RMSNorm(h) g W^T = r (h g) W^T with r = 1/sqrt(mean(h^2) + eps)
+per row: the projection's input is h g, and its output is multiplied by r.
+The two forms are equal in exact arithmetic; the factored one fixes where a
+reduced-precision implementation rounds.
+
 Precision modes:
-  "f64"  everything in float64;
-  "f32"  everything in float32;
-  "bf16" float32 arithmetic with values rounded to bfloat16 (nearest even)
-         where the GPU path stores bfloat16 tensors: the normalised GEMM
-         inputs, q and k after RoPE, v, the attention output, the SwiGLU
-         product, and the KV cache.  The residual stream and logits stay
-         float32.
+  "f64"      everything in float64;
+  "f32"      everything in float32;
+  "bf16"     float32 arithmetic with values rounded to bfloat16 (nearest
+             even) at exactly these points, where the GPU path stores
+             bfloat16 tensors (the bf16 rounding-point contract):
+               1. each norm's projection input, bf16(h g);
+               2. q and k after RoPE, and v;
+               3. the attention output o = p V (the probabilities p are
+                  not rounded);
+               4. the SwiGLU product silu(gate) up;
+               and the KV cache holds the rounded k and v.  The residual
+             stream h, the row scales r, the projections' outputs and the
+             logits stay float32;
+  "bf16_f64" the same rounding points with float64 arithmetic (each rounded
+             value passes through float32 first, as a float32 value stored
+             as bfloat16 would).
 """
 from __future__ import annotations
 
@@ -54,24 +69,35 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
 
 class _Prec:
     def __init__(self, mode: str):
-        if mode not in ("f64", "f32", "bf16"):
+        if mode not in ("f64", "f32", "bf16", "bf16_f64"):
             raise ValueError(mode)
         self.mode = mode
-        self.dt = np.float64 if mode == "f64" else np.float32
+        self.dt = np.float64 if mode in ("f64", "bf16_f64") else np.float32
 
     def cast(self, x):
         return np.asarray(x, dtype=self.dt)
 
     def store(self, x):
-        """Value as the GPU path stores it (bf16 rounding in bf16 mode)."""
+        """Value as the GPU path stores it (bf16 rounding in the bf16 modes)."""
         x = np.asarray(x, dtype=self.dt)
-        return round_bf16(x) if self.mode == "bf16" else x
+        if self.mode == "bf16":
+            return round_bf16(x)
+        if self.mode == "bf16_f64":
+            return round_bf16(x.astype(np.float32)).astype(np.float64)
+        return x
 
 
 def rms_norm(x: np.ndarray, g: np.ndarray, eps: float, dt) -> np.ndarray:
     x = x.astype(dt)
     ms = np.mean(x * x, axis=-1, keepdims=True)
     return (x / np.sqrt(ms + dt(eps))) * g.astype(dt)
+
+
+def rms_scale(x: np.ndarray, eps: float, dt) -> np.ndarray:
+    """r = 1/sqrt(mean(x^2) + eps) per row, shape [rows][1]."""
+    x = x.astype(dt)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return dt(1) / np.sqrt(ms + dt(eps))
 
 
 def rope_tables(pos: np.ndarray, head_dim: int, base: float, dt):
@@ -125,10 +151,12 @@ def tree_forward(shape, weights: dict, prefix_k, prefix_v, kv_len: int, tokens, 
     v_tree = np.zeros((shape.n_layers, nkv, N, d), dtype=dt)
     for li in range(shape.n_layers):
         W = weights["layers"][li]
-        a = P.store(rms_norm(h, W["attn_norm"], eps, dt))
-        q = (a @ P.cast(W["wq"]).T).reshape(N, nh, d)
-        k = (a @ P.cast(W["wk"]).T).reshape(N, nkv, d)
-        v = (a @ P.cast(W["wv"]).T).reshape(N, nkv, d)
+        # RMSNorm(h) g1 W^T = r1 (h g1) W^T
+        r1 = rms_scale(h, eps, dt)
+        a = P.store(h * P.cast(W["attn_norm"]))
+        q = ((a @ P.cast(W["wq"]).T) * r1).reshape(N, nh, d)
+        k = ((a @ P.cast(W["wk"]).T) * r1).reshape(N, nkv, d)
+        v = ((a @ P.cast(W["wv"]).T) * r1).reshape(N, nkv, d)
         q = P.store(apply_rope(q, cos, sin))
         k = P.store(apply_rope(k, cos, sin))
         v = P.store(v)
@@ -149,15 +177,18 @@ def tree_forward(shape, weights: dict, prefix_k, prefix_v, kv_len: int, tokens, 
                 o[i, hh] = p @ V
         o = P.store(o.reshape(N, nh * d))
         h = h + o @ P.cast(W["wo"]).T
-        m = P.store(rms_norm(h, W["mlp_norm"], eps, dt))
-        gt = m @ P.cast(W["wg"]).T
-        up = m @ P.cast(W["wu"]).T
+        # RMSNorm(h) g2 W^T = r2 (h g2) W^T for the gate and up projections
+        r2 = rms_scale(h, eps, dt)
+        m = P.store(h * P.cast(W["mlp_norm"]))
+        gt = (m @ P.cast(W["wg"]).T) * r2
+        up = (m @ P.cast(W["wu"]).T) * r2
         act = P.store(silu(gt) * up)
         h = h + act @ P.cast(W["wd"]).T
         if hidden is not None:
             hidden.append(h.copy())
-    fin = P.store(rms_norm(h, weights["final_norm"], eps, dt))
-    logits = fin @ P.cast(weights["lm_head"]).T
+    rf = rms_scale(h, eps, dt)
+    fin = P.store(h * P.cast(weights["final_norm"]))
+    logits = (fin @ P.cast(weights["lm_head"]).T) * rf
     return logits, k_tree, v_tree
 
 

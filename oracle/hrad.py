@@ -14,8 +14,14 @@ and a small MLP maps them to a class
 The MLP has two hidden layers of 256 and 64 units with ReLU and a 3-way
 output layer (Appendix, "H-RAD Training"; dropout is a training-time
 device and is absent at inference).  The trained weights are not
-available: the weights are the caller's.  h^k is the residual stream after
-layer L - K + k (k = 1..K), in the order the layers run.
+available: the weights are the caller's.
+
+Which form a "hidden state of layer l" takes (the paper names the states,
+not their form): h^k, k = 1..K-1, is the residual stream after layer
+L - K + k, in the order the layers run, and the last one, h^K, is the output
+of the final RMSNorm applied to the residual after layer L.  These are the
+last K hidden states a library Llama model reports (its last entry is
+normalised), the form a predictor trained on that model's features reads.
 
 Softmax is monotone, so s_t is the argmax of the MLP's logits; ties go to
 the lowest class index.  Computed in float64.
@@ -26,6 +32,18 @@ import numpy as np
 
 HIDDEN = (256, 64)
 CLASSES = 3
+
+
+def tapped_states(hidden, final_norm, eps: float, k: int) -> list:
+    """The last k hidden states from the residual stream after every layer
+    (``hidden``, layer 0 first): the residuals after layers L-k+1..L-1, then
+    the final norm's output RMSNorm(h_L) g_f, all in float64."""
+    L = len(hidden)
+    out = [np.asarray(hidden[l], dtype=np.float64) for l in range(L - k, L - 1)]
+    h = np.asarray(hidden[-1], dtype=np.float64)
+    r = 1.0 / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps)
+    out.append(h * r * np.asarray(final_norm, dtype=np.float64))
+    return out
 
 
 def features(hidden_last_k, embed_row) -> np.ndarray:

@@ -42,7 +42,7 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
   size_t meta, rope, h, delta;
   // bf16
-  size_t xa, act, q, part_o, part_ml, xn, ss;
+  size_t xa, act, q, part_o, part_ml, xn, ss, rs;
   // f32
   size_t fa, qkv, fq, fo, gu, fact;
   size_t total;
@@ -79,6 +79,8 @@ Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
     // residual (packed) and per-(token, group) sums of squares
     L.xn = take((size_t)np * L.ks_h * 32 * 2);
     L.ss = take((size_t)np * kSsGroups * sizeof(float));
+    // 1/rms per row of the last RMSNorm kernel (its projection's scale)
+    L.rs = take((size_t)np * sizeof(float));
     L.q = take((size_t)np * qd * 2);
     L.part_o = take((size_t)c.n_kv_heads * L.n_chunks * n_rows * G * d * sizeof(float));
     L.part_ml = take((size_t)c.n_kv_heads * L.n_chunks * n_rows * G * 2 * sizeof(float));
@@ -208,6 +210,7 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   uint16_t *q = (uint16_t *)(ws + L.q);
   uint16_t *xn = (uint16_t *)(ws + L.xn);
   float *ss = (float *)(ws + L.ss);
+  float *rs = (float *)(ws + L.rs);
 
   EmbedArgs ea = embed_args(m, tokens, h, n, kv_len, meta, rope);
   SB_TRY(launch_embed_meta(ea, tree, L.np, 1, s));
@@ -263,11 +266,12 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
     uint16_t *kc = (uint16_t *)kv->k + l * layer_kv;
     uint16_t *vc = (uint16_t *)kv->v + l * layer_kv;
     SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, split ? delta : nullptr, split ? split : 1,
-                                             lw.attn_norm, H, L.ks_h, n, L.np, c.rms_eps, xa,
+                                             lw.attn_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, rs,
                                              s, tap_of(l - 1)));
     ga.W = (const uint16_t *)lw.qkv;
     ga.X = xa;
     ga.ks = gq.ks;
+    ga.rs_in = rs;
     ga.kc = kc;
     ga.vc = vc;
     SB_TIMED(SB_KC_QKV, launch_gemm(EPI_QKV, ga, gq.tiles, nullptr, s));
@@ -286,6 +290,7 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
       gn.xn = xn;
       gn.xn_ks = L.ks_h;
       gn.ss = ss;
+      gn.rs_in = nullptr;
       SB_TIMED(SB_KC_O, launch_gemm(EPI_RESID_NORM, gn, go.tiles, nullptr, s));
       ga.X = xn;
       ga.ss_in = ss;
@@ -293,25 +298,30 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
       ga.norm_dim = H;
       ga.eps = c.rms_eps;
     } else {
+      ga.rs_in = nullptr;
       SB_TIMED(SB_KC_O, launch_gemm(EPI_RESID, ga, go.tiles, &split, s));
       SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, delta, split, lw.mlp_norm, H, L.ks_h, n, L.np,
-                                               c.rms_eps, xa, s));
+                                               c.rms_eps, xa, rs, s));
       ga.X = xa;
+      ga.rs_in = rs;
     }
     ga.W = (const uint16_t *)lw.gate_up;
     ga.ks = gg.ks;
     SB_TIMED(SB_KC_GATE_UP, launch_gemm(EPI_SWIGLU, ga, gg.tiles, nullptr, s));
     ga.ss_in = nullptr;
+    ga.rs_in = nullptr;
     ga.W = (const uint16_t *)lw.down;
     ga.X = act;
     ga.ks = gd.ks;
     ga.out_rows = H;
     SB_TIMED(SB_KC_DOWN, launch_gemm(EPI_RESID, ga, gd.tiles, &split, s));
   }
+  // the last layer's H-RAD state is the final norm's output
   SB_TIMED(SB_KC_NORM, launch_rmsnorm_pack(h, split ? delta : nullptr, split ? split : 1,
-                                           m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, s,
-                                           tap_of(c.n_layers - 1)));
+                                           m->final_norm, H, L.ks_h, n, L.np, c.rms_eps, xa, rs,
+                                           s, tap_of(c.n_layers - 1), 1));
   ga.W = (const uint16_t *)m->lm_head;
+  ga.rs_in = rs;
   ga.X = xa;
   ga.ks = gl.ks;
   ga.out_rows = c.vocab;

@@ -15,11 +15,15 @@
 //   1. wave w scores steps w and w + NW: S^T = K Q^T, masked, row max into
 //      LDS;
 //   2. after a barrier, the block max M of each row gives p = exp(s - M);
-//      the wave writes its probabilities (bf16) and their row sums to LDS;
+//      the wave writes its probabilities and their row sums to LDS, each
+//      probability as two bf16 parts, hi = bf16(p) and lo = bf16(p - hi),
+//      so the matrix-core product below sees p to about 16 bits (the
+//      probabilities are not a bf16 rounding point of the forward);
 //   3. after a barrier, wave w computes the 16 dimensions 16 w .. 16 w + 15
-//      of O^T = V^T P^T over all of the workgroup's keys, reading P from LDS,
-//      and writes them: every output element is finished by one wave, so
-//      the waves never merge accumulators.
+//      of O^T = V^T P^T = V^T P_hi^T + V^T P_lo^T over all of the
+//      workgroup's keys, reading P from LDS, and writes them: every output
+//      element is finished by one wave, so the waves never merge
+//      accumulators.
 // K rows are fetched in a permuted order so that lane group lg of S^T holds
 // keys 8 lg .. 8 lg + 7, the layout P is stored and read back in.  The
 // workgroup writes an unnormalised partial (row max m, row sum l, sum p v)
@@ -101,7 +105,8 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
   constexpr int SW = 2;        // steps per wave (at most)
   constexpr int MS = SW * NW;  // steps of a workgroup (at most)
   constexpr int KW = 32 * MS;  // keys of a workgroup (at most)
-  __shared__ uint16_t sp[RB][KW + 8];  // probabilities (bf16), row-major
+  __shared__ uint16_t sp[RB][KW + 8];  // probabilities, bf16 high part, row-major
+  __shared__ uint16_t spl[RB][KW + 8]; // probabilities, bf16 low part
   __shared__ uint16_t sq[RB][D + 8];   // query rows of the block (bf16)
   __shared__ uint32_t sanc[RB][8];
   __shared__ float smax[NW][RB];
@@ -266,9 +271,16 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
           pv[j] = __builtin_amdgcn_exp2f(fmaf(sv[u][rt][j], c, -mc));  // exp2(-inf) = 0 when masked
           ps += pv[j];
         }
-        *(uint4 *)&sp[rr][32 * sl + 8 * lg] =
-            make_uint4(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
-                       pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7]));
+        uint32_t hi[4], lo[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          hi[e] = pack_bf16x2(pv[2 * e], pv[2 * e + 1]);
+          // p - bf16(p) is exact in float32
+          lo[e] = pack_bf16x2(pv[2 * e] - __uint_as_float(hi[e] << 16),
+                              pv[2 * e + 1] - __uint_as_float(hi[e] & 0xffff0000u));
+        }
+        *(uint4 *)&sp[rr][32 * sl + 8 * lg] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+        *(uint4 *)&spl[rr][32 * sl + 8 * lg] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
       }
       ps = sum_x32(sum_x16(ps));
       if (lg == 0) ssum[w][rr] = ps;
@@ -296,7 +308,9 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
           const uint4 pf = *(const uint4 *)&sp[rt * 16 + lr][32 * j + 8 * lg];
+          const uint4 pl = *(const uint4 *)&spl[rt * 16 + lr][32 * j + 8 * lg];
           oacc[rt] = mfma16(__builtin_bit_cast(bf16x8, vv), as_bf16x8(pf), oacc[rt]);
+          oacc[rt] = mfma16(__builtin_bit_cast(bf16x8, vv), as_bf16x8(pl), oacc[rt]);
         }
       }
     }

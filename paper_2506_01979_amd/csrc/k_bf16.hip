@@ -181,6 +181,14 @@ constexpr int kNormThreads = 512;
 // range of a split-K GEMM, [n_delta][n_tok][hidden]) are first summed in
 // slice order and added to the residual row, which is written back.
 //
+// The norm is applied in factored form, RMSNorm(h) g W^T = r (h g) W^T: the
+// packed output is bf16(h g), and r = 1/sqrt(mean(h^2) + eps) goes to
+// rs[t] for the projection's epilogue to multiply by.
+//
+// tap (H-RAD features, nullable): with tap_normed == 0 the residual row
+// after the delta slices are added; with tap_normed != 0 the normalised row
+// (h r) g in float32 (the last layer's state as the final norm leaves it).
+//
 // Every load of a thread (residual, all kMaxSplit delta slices, gains) is a
 // buffer load issued before the first use, so a row costs one memory round
 // trip; slices past n_delta, columns past hidden and rows past n_tok read
@@ -193,7 +201,9 @@ __global__ __launch_bounds__(kNormThreads) void k_rmsnorm_pack(float *__restrict
                                                                int hidden, int ks, int n_tok,
                                                                float eps,
                                                                uint16_t *__restrict__ out,
-                                                               float *__restrict__ tap) {
+                                                               float *__restrict__ rs,
+                                                               float *__restrict__ tap,
+                                                               int tap_normed) {
   const int t = blockIdx.x;
   __shared__ float red[kNormThreads / 64];
   const int items = ks * 4;
@@ -241,7 +251,7 @@ __global__ __launch_bounds__(kNormThreads) void k_rmsnorm_pack(float *__restrict
         f32x4 *dst = (f32x4 *)(h + (size_t)t * hidden + k0);
         dst[0] = hv[j][0];
         dst[1] = hv[j][1];
-        if (tap) {  // the residual after the previous layer, for H-RAD
+        if (tap && !tap_normed) {  // the residual after the previous layer, for H-RAD
           f32x4 *tp = (f32x4 *)(tap + (size_t)t * hidden + k0);
           tp[0] = hv[j][0];
           tp[1] = hv[j][1];
@@ -260,6 +270,7 @@ __global__ __launch_bounds__(kNormThreads) void k_rmsnorm_pack(float *__restrict
 #pragma unroll
   for (int i = 1; i < kNormThreads / 64; ++i) ss += red[i];
   const float scale = live ? 1.0f / sqrtf(ss / (float)hidden + eps) : 0.0f;
+  if (rs && threadIdx.x == 0) rs[t] = scale;  // padding rows get 0
 #pragma unroll
   for (int j = 0; j < IPT; ++j) {
     const int it = threadIdx.x + j * kNormThreads;
@@ -268,13 +279,18 @@ __global__ __launch_bounds__(kNormThreads) void k_rmsnorm_pack(float *__restrict
     // columns past hidden have zero residual and gain: they pack to zero
     uint16_t v[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = f2bf((hv[j][e >> 2][e & 3] * scale) * gv[j][e >> 2][e & 3]);
+    for (int e = 0; e < 8; ++e) v[e] = f2bf(hv[j][e >> 2][e & 3] * gv[j][e >> 2][e & 3]);
     uint4 o;
     o.x = v[0] | ((uint32_t)v[1] << 16);
     o.y = v[2] | ((uint32_t)v[3] << 16);
     o.z = v[4] | ((uint32_t)v[5] << 16);
     o.w = v[6] | ((uint32_t)v[7] << 16);
     *(uint4 *)(out + packed_index(t, k0, ks)) = o;
+    if (tap && tap_normed && live && k0 < hidden) {  // the final norm's output, float32
+      f32x4 *tp = (f32x4 *)(tap + (size_t)t * hidden + k0);
+      tp[0] = (hv[j][0] * scale) * gv[j][0];
+      tp[1] = (hv[j][1] * scale) * gv[j][1];
+    }
   }
 }
 
@@ -315,14 +331,14 @@ hipError_t launch_embed_meta(const EmbedArgs &a, const TreeArg &tree, int blocks
 
 hipError_t launch_rmsnorm_pack(float *h, const float *delta, int n_delta, const float *g,
                                int hidden, int ks, int n_tok, int n_pad, float eps, uint16_t *out,
-                               hipStream_t s, float *tap) {
+                               float *rs, hipStream_t s, float *tap, int tap_normed) {
   if (hidden % 8 != 0 || n_delta < 1 || n_delta > kMaxSplit) return hipErrorInvalidValue;
   const int ipt = (ks * 4 + kNormThreads - 1) / kNormThreads;
   switch (ipt) {
 #define SB_IPT(n)                                                                              \
   case n:                                                                                      \
     hipLaunchKernelGGL(k_rmsnorm_pack<n>, dim3(n_pad), dim3(kNormThreads), 0, s, h, delta,        \
-                       n_delta, g, hidden, ks, n_tok, eps, out, tap);                          \
+                       n_delta, g, hidden, ks, n_tok, eps, out, rs, tap, tap_normed);          \
     break;
     SB_IPT(1) SB_IPT(2) SB_IPT(3) SB_IPT(4) SB_IPT(5) SB_IPT(6) SB_IPT(7) SB_IPT(8)
 #undef SB_IPT

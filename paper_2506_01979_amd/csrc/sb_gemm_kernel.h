@@ -406,6 +406,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
                 const float r = sinv[tok];
                 v1 *= r;
                 v2 *= r;
+              } else if ((EPI == EPI_QKV || EPI == EPI_SWIGLU || EPI == EPI_LOGITS) && a.rs_in) {
+                // the RMSNorm scale of the projection's input row
+                const float r = a.rs_in[tok];
+                v1 *= r;
+                v2 *= r;
               }
               epilogue4<EPI>(a, rope, split, gb + t0 + tl, 4 * g, tok, v1, v2);
             }

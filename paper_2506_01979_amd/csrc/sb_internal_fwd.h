@@ -115,10 +115,13 @@ struct GemmArgs {
   float *ss;
   // Consumer of a RESID_NORM launch (X = its xn): every output of token t
   // is multiplied by 1 / sqrt(sum_{g < ss_groups} ss_in[t][g] / norm_dim + eps),
-  // the RMSNorm scale applied after the projection.  Null: X is normalised.
+  // the RMSNorm scale applied after the projection.
   const float *ss_in;
   int ss_groups, norm_dim;
   float eps;
+  // Otherwise, consumer of an RMSNorm kernel (X = bf16(h g)): every output
+  // of token t is multiplied by rs_in[t] = 1/rms (QKV, SWIGLU, LOGITS).
+  const float *rs_in;
 };
 
 // Row stride of the per-(token, group) sums of squares of a RESID_NORM
@@ -143,11 +146,13 @@ hipError_t launch_pack_bf16(int kind, const sb_model_config &c, const void *src0
                             const void *src2, void *dst, hipStream_t s);
 hipError_t launch_embed_meta(const EmbedArgs &a, const TreeArg &tree, int blocks, int bf16,
                              hipStream_t s);
-// tap (nullable, [n_tok][hidden] fp32): also receives the residual rows
-// after the delta slices are added
+// Packs bf16(h g) and writes r = 1/rms per row to rs (nullable); tap
+// (nullable, [n_tok][hidden] fp32) also receives the residual rows after
+// the delta slices are added, or with tap_normed the normalised rows (h r) g.
 hipError_t launch_rmsnorm_pack(float *h, const float *delta, int n_delta, const float *g,
                                int hidden, int ks, int n_tok, int n_pad, float eps, uint16_t *out,
-                               hipStream_t s, float *tap = nullptr);
+                               float *rs, hipStream_t s, float *tap = nullptr,
+                               int tap_normed = 0);
 // H-RAD (k_hrad.hip): y1 = ReLU(W1 z + b1) into ws, then the 64-unit layer,
 // the 3 logits and their argmax
 struct HradArgs {

@@ -13,19 +13,17 @@
   and 4x8.  The slices run the same kernels at the same widths, tile counts
   and vocabulary sizes as the full models.
 
-Why the whole 32-layer step has its own bound: this seeded N(0, 0.02) model
-amplifies float32-level differences through its depth.  Measured with the
-oracle alone on the 7B step: accumulating its GEMMs in float64 (then
-rounding to float32) moves the logits by 2.2e-2 (max row-relative), and
-perturbing every RMSNorm input by 6e-8 relative noise moves them by 1.6e-2.
-Two correct bf16 implementations therefore differ by about 2e-2 at this
-depth from summation order alone, so the 2e-2 bound is held per layer (the
-2-layer slices) and the full depth is held to FULL_DEPTH_TOL = 5e-2, about
-2.3 times the oracle's own summation-order spread.  The GPU path's largest
-single departure from the oracle is that it rounds the attention
-probabilities to bf16 for the matrix-core P.V product (the oracle keeps them
-float32); that alone accounts for 3.7e-2 at full depth in the same
-measurement.
+The whole-depth bound is derived, not fixed.  A bf16 forward of this seeded
+N(0, 0.02) model is sensitive to arithmetic order through its depth: a
+float32-level difference flips a few bf16 roundings, and each flip moves a
+value by 2^-9 relative.  The oracle measures that sensitivity on itself, on
+the same inputs: its bf16 contract run with float32 arithmetic (the parity
+reference, the GPU's arithmetic precision) and with float64 arithmetic
+(same rounding points) differ by `spread`.  Two correct implementations of
+the contract differ by about that much from summation order alone, so the
+GPU is held to max(2e-2, 2 * spread) at full depth and the ratio
+err / spread is reported; on the 2-layer slices the spread is far below
+2e-2 and the fixed 2e-2 applies.
 """
 import numpy as np
 import pytest
@@ -38,7 +36,6 @@ from paper_2506_01979_amd import synth
 pytestmark = pytest.mark.gpu
 
 TOL_BF16 = 2e-2
-FULL_DEPTH_TOL = 5e-2
 TIE = 1e-6
 
 
@@ -92,7 +89,7 @@ def oracle_weights(shape, bits):
             "layers": PerLayer(shape.n_layers, layer)}
 
 
-def run_case(api, m, bits, shape, prefix, B, k, seed, tol=TOL_BF16, check_walk=True):
+def run_case(api, m, bits, shape, prefix, B, k, seed, full_depth=False, check_walk=True):
     L = shape.n_layers
     kv_len = prefix - 1
     parents = synth.branch_parents(B, k)
@@ -134,7 +131,15 @@ def run_case(api, m, bits, shape, prefix, B, k, seed, tol=TOL_BF16, check_walk=T
     Vp = PerLayer(L, lambda l: synth.bits_to_f32(kv_bits[l][1]))
     ref, k_tree, v_tree = decoder.tree_forward(shape, W, Kp, Vp, kv_len, toks, parents, "bf16")
     err = row_relerr(lg, ref)
-    say(f"  logits row-relative error {err:.3e} (bound {tol:.0e})")
+    tol = TOL_BF16
+    if full_depth:
+        say(f"  oracle forward {shape.name}, float64 arithmetic (host)")
+        ref64, _, _ = decoder.tree_forward(shape, W, Kp, Vp, kv_len, toks, parents, "bf16_f64")
+        spread = row_relerr(ref, ref64)
+        tol = max(TOL_BF16, 2.0 * spread)
+        say(f"  oracle spread float32 vs float64 arithmetic {spread:.3e}; "
+            f"GPU error / spread = {err / spread:.2f}")
+    say(f"  logits row-relative error {err:.3e} (bound {tol:.2e})")
     assert err < tol
     for l in tree_k:
         ek = row_relerr(tree_k[l].reshape(-1, shape.head_dim), k_tree[l].reshape(-1, shape.head_dim))
@@ -206,7 +211,18 @@ def test_llama7b_full_step(api):
     shape = w.shape
     say("full-size 7B: generating and packing weights")
     m, bits = build(api, shape)
-    run_case(api, m, bits, shape, w.prefix, w.branches, w.depth, seed=2, tol=FULL_DEPTH_TOL)
+    run_case(api, m, bits, shape, w.prefix, w.branches, w.depth, seed=2, full_depth=True)
+
+
+@pytest.mark.timeout(1200)
+def test_llama13b_full_step(api):
+    """The whole 40-layer 13B step at B=4 x k=8, prefix 4096."""
+    w = synth.WORKLOADS["llama13b_b4k8_p4096"]
+    shape = w.shape
+    say("full-size 13B: generating and packing weights")
+    m, bits = build(api, shape)
+    run_case(api, m, bits, shape, w.prefix, w.branches, w.depth, seed=3, full_depth=True,
+             check_walk=False)
 
 
 @pytest.mark.timeout(600)

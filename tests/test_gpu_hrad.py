@@ -76,8 +76,9 @@ def test_tap_matches_oracle_hidden_states(api, sname, P, K):
     say(f"hrad tap {sname} P={P} K={K}")
     m, W, taps, hidden, n = run_forward(api, shape, P, parents, K, 40)
     got = taps.cpu().numpy()
+    states = hrad.tapped_states(hidden, W["final_norm"], shape.rms_eps, K)
     for kk in range(K):
-        want = hidden[shape.n_layers - K + kk]
+        want = states[kk]
         assert np.all(np.isfinite(got[kk, :n]))
         err = row_relerr(got[kk, :n], want)
         say(f"  tap {kk}: row-relative error {err:.3e}")

@@ -36,6 +36,24 @@ def test_hidden_states_match_library_model():
     assert relerr(fin, hs[-1]) < 1e-6
 
 
+@pytest.mark.parametrize("K", [1, 2])
+def test_tapped_states_are_the_library_models_last_hidden_states(K):
+    """The K states H-RAD reads equal the library model's last K reported
+    hidden states, whose last entry is the final norm's output."""
+    shape = GQA
+    W = synth.model_weights(shape)
+    toks = synth.prefix_tokens(shape.vocab, 10)
+    _, hidden = _chain_hidden(shape, W, toks)
+    m = hf_model(shape, W, exact_rope=True)
+    with torch.no_grad():
+        out = m(torch.tensor(np.asarray(toks, dtype=np.int64))[None], output_hidden_states=True)
+    hs = [h[0].double().numpy() for h in out.hidden_states]
+    got = hrad.tapped_states(hidden, W["final_norm"], shape.rms_eps, K)
+    assert len(got) == K
+    for kk in range(K):
+        assert relerr(got[kk], hs[len(hs) - K + kk]) < 1e-6
+
+
 def test_last_hidden_state_gives_the_logits():
     shape = synth.SHAPES["exact"]
     W = synth.model_weights(shape)

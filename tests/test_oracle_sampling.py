@@ -325,3 +325,35 @@ def test_whole_step_is_lossless():
         rhs = seq_prob([], t)
         worst = max(worst, abs(lhs - rhs))
     assert worst < 1e-9
+
+
+def test_minus_inf_logit_is_a_masked_token():
+    """A -inf logit is a token with zero probability: it carries no mass in
+    the row total, is never drawn (whatever the uniform), is never accepted
+    as a draft, and the remaining tokens keep the softmax of the finite
+    logits.  The row stays finite (no flag)."""
+    l = np.array([0.3, -np.inf, 1.2, -np.inf, -0.7, 0.0], dtype=np.float32)
+    fin = np.isfinite(l)
+    st = sampling.row_stats(l, 1.0)
+    assert not st.nonfinite
+    w = np.exp(l[fin] - np.float32(1.2)).astype(np.float64)   # fl32(exp(fl32(z - M)))
+    assert abs(st.total - w.sum()) < 1e-12
+    p = sampling.target_probs(l, 1.0, st)
+    assert np.all(p[~fin] == 0.0)
+    assert abs(p.sum() - 1.0) < 1e-12
+    ref = np.exp(l[fin].astype(np.float64)) / np.exp(l[fin].astype(np.float64)).sum()
+    assert np.max(np.abs(p[fin] - ref)) < 1e-6
+    # never drawn, over a fine grid of uniforms including both ends
+    for u in np.concatenate([np.linspace(0.0, 1.0 - 2**-24, 4097), [0.0, 1.0 - 2**-24]]):
+        assert fin[sampling.draw(p, float(u))]
+    # a draft of a masked token is never accepted (p = 0 < u for every u,
+    # and u = 0 is not < 0), and the emitted token is a finite-logit one
+    par = [-1, 0]
+    logits = np.stack([l, l])
+    q = np.full((2, 6), 1.0 / 6.0, dtype=np.float32)
+    for u1 in (0.0, 0.5, 1.0 - 2**-24):
+        r = sampling.accept_resample([0, 1], par, logits, 1.0, q, np.array([0.3, u1], np.float32))
+        assert r.n_accepted == 0 and fin[r.next_token] and r.flags == 0
+    # greedy (T = 0) ignores -inf as well
+    st0 = sampling.row_stats(l, 0.0)
+    assert st0.argmax == 2 and not st0.nonfinite
