@@ -190,6 +190,30 @@ sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
                             float temperature, float *d_logits, sb_row_stats *d_stats,
                             void *d_ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- the verify forward without a workspace argument -------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).
+ * Same computation, arguments and results as sb_verify_forward, with the
+ * workspace taken from a file-scope device array of the library of
+ * SB_NOALLOC_SCRATCH_BYTES bytes (64 MiB), one per device, allocated when
+ * the library's code is loaded on that device and held until the process
+ * ends.  The call allocates nothing: its first call on a device (with that
+ * device current) looks the array's address up once.
+ * Errors: SB_ERR_CAPACITY when the step needs more workspace than the
+ * array holds (sb_workspace_bytes(m, n_rows, kv_len) >
+ * SB_NOALLOC_SCRATCH_BYTES), before anything is enqueued; otherwise the
+ * errors of sb_verify_forward.
+ * Every call on one device shares that device's array: calls that overlap
+ * on a device (two streams, two threads) race and must be serialised by
+ * the caller.  The array keeps the last call's contents; every value the
+ * forward reads from it is written earlier in the same call. */
+#define SB_NOALLOC_SCRATCH_BYTES (64 * 1024 * 1024)
+#define SB_NOALLOC_MAX_DEVICES 64
+sb_status sb_verify_forward_noalloc(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
+                                    const int32_t *d_tokens, const int32_t *h_parents,
+                                    int32_t n_rows, float temperature, float *d_logits,
+                                    sb_row_stats *d_stats, hipStream_t stream);
+
 /* Row softmax statistics of [n_rows][vocab] float32 logits at T >= 0 (the
  * fused LM-head softmax of the verify step, callable on its own). */
 sb_status sb_softmax_stats(int32_t vocab, int32_t n_rows, const float *d_logits,

@@ -33,7 +33,7 @@ EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight"
            "sb_model_set_tap", "sb_hrad_workspace_bytes", "sb_hrad_predict",
            "sb_branch_workspace_bytes", "sb_branch_candidates", "sb_draft_sample",
            "sb_draft_sample_workspace_bytes",
-           "sb_draft_round_workspace_bytes", "sb_draft_round")
+           "sb_draft_round_workspace_bytes", "sb_draft_round", "sb_verify_forward_noalloc")
 
 SB_HRAD_H1, SB_HRAD_H2, SB_HRAD_CLASSES = 256, 64, 3
 BRANCH_MODES = {"topk": 0, "iid": 1, "wor": 2}
@@ -97,6 +97,10 @@ lib.sb_workspace_bytes.argtypes = [_vp, _i32, _i32]
 lib.sb_verify_forward.restype = _i32
 lib.sb_verify_forward.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, C.POINTER(_i32), _i32, _f,
                                   _vp, _vp, _vp, _sz, _vp]
+lib.sb_verify_forward_noalloc.restype = _i32
+lib.sb_verify_forward_noalloc.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, C.POINTER(_i32),
+                                          _i32, _f, _vp, _vp, _vp]
+SB_NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
 lib.sb_softmax_stats.restype = _i32
 lib.sb_softmax_stats.argtypes = [_i32, _i32, _vp, _f, _vp, _vp]
 lib.sb_sample_workspace_bytes.restype = _sz
@@ -466,6 +470,21 @@ class Model:
                                      len(par), temperature, logits.data_ptr(), stats.data_ptr(),
                                      ws.data_ptr(), ws.numel() * ws.element_size(),
                                      _stream(stream)), "sb_verify_forward")
+
+    def sb_verify_forward_noalloc(self, k: torch.Tensor, v: torch.Tensor, kv_len: int,
+                                  tokens: torch.Tensor, parents, temperature: float,
+                                  logits: torch.Tensor, stats: torch.Tensor, stream=None) -> None:
+        self._check_kv(k, v)
+        kv = KVCache(k.data_ptr(), v.data_ptr(), k.shape[2])
+        par, pp = _host_i32(parents)
+        n = len(par)
+        _need(tokens, n * 4, "tokens", torch.int32)
+        _need(logits, n * self.shape.vocab * 4, "logits", torch.float32)
+        _need(stats, n * 16, "stats")
+        _check(lib.sb_verify_forward_noalloc(self.handle, C.byref(kv), kv_len, tokens.data_ptr(),
+                                             pp, len(par), temperature, logits.data_ptr(),
+                                             stats.data_ptr(), _stream(stream)),
+               "sb_verify_forward_noalloc")
 
     def sb_timer_start(self, kernel_class: str, capacity: int) -> None:
         _check(lib.sb_timer_start(self.handle, KERNEL_CLASSES[kernel_class], capacity),

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -28,6 +29,13 @@ struct sb_model {
   float *tap = nullptr;
   int tap_k = 0, tap_rows = 0;
 };
+
+// Scratch memory of sb_verify_forward_noalloc: the forward's workspace as a
+// file-scope device array, one copy per device the library runs on, held
+// until the process ends.  Host code never passes this name to a kernel:
+// it is a host-side stand-in; the device address comes from
+// hipGetSymbolAddress, once per device.
+static __device__ __align__(256) char scratch[SB_NOALLOC_SCRATCH_BYTES];
 
 namespace sb {
 thread_local LaunchEvents g_launch_events;
@@ -569,6 +577,40 @@ sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
                         (char *)d_ws, L, stream);
   return forward_f32(m, kv, kv_len, d_tokens, tree, n_rows, temperature, d_logits, d_stats,
                      (char *)d_ws, L, stream);
+}
+
+// Device address of this device's scratch array, looked up once per device
+// (with that device current) and kept.
+static sb_status scratch_address(void **out) {
+  static std::mutex mu;
+  static void *addr[SB_NOALLOC_MAX_DEVICES] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SB_NOALLOC_MAX_DEVICES)
+    return SB_ERR_HIP;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SB_ERR_HIP;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return SB_OK;
+}
+
+sb_status sb_verify_forward_noalloc(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
+                                    const int32_t *d_tokens, const int32_t *h_parents,
+                                    int32_t n_rows, float temperature, float *d_logits,
+                                    sb_row_stats *d_stats, hipStream_t stream) {
+  if (!m || kv_len < 0 || n_rows < 1 || n_rows > SB_MAX_ROWS) return SB_ERR_INVALID_ARG;
+  // the step's workspace must fit the scratch array (checked before any
+  // device call)
+  if (make_layout(m->cfg, n_rows, kv_len).total > (size_t)SB_NOALLOC_SCRATCH_BYTES)
+    return SB_ERR_CAPACITY;
+  void *ws = nullptr;
+  sb_status st = scratch_address(&ws);
+  if (st != SB_OK) return st;
+  return sb_verify_forward(m, kv, kv_len, d_tokens, h_parents, n_rows, temperature, d_logits,
+                           d_stats, ws, (size_t)SB_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 sb_status sb_softmax_stats(int32_t vocab, int32_t n_rows, const float *d_logits,

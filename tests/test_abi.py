@@ -202,3 +202,25 @@ def test_draft_host_validation_without_device(api):
         assert rnd(cap=120) == 3                        # 100 + 25 slots needed
     finally:
         lib.sb_model_destroy(h)
+
+
+def test_noalloc_rejects_a_step_larger_than_its_scratch_without_device(api):
+    """sb_verify_forward_noalloc checks the step's workspace against its
+    scratch array before any device call: a 70B-shaped step of 256 rows at
+    a 60000-slot prefix needs more than 64 MiB."""
+    lib = api.lib
+    w = api.ModelWeights(1, 1, 1, (api.LayerWeights * 2)(*[api.LayerWeights(1, 1, 1, 1, 1, 1)] * 2))
+    from paper_2506_01979_amd import synth
+    c = api.make_config(synth.SHAPES["llama70b"].with_layers(2))
+    h = C.c_void_p()
+    assert lib.sb_model_create(C.byref(c), C.byref(w), C.byref(h)) == 0
+    try:
+        assert lib.sb_workspace_bytes(h, 256, 60000) > api.SB_NOALLOC_SCRATCH_BYTES
+        kv = api.KVCache(1, 1, 65536)
+        par = (C.c_int32 * 256)(*([-1] + list(range(255))))
+        assert lib.sb_verify_forward_noalloc(h, C.byref(kv), 60000, 1, par, 256, 1.0, 1, 1,
+                                             None) == 3
+        assert lib.sb_verify_forward_noalloc(None, C.byref(kv), 60000, 1, par, 256, 1.0, 1, 1,
+                                             None) == 1
+    finally:
+        lib.sb_model_destroy(h)
