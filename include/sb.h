@@ -255,6 +255,25 @@ sb_status sb_accept_resample(int32_t vocab, int32_t n_rows, const int32_t *d_tok
                              const float *d_u, sb_step_result *d_result, void *d_ws,
                              size_t ws_bytes, hipStream_t stream);
 
+/* How sb_verify_forward runs a bf16 model (the results are the same to the
+ * bf16 tolerance; float32 models always use the kernel chain):
+ *   SB_FWD_AUTO        the chain of kernels (the faster form on MI355X);
+ *   SB_FWD_KERNELS     a chain of kernels, several per layer;
+ *   SB_FWD_PERSISTENT  the persistent forward: every layer and the LM head
+ *                      in one cooperative launch of one workgroup per
+ *                      compute unit, phases separated by device-wide
+ *                      barriers; steps it does not fit return
+ *                      SB_ERR_UNSUPPORTED.
+ * A barrier of the persistent forward that does not complete within 2 s
+ * ends the launch; the step's logits are then not valid and its row
+ * statistics are NaN (SB_FLAG_NONFINITE in the walk).  New models start in
+ * SB_FWD_AUTO.  The H-RAD tap is written by the chain only: while a tap is
+ * set, SB_FWD_PERSISTENT runs the chain. */
+#define SB_FWD_AUTO 0
+#define SB_FWD_KERNELS 1
+#define SB_FWD_PERSISTENT 2
+sb_status sb_model_set_forward(sb_model *m, int32_t mode);
+
 /* KV rollback (Section "Branch Resampling": non-selected branches and their
  * KV are discarded): copies the K/V of the rows on d_result->path from slot
  * kv_len + path[j] to slot kv_len + j for j = 0..path_len-1, in ascending j,
@@ -272,12 +291,15 @@ sb_status sb_kv_rollback(const sb_model *m, const sb_kv_cache *kv, int32_t kv_le
 #define SB_HRAD_CLASSES 3
 
 /* Feature tap of H-RAD (Section "H-RAD", z_t): while set, every
- * sb_verify_forward of this model also writes the residual stream after
- * each of its last k_layers layers, float32 d_taps[k][row][hidden] with
- * k = 0 the layer n_layers - k_layers (rows of the call's tree, at most
- * max_rows of them; a call with more rows returns SB_ERR_CAPACITY).
- * d_taps = NULL clears the tap.  SB_BF16 models only (SB_ERR_DTYPE
- * otherwise); 1 <= k_layers <= n_layers. */
+ * sb_verify_forward of this model also writes its last k_layers hidden
+ * states, float32 d_taps[k][row][hidden] with k = 0 the layer
+ * n_layers - k_layers (rows of the call's tree, at most max_rows of them;
+ * a call with more rows returns SB_ERR_CAPACITY): for k < k_layers - 1 the
+ * residual stream after that layer, for the last one the final RMSNorm's
+ * output RMSNorm(h) * g_final (the last hidden state in the form a library
+ * Llama model reports it).  d_taps = NULL clears the tap.  SB_BF16 models
+ * only (SB_ERR_DTYPE otherwise); 1 <= k_layers <= n_layers.  While a tap is
+ * set the forward runs as the chain of kernels (SB_FWD_KERNELS). */
 sb_status sb_model_set_tap(sb_model *m, float *d_taps, int32_t k_layers, int32_t max_rows);
 
 /* H-RAD's MLP weights, float32 device arrays, y = W x + b per layer:
@@ -430,7 +452,8 @@ typedef enum {
   SB_KC_ATTN = 5,       /* branch-masked attention */
   SB_KC_ATTN_MERGE = 6, /* attention chunk merge */
   SB_KC_NORM = 7,       /* RMSNorm */
-  SB_KC_STATS = 8       /* softmax statistics */
+  SB_KC_STATS = 8,      /* softmax statistics */
+  SB_KC_PERSIST = 9     /* the persistent forward (every layer + LM head) */
 } sb_kernel_class;
 
 /* Starts timing one kernel class of this model: every later launch of that

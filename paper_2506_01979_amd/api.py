@@ -33,7 +33,9 @@ EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight"
            "sb_model_set_tap", "sb_hrad_workspace_bytes", "sb_hrad_predict",
            "sb_branch_workspace_bytes", "sb_branch_candidates", "sb_draft_sample",
            "sb_draft_sample_workspace_bytes",
-           "sb_draft_round_workspace_bytes", "sb_draft_round", "sb_verify_forward_noalloc")
+           "sb_draft_round_workspace_bytes", "sb_draft_round", "sb_verify_forward_noalloc",
+           "sb_model_set_forward")
+SB_FWD_AUTO, SB_FWD_KERNELS, SB_FWD_PERSISTENT = 0, 1, 2
 
 SB_HRAD_H1, SB_HRAD_H2, SB_HRAD_CLASSES = 256, 64, 3
 BRANCH_MODES = {"topk": 0, "iid": 1, "wor": 2}
@@ -41,7 +43,7 @@ SB_BRANCH_MAX_K, SB_BRANCH_MAX_VOCAB = 16, 1048576
 SB_DRAFT_MAX_ROWS = 64
 
 KERNEL_CLASSES = {"qkv": 0, "o": 1, "gate_up": 2, "down": 3, "lm_head": 4, "attn": 5,
-                  "attn_merge": 6, "norm": 7, "stats": 8}
+                  "attn_merge": 6, "norm": 7, "stats": 8, "persist": 9}
 
 
 class SBError(RuntimeError):
@@ -101,6 +103,8 @@ lib.sb_verify_forward_noalloc.restype = _i32
 lib.sb_verify_forward_noalloc.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, C.POINTER(_i32),
                                           _i32, _f, _vp, _vp, _vp]
 SB_NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
+lib.sb_model_set_forward.restype = _i32
+lib.sb_model_set_forward.argtypes = [_vp, _i32]
 lib.sb_softmax_stats.restype = _i32
 lib.sb_softmax_stats.argtypes = [_i32, _i32, _vp, _f, _vp, _vp]
 lib.sb_sample_workspace_bytes.restype = _sz
@@ -495,6 +499,9 @@ class Model:
         n = C.c_int32()
         _check(lib.sb_timer_stop(self.handle, C.byref(ms), C.byref(n)), "sb_timer_stop")
         return ms.value, n.value
+
+    def sb_model_set_forward(self, mode: int) -> None:
+        _check(lib.sb_model_set_forward(self.handle, mode), "sb_model_set_forward")
 
     def sb_model_set_tap(self, taps, k_layers: int = 0, max_rows: int = 0) -> None:
         """H-RAD feature tap: later forwards write the residual after each of

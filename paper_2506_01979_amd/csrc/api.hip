@@ -28,6 +28,7 @@ struct sb_model {
   // [tap_k][tap_rows][hidden] fp32 (null: no tap)
   float *tap = nullptr;
   int tap_k = 0, tap_rows = 0;
+  int fwd_mode = SB_FWD_AUTO;  // sb_model_set_forward
 };
 
 // Scratch memory of sb_verify_forward_noalloc: the forward's workspace as a
@@ -50,12 +51,23 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
   size_t meta, rope, h, delta;
   // bf16
-  size_t xa, act, q, part_o, part_ml, xn, ss, rs;
+  size_t xa, act, q, part_o, part_ml, xn, ss, rs, pk_table, pk_sync;
   // f32
   size_t fa, qkv, fq, fo, gu, fact;
   size_t total;
-  int np, n_chunks, ks_h, ks_o, ks_f;
+  int np, n_chunks, pk_chunks, ks_h, ks_o, ks_f;
 };
+
+// Compute units of the current device (256 when it cannot be queried: the
+// layout must not depend on a device being present).
+int device_cus_host() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return 256;
+  return cus;
+}
 
 Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
   Layout L{};
@@ -81,6 +93,9 @@ Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
     L.ks_f = pack_geom(c, SB_W_DOWN).ks;
     const int ksx = L.ks_h > L.ks_o ? L.ks_h : L.ks_o;
     L.n_chunks = attn_splits(c.n_kv_heads, c.head_dim, kv_len + n_rows);
+    // key ranges of the persistent kernel's attention (one item per unit)
+    L.pk_chunks = pk_attn_chunks(c.n_kv_heads, kv_len + n_rows, device_cus_host());
+    const int chunks = L.n_chunks > L.pk_chunks ? L.n_chunks : L.pk_chunks;
     L.xa = take((size_t)np * ksx * 32 * 2);
     L.act = take((size_t)np * L.ks_f * 32 * 2);
     // the post-attention RMSNorm fused into the O projection: gated
@@ -90,8 +105,11 @@ Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
     // 1/rms per row of the last RMSNorm kernel (its projection's scale)
     L.rs = take((size_t)np * sizeof(float));
     L.q = take((size_t)np * qd * 2);
-    L.part_o = take((size_t)c.n_kv_heads * L.n_chunks * n_rows * G * d * sizeof(float));
-    L.part_ml = take((size_t)c.n_kv_heads * L.n_chunks * n_rows * G * 2 * sizeof(float));
+    L.part_o = take((size_t)c.n_kv_heads * chunks * n_rows * G * d * sizeof(float));
+    L.part_ml = take((size_t)c.n_kv_heads * chunks * n_rows * G * 2 * sizeof(float));
+    // the persistent kernel's layer table and barrier counters
+    L.pk_table = take((size_t)c.n_layers * sizeof(PkLayer));
+    L.pk_sync = take(sizeof(PkSync));
   } else {
     L.fa = take((size_t)np * H * sizeof(float));
     L.qkv = take((size_t)np * (qd + 2 * kvd) * sizeof(float));
@@ -338,6 +356,62 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   return SB_OK;
 }
 
+// The persistent forward of a bf16 model: embedding and tree metadata, the
+// layer table, one cooperative launch for every layer and the LM head, then
+// the row statistics.
+sb_status forward_persist(sb_model *m, const sb_kv_cache *kv, int kv_len, const int32_t *tokens,
+                          const TreeArg &tree, int n, float temperature, float *logits,
+                          sb_row_stats *stats, char *ws, const Layout &L, PkArgs &a,
+                          const void *kernel, int nwg, hipStream_t s) {
+  const sb_model_config &c = m->cfg;
+  Meta *meta = (Meta *)(ws + L.meta);
+  float2 *rope = (float2 *)(ws + L.rope);
+  float *h = (float *)(ws + L.h);
+  EmbedArgs ea = embed_args(m, tokens, h, n, kv_len, meta, rope);
+  SB_TRY(launch_embed_meta(ea, tree, L.np, 1, s));
+  PkLayer *table = (PkLayer *)(ws + L.pk_table);
+  for (int l0 = 0; l0 < c.n_layers; l0 += kPkTableLayers) {
+    PkTableArgs t{};
+    t.n = c.n_layers - l0 < kPkTableLayers ? c.n_layers - l0 : kPkTableLayers;
+    for (int i = 0; i < t.n; ++i) {
+      const sb_layer_weights &lw = m->layers[l0 + i];
+      t.layer[i] = PkLayer{(const uint16_t *)lw.qkv, (const uint16_t *)lw.o,
+                           (const uint16_t *)lw.gate_up, (const uint16_t *)lw.down,
+                           lw.attn_norm, lw.mlp_norm};
+    }
+    t.dst = table + l0;
+    t.sync = l0 == 0 ? (PkSync *)(ws + L.pk_sync) : nullptr;
+    SB_TRY(launch_pk_table(t, s));
+  }
+  a.n_tok = n;
+  a.kv_len = kv_len;
+  a.cap = kv->capacity;
+  a.n_chunks = L.pk_chunks;
+  a.layers = table;
+  a.lm_head = (const uint16_t *)m->lm_head;
+  a.g_final = m->final_norm;
+  a.kc = (uint16_t *)kv->k;
+  a.vc = (uint16_t *)kv->v;
+  a.layer_kv = (size_t)c.n_kv_heads * kv->capacity * c.head_dim;
+  a.h = h;
+  a.delta = (float *)(ws + L.delta);
+  a.ss = (float *)(ws + L.ss);
+  a.part_o = (float *)(ws + L.part_o);
+  a.part_ml = (float *)(ws + L.part_ml);
+  a.logits = logits;
+  a.xa = (uint16_t *)(ws + L.xa);
+  a.xo = (uint16_t *)(ws + L.xa);  // the attention output reuses the norm's buffer
+  a.act = (uint16_t *)(ws + L.act);
+  a.q = (uint16_t *)(ws + L.q);
+  a.meta = meta;
+  a.rope = rope;
+  a.sync = (PkSync *)(ws + L.pk_sync);
+  SB_TIMED(SB_KC_PERSIST, launch_persist(a, kernel, nwg, s));
+  SB_TIMED(SB_KC_STATS, launch_softmax_stats(c.vocab, n, logits, temperature, stats, s,
+                                             &a.sync->status[0]));
+  return SB_OK;
+}
+
 sb_status forward_f32(sb_model *m, const sb_kv_cache *kv, int kv_len, const int32_t *tokens,
                       const TreeArg &tree, int n, float temperature, float *logits,
                       sb_row_stats *stats, char *ws, const Layout &L, hipStream_t s) {
@@ -394,6 +468,63 @@ sb_status forward_f32(sb_model *m, const sb_kv_cache *kv, int kv_len, const int3
 bool temperature_ok(float t) { return isfinite(t) && t >= 0.0f; }
 
 }  // namespace
+
+bool pk_plan(const sb_model_config &c, int n_tok, int nwg, PkArgs *a, const void **kernel) {
+  if (c.dtype != SB_BF16 || c.head_dim != 128 || c.n_heads % c.n_kv_heads != 0) return false;
+  if (n_tok < 1 || n_tok > 64 || nwg < 8 || nwg > kSsGroups) return false;
+  const int tt = (n_tok + 15) / 16;
+  const int G = c.n_heads / c.n_kv_heads;
+  const int rt = G == 1 ? tt : 4;  // grouped queries: 64-row attention blocks
+  // the norm phase: 8-column groups of the packed width over the units, at
+  // most 8 per unit and one thread per (row, group)
+  const int ks_h = pack_geom(c, SB_W_QKV).ks;
+  const int gpw = (ks_h * 4 + nwg - 1) / nwg;
+  if (gpw > 8 || gpw * n_tok > kPkThreadsHost) return false;
+  PkArgs p{};
+  p.n_layers = c.n_layers;
+  p.hidden = c.hidden;
+  p.n_heads = c.n_heads;
+  p.n_kv = c.n_kv_heads;
+  p.head_dim = c.head_dim;
+  p.ffn = c.ffn;
+  p.vocab = c.vocab;
+  p.eps = c.rms_eps;
+  p.scale = 1.0f / sqrtf((float)c.head_dim);
+  p.xa_ks = ks_h;
+  p.xo_ks = pack_geom(c, SB_W_O).ks;
+  p.act_ks = pack_geom(c, SB_W_DOWN).ks;
+  struct K {
+    int kind, epi;
+    PkGemmPlan *dst;
+  } kinds[] = {{SB_W_QKV, EPI_QKV, &p.qkv},
+               {SB_W_O, EPI_RESID, &p.o},
+               {SB_W_GATE_UP, EPI_SWIGLU, &p.gu},
+               {SB_W_DOWN, EPI_RESID, &p.dn},
+               {SB_W_LM_HEAD, EPI_LOGITS, &p.lm}};
+  // the planner's tiles per pass, and whether they are the special set
+  // (3 / 4 / 6 / 4 / 8 at three token tiles); otherwise the generic set
+  // 4 / 4 / 8 / 4 / 8 (passes as many as a group's tiles need)
+  static const int special[5] = {3, 4, 6, 4, 8}, generic[5] = {4, 4, 8, 4, 8};
+  bool is_special = tt == 3 && rt == 3;
+  GemmPlan gp[5];
+  for (int i = 0; i < 5; ++i) {
+    const PackGeom g = pack_geom(c, kinds[i].kind);
+    gp[i] = plan_gemm(kinds[i].epi, g.tiles, g.ks, n_tok);
+    if (gp[i].tt != tt || gp[i].split > kMaxSplit || gp[i].grid > nwg) return false;
+    if (gp[i].nt != special[i]) is_special = false;
+  }
+  for (int i = 0; i < 5; ++i) {
+    const PackGeom g = pack_geom(c, kinds[i].kind);
+    *kinds[i].dst = PkGemmPlan{g.ks, g.tiles, is_special ? special[i] : generic[i], gp[i].split,
+                               gp[i].groups};
+  }
+  const void *k = pk_kernel(tt, rt, is_special);
+  if (!k) return false;
+  *a = p;
+  *kernel = k;
+  return true;
+}
+
 }  // namespace sb
 
 using namespace sb;
@@ -510,7 +641,7 @@ void sb_model_destroy(sb_model *m) {
 }
 
 sb_status sb_timer_start(sb_model *m, int32_t kernel_class, int32_t capacity) {
-  if (!m || kernel_class < SB_KC_QKV || kernel_class > SB_KC_STATS || capacity < 1 ||
+  if (!m || kernel_class < SB_KC_QKV || kernel_class > SB_KC_PERSIST || capacity < 1 ||
       capacity > (1 << 20))
     return SB_ERR_INVALID_ARG;
   timer_release(m->timer);
@@ -572,9 +703,23 @@ sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
   const Layout L = make_layout(m->cfg, n_rows, kv_len);
   if (ws_bytes < L.total) return SB_ERR_CAPACITY;
   if (m->tap && n_rows > m->tap_rows) return SB_ERR_CAPACITY;
-  if (m->cfg.dtype == SB_BF16)
+  if (m->cfg.dtype == SB_BF16) {
+    // the persistent forward only when asked for (it measured slower than
+    // the chain: a device-wide barrier costs about what a launch does), and
+    // not with the H-RAD tap (the chain writes it)
+    if (m->fwd_mode == SB_FWD_PERSISTENT && !m->tap) {
+      PkArgs a;
+      const void *kernel = nullptr;
+      const int nwg = device_cus_host();
+      if (pk_plan(m->cfg, n_rows, nwg, &a, &kernel))
+        return forward_persist(m, kv, kv_len, d_tokens, tree, n_rows, temperature, d_logits,
+                               d_stats, (char *)d_ws, L, a, kernel, nwg, stream);
+    }
+    if (m->fwd_mode == SB_FWD_PERSISTENT) return SB_ERR_UNSUPPORTED;
     return forward_bf16(m, kv, kv_len, d_tokens, tree, n_rows, temperature, d_logits, d_stats,
                         (char *)d_ws, L, stream);
+  }
+  if (m->fwd_mode == SB_FWD_PERSISTENT) return SB_ERR_UNSUPPORTED;
   return forward_f32(m, kv, kv_len, d_tokens, tree, n_rows, temperature, d_logits, d_stats,
                      (char *)d_ws, L, stream);
 }
@@ -652,6 +797,13 @@ sb_status sb_accept_resample(int32_t vocab, int32_t n_rows, const int32_t *d_tok
   if (ws_bytes < sample_ws_bytes(vocab)) return SB_ERR_CAPACITY;
   return hip_status(launch_walk(vocab, tree, d_tokens, d_logits, d_stats, temperature, d_q, d_u,
                                 d_result, d_ws, stream));
+}
+
+sb_status sb_model_set_forward(sb_model *m, int32_t mode) {
+  if (!m || (mode != SB_FWD_AUTO && mode != SB_FWD_KERNELS && mode != SB_FWD_PERSISTENT))
+    return SB_ERR_INVALID_ARG;
+  m->fwd_mode = mode;
+  return SB_OK;
 }
 
 sb_status sb_model_set_tap(sb_model *m, float *d_taps, int32_t k_layers, int32_t max_rows) {

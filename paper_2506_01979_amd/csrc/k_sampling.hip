@@ -453,7 +453,8 @@ struct ChildCands {
 template <int NB>
 __global__ __launch_bounds__(1024) void k_softmax_stats_reg(const float *__restrict__ logits,
                                                             int vocab, float inv_t, int greedy,
-                                                            sb_row_stats *__restrict__ out) {
+                                                            sb_row_stats *__restrict__ out,
+                                                            const unsigned *invalid) {
   constexpr int NT = 1024, NW = NT / 64;
   __shared__ float smax[NW], szmax[NW];
   __shared__ int sarg[NW];
@@ -550,14 +551,16 @@ __global__ __launch_bounds__(1024) void k_softmax_stats_reg(const float *__restr
     sb_row_stats st;
     st.zmax = zmax;
     st.argmax = arg;
-    st.total = anybad ? (double)NAN : total;
+    // a producer that flagged the logits invalid makes the row non-finite
+    st.total = (anybad || (invalid && *invalid != 0u)) ? (double)NAN : total;
     out[blockIdx.x] = st;
   }
 }
 
 __global__ __launch_bounds__(1024) void k_softmax_stats(const float *__restrict__ logits,
                                                         int vocab, float inv_t, int greedy,
-                                                        sb_row_stats *__restrict__ out) {
+                                                        sb_row_stats *__restrict__ out,
+                                                            const unsigned *invalid) {
   constexpr int NT = 1024, NW = NT / 64;
   __shared__ float smax[NW], szmax[NW];
   __shared__ int sarg[NW];
@@ -673,7 +676,8 @@ __global__ __launch_bounds__(1024) void k_softmax_stats(const float *__restrict_
     sb_row_stats st;
     st.zmax = zmax;
     st.argmax = arg;
-    st.total = anybad ? (double)NAN : total;
+    // a producer that flagged the logits invalid makes the row non-finite
+    st.total = (anybad || (invalid && *invalid != 0u)) ? (double)NAN : total;
     out[blockIdx.x] = st;
   }
 }
@@ -1072,7 +1076,7 @@ static inline void temp_args(float temperature, float *inv_t, int *greedy) {
 }
 
 hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, float temperature,
-                                sb_row_stats *stats, hipStream_t s) {
+                                sb_row_stats *stats, hipStream_t s, const unsigned *invalid) {
   float inv_t;
   int greedy;
   temp_args(temperature, &inv_t, &greedy);
@@ -1081,14 +1085,14 @@ hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, floa
 #define SB_NB(k)                                                                                  \
   if (nb <= k) {                                                                                  \
     hipLaunchKernelGGL(k_softmax_stats_reg<k>, dim3(n_rows), dim3(1024), 0, s, logits, vocab,     \
-                       inv_t, greedy, stats);                                                     \
+                       inv_t, greedy, stats, invalid);                                            \
     return hipGetLastError();                                                                     \
   }
     SB_NB(1) SB_NB(2) SB_NB(4) SB_NB(8) SB_NB(16)
 #undef SB_NB
   }
   hipLaunchKernelGGL(k_softmax_stats, dim3(n_rows), dim3(1024), 0, s, logits, vocab, inv_t, greedy,
-                     stats);
+                     stats, invalid);
   return hipGetLastError();
 }
 

@@ -15,8 +15,10 @@ struct TreeArg {
 };
 
 // ---- sampling (k_sampling.hip) --------------------------------------------
+// invalid (nullable): a device word; non-zero marks every row non-finite
 hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, float temperature,
-                                sb_row_stats *stats, hipStream_t s);
+                                sb_row_stats *stats, hipStream_t s,
+                                const unsigned *invalid = nullptr);
 hipError_t launch_walk(int vocab, const TreeArg &tree, const int32_t *tokens, const float *logits,
                        const sb_row_stats *stats, float temperature, const float *q,
                        const float *u, sb_step_result *result, void *ws, hipStream_t s);

@@ -221,6 +221,70 @@ hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s);
 hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,
                                   hipStream_t s);
 
+// ---- persistent forward (k_persist.hip) ------------------------------------
+// One cooperative launch runs every layer of a bf16 verify forward: one
+// 512-thread workgroup per compute unit, the phases of a layer separated by
+// device-wide barriers, each GEMM's first weight loads issued before the
+// barrier that precedes it.
+
+// Per-layer weight pointers, read by the kernel from a device table.
+struct PkLayer {
+  const uint16_t *qkv, *o, *gu, *dn;
+  const float *g_attn, *g_mlp;
+};
+// A GEMM of the persistent forward: packed weights, k-steps, 16-row tiles,
+// tiles per pass, K split, tile groups.
+struct PkGemmPlan {
+  int ks, tiles, nt, split, groups;
+};
+// Barrier counters (one per XCD group of workgroups, 128 bytes apart) and
+// the status word (non-zero: a barrier timed out, the step is invalid).
+struct PkSync {
+  unsigned grp[8][32];
+  unsigned status[32];
+};
+struct PkArgs {
+  int n_layers, hidden, n_heads, n_kv, head_dim, ffn, vocab;
+  int n_tok, kv_len, cap;
+  float eps, scale;
+  PkGemmPlan qkv, o, gu, dn, lm;
+  int n_chunks;              // attention key ranges per KV head
+  int xa_ks, xo_ks, act_ks;  // k-steps of the packed activations
+  const PkLayer *layers;     // [n_layers] device table
+  const uint16_t *lm_head;
+  const float *g_final;
+  uint16_t *kc, *vc;         // layer 0 of the caches
+  size_t layer_kv;           // elements per layer of one cache
+  float *h, *delta, *ss, *part_o, *part_ml, *logits;
+  uint16_t *xa, *xo, *act, *q;
+  const Meta *meta;
+  const float2 *rope;
+  PkSync *sync;
+};
+// Layers whose table one k_pk_table launch writes (kernel arguments hold
+// their pointers).
+constexpr int kPkTableLayers = 64;
+struct PkTableArgs {
+  PkLayer layer[kPkTableLayers];
+  PkLayer *dst;
+  int n;
+  PkSync *sync;  // zeroed by the first launch (nullptr for the others)
+};
+// Threads of a persistent workgroup; 32-key steps of an attention item.
+constexpr int kPkThreadsHost = 512;
+constexpr int kPkAttnMaxSteps = 16;
+// Key ranges per KV head of the persistent attention phase (about one work
+// item per workgroup, at most kPkAttnMaxSteps steps of 32 keys each).
+int pk_attn_chunks(int n_kv, int nkeys, int nwg);
+// Whether the persistent kernel runs this step, with its GEMM plans and
+// kernel (nwg: workgroups = compute units).
+bool pk_plan(const sb_model_config &c, int n_tok, int nwg, PkArgs *a, const void **kernel);
+// Kernel of a signature: tt token tiles, rt query tiles per attention
+// block, special = the 7B-shaped tiles per pass (null: not built).
+const void *pk_kernel(int tt, int rt, bool special);
+hipError_t launch_pk_table(const PkTableArgs &t, hipStream_t s);
+hipError_t launch_persist(const PkArgs &a, const void *kernel, int grid, hipStream_t s);
+
 // k_f32.hip
 hipError_t launch_f32_rmsnorm(const float *h, const float *g, int hidden, int n_tok, float eps,
                               float *out, hipStream_t s);
