@@ -658,13 +658,14 @@ def main():
     # depth k (a near-flat q at the branch point gives the verify step's B),
     # then the branch-point candidates and the draft sampler on their own.
     # Not part of `value`.
-    draft_out = overlap_out = spec_out = None
+    draft_out = round_out = None
     if not args.no_draft:
         dshape = synth.SHAPES["draft68m"]
         dm = api.Model(dshape, api.synth_tensors(dshape, seed=1), device=dev)
         DK, DD = B, kd
         R = 1 + DK * DD
-        dk_, dv_ = dm.new_kv(kv_len + R + 8)
+        TRUNK = 4
+        dk_, dv_ = dm.new_kv(kv_len + max(R, TRUNK + (B + 1) * DD) + 8)
         fill_prefix(dshape, dk_, dv_)
         du = torch.from_numpy(synth.uniforms(R, 31)).to(dev)
         dtok = torch.full((R,), root, dtype=torch.int32, device=dev)
@@ -721,83 +722,100 @@ def main():
         dsws = torch.empty(api.sb_draft_sample_workspace_bytes(V, B), dtype=torch.uint8, device=dev)
         samp_us = graph_us(lambda st: api.sb_draft_sample(logits, stats, src, 1.0, du, dtok, dq, dst,
                                                           dsws, st))
-        # One whole round on the draft's own output: the 7B target verifies
-        # the draft's tree with the q rows its tokens were drawn from, then
-        # the walk and the rollback (random weights on both sides, so few
-        # drafts are accepted; the mechanics and the time are the point).
-        rtok = torch.empty(R, dtype=torch.int32, device=dev)
-        rq = torch.empty((R, V), dtype=torch.float32, device=dev)
-
-        def spec_round():
-            nb, par_d, _ = dm.sb_draft_round(dk_, dv_, kv_len, DK, "wor", DD, 1.0, du, rtok, rq, dws,
-                                          stream)
-            m.sb_verify_forward(k_, v_, kv_len, rtok, par_d, 1.0, logits, stats, ws, stream)
-            api.sb_accept_resample(rtok, par_d, logits, stats, 1.0, rq, d_u, res, sws, stream)
-            m.sb_kv_rollback(k_, v_, kv_len, res, new_len, stream)
-            return nb, par_d
-        rtok[0] = root
-        for _ in range(2):
-            spec_round()
-        torch.cuda.synchronize()
-        committed = []
-        ev0.record(stream)
-        for _ in range(reps):
-            nb_r, par_r = spec_round()
-        ev1.record(stream)
-        torch.cuda.synchronize()
-        spec_ms = ev0.elapsed_time(ev1) / reps
-        rr = api.decode_result(res)
-        spec_out = {"round_ms": round(spec_ms, 4), "tree_rows": int(len(par_r)), "branches": nb_r,
-                    "committed": rr["n_accepted"] + 1, "kept_branch": rr["branch"]}
-
-        # Algorithm 2's overlap on one GPU: the target's verify step on one
-        # stream while the draft builds the next round's branches on another
-        # (default priorities), then Algorithm 1 over the branches' first
-        # tokens at the verified tree's first leaf row.  Serial first, then
-        # overlapped; the results must not change.
+        # One whole round of Algorithm 2 (sb_spec_round): the 68M draft
+        # drafts a chain (confidence threshold 0: always trunk_max - 1 = 3
+        # drafts, a length independent of the drafted values), the target
+        # verifies that chain on one stream while the draft spawns B + 1
+        # candidates' worth of branches at x_b (k_max = B + 1 gives B
+        # branches at a near-flat q) and extends them to depth k on another;
+        # then Algorithm 1 at the chain's last row and both rollbacks.  Timed
+        # on one stream and on two (default priorities); the results must
+        # not change.  Random weights on both sides, so the mechanics and
+        # the time are the point, not the acceptance.
+        RK = B + 1
+        rparams = api.round_params(RK, "wor", DD, TRUNK, 0.0, 1.0)
+        rbuf = api.RoundBuffers(m, dm, rparams, kv_len, kv_len, dev)
+        RR = TRUNK + RK * DD
+        r_ud = torch.from_numpy(synth.uniforms(RR, 51)).to(dev)
+        r_uw = torch.from_numpy(synth.uniforms(TRUNK + 1, 52)).to(dev)
+        r_us = torch.from_numpy(synth.uniforms(RK + 1, 53)).to(dev)
+        rbuf.tokens[0] = root
         sv, sd = torch.cuda.Stream(), torch.cuda.Stream()
-        sel_out = torch.empty(3, dtype=torch.int32, device=dev)
-        su = torch.from_numpy(synth.uniforms(DK + 1, 41)).to(dev)
-        leaf = n - 1
 
-        def select(st):
-            api.sb_select_branch(logits[leaf], stats[leaf], 1.0, dtok[1:1 + bd], dq[1:1 + bd], su,
-                                 sel_out, sws_sel, st)
-        sws_sel = torch.empty(api.sb_sample_workspace_bytes(V), dtype=torch.uint8, device=dev)
-
-        def serial():
-            step(stream)
-            draft_round()
-            select(stream)
-
-        def overlapped():
-            sv.wait_stream(stream)
-            sd.wait_stream(stream)
-            step(sv)
-            dm.sb_draft_round(dk_, dv_, kv_len, DK, "wor", DD, 1.0, du, dtok, dq, dws, sd)
-            stream.wait_stream(sv)
-            stream.wait_stream(sd)
-            select(stream)
-        times = {}
-        outs = {}
-        for name, fn in (("serial", serial), ("overlapped", overlapped)):
+        def round_on(vs, ds):
+            vs.wait_stream(stream)
+            ds.wait_stream(stream)
+            got = api.sb_spec_round(m, k_, v_, kv_len, dm, dk_, dv_, kv_len, r_ud, r_uw, r_us, rbuf,
+                                    vs, ds)
+            stream.wait_stream(vs)
+            return got
+        times, outs = {}, {}
+        for name, (vs, ds) in (("serial", (stream, stream)), ("overlapped", (sv, sd))):
             for _ in range(2):
-                fn()
+                round_on(vs, ds)
             torch.cuda.synchronize()
             ev0.record(stream)
             for _ in range(reps):
-                fn()
+                rc, rb, rpar = round_on(vs, ds)
             ev1.record(stream)
             torch.cuda.synchronize()
             times[name] = ev0.elapsed_time(ev1) / reps
-            outs[name] = (api.decode_result(res), sel_out.cpu().tolist(), dtok.cpu().tolist())
+            outs[name] = (api.decode_round(rbuf.round), api.decode_result(rbuf.walk),
+                          rbuf.tokens.cpu().tolist(), rbuf.new_lens.cpu().tolist())
         if outs["serial"] != outs["overlapped"]:
-            raise RuntimeError("the overlapped round changed a result")
-        overlap_out = {"verify_ms": round(ms_per_step, 4), "draft_round_ms": round(round_ms, 4),
-                       "serial_ms": round(times["serial"], 4),
-                       "overlapped_ms": round(times["overlapped"], 4),
-                       "hidden_frac_of_draft": round((times["serial"] - times["overlapped"])
-                                                     / round_ms, 3)}
+            raise RuntimeError("the two-stream round changed a result")
+        # the target's part alone: the chain's forward and its walk
+        cpar = list(range(-1, rc))
+
+        def verify_chain():
+            m.sb_verify_forward(k_, v_, kv_len, rbuf.tokens, cpar, 1.0, rbuf.logits, rbuf.stats, ws,
+                                stream)
+            api.sb_accept_resample(rbuf.tokens, cpar, rbuf.logits, rbuf.stats, 1.0, rbuf.q, r_uw,
+                                   rbuf.walk, sws, stream)
+        verify_chain()
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(reps):
+            verify_chain()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        vc_ms = ev0.elapsed_time(ev1) / reps
+        # the draft's part alone: the chain, then the branches
+        dws_r = dm.draft_round_workspace(RK, DD, kv_len, TRUNK)
+        xb_r = torch.empty(1, dtype=torch.int32, device=dev)
+
+        def draft_part(with_branches):
+            c_ = dm.sb_draft_chain(dk_, dv_, kv_len, TRUNK, 0.0, 1.0, r_ud, rbuf.tokens, rbuf.q, xb_r,
+                                   dws_r, stream)
+            if with_branches:
+                dm.sb_draft_branches(dk_, dv_, kv_len, c_, xb_r, RK, "wor", DD, 1.0, r_ud[TRUNK:],
+                                     rbuf.tokens, rbuf.q, dws_r, stream)
+        part_ms = {}
+        for wb in (False, True):
+            draft_part(wb)
+            torch.cuda.synchronize()
+            ev0.record(stream)
+            for _ in range(reps):
+                draft_part(wb)
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            part_ms[wb] = ev0.elapsed_time(ev1) / reps
+        br_ms = part_ms[True] - part_ms[False]
+        ro = outs["serial"][0]
+        saved = times["serial"] - times["overlapped"]
+        round_out = {"trunk_max": TRUNK, "confidence": 0.0, "k_max": RK, "depth": DD,
+                     "mode": "wor", "chain": rc, "branches": rb, "draft_rows": int(len(rpar)),
+                     "n_trunk": ro["n_trunk"], "kept": ro["kept"],
+                     "committed": ro["n_trunk"] + 1,
+                     "serial_ms": round(times["serial"], 4),
+                     "overlapped_ms": round(times["overlapped"], 4),
+                     "verify_chain_ms": round(vc_ms, 4),
+                     "draft_chain_ms": round(part_ms[False], 4),
+                     "draft_branches_ms": round(br_ms, 4),
+                     "saved_ms": round(saved, 4),
+                     # the most two streams can save is the shorter of the
+                     # two concurrent parts
+                     "hidden_frac": round(saved / min(vc_ms, br_ms), 3)}
         draft_out = {"shape": f"{dshape.name}: {dshape.n_layers} layers, hidden {dshape.hidden}, "
                               f"{dshape.n_heads}x{dshape.head_dim} heads, ffn {dshape.ffn}, "
                               f"vocab {V}, bf16",
@@ -856,8 +874,7 @@ def main():
         out["hrad"] = hrad_out
     if draft_out is not None:
         out["draft"] = draft_out
-        out["overlap"] = overlap_out
-        out["spec_round"] = spec_out
+        out["overlap"] = round_out
 
     if not args.no_alpha_sweep:
         sweep = {}

@@ -141,6 +141,17 @@ typedef struct {
   int32_t path[SB_MAX_ROWS]; /* rows root .. last accepted, by depth */
 } sb_step_result;
 
+/* Outcome of one SpecBranch round (sb_round_finish, device-resident). */
+typedef struct {
+  int32_t n_trunk;   /* accepted trunk drafts (0 .. chain) */
+  int32_t kept;      /* kept branch (candidate index), or -1 */
+  int32_t token;     /* the committed token after the accepted trunk: the
+                        kept candidate, or a residual draw */
+  int32_t flags;     /* SB_FLAG_* of the walk and the selection */
+  int32_t draft_len; /* rows of the draft tree the draft cache keeps */
+  int32_t reserved[3];
+} sb_round_result;
+
 typedef struct sb_model sb_model;
 
 const char *sb_status_string(sb_status s);
@@ -439,6 +450,115 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
                          float temperature, const float *d_u, int32_t *d_tokens, float *d_q,
                          int32_t *h_parents, int32_t *h_branches, int32_t *h_chain, void *d_ws,
                          size_t ws_bytes, hipStream_t stream);
+
+/* The two phases of sb_draft_round as separate calls, so that the target
+ * can verify the chain while the draft spawns the branches (Algorithm 2:
+ * the DRAFTING phase drafts the chain; in the VERIFICATION phase the draft
+ * branches at x_b while the target verifies the chain).
+ * sb_draft_chain: step 1 of sb_draft_round -- d_tokens[0] the root on entry;
+ *   rows 1 .. c of d_tokens / d_q the confident chain, row 0 of d_q the
+ *   distribution x_b was drawn from, *d_xb (device int32) = x_b,
+ *   *h_chain = c; d_u float32 [trunk_max]; d_tokens and d_q have at least
+ *   trunk_max + 1 rows; d_ws of sb_draft_round_workspace_bytes(draft, 1, 1,
+ *   trunk_max, kv_len) bytes.  Blocks the host once per chain draft before
+ *   the last allowed one.
+ * sb_draft_branches: steps 2 and 3 of sb_draft_round after a chain of
+ *   `chain` rows (rows 0 .. chain of d_tokens, row 0 of d_q as
+ *   sb_draft_chain leaves them, d_xb): the candidates into rows chain + 1
+ *   .. chain + B, the continuations depth-major after them; d_u float32
+ *   [k_max depth] (candidates first, then one per branch per depth, as
+ *   d_u + trunk_max of sb_draft_round); h_parents[0 .. chain + B depth],
+ *   *h_branches = B; d_ws of sb_draft_round_workspace_bytes(draft, k_max,
+ *   depth, chain + 1, kv_len) bytes.  Blocks the host once, to read B.
+ * The draft's cache slots kv_len .. are written by both, as sb_draft_round
+ * writes them.  Errors as sb_draft_round. */
+sb_status sb_draft_chain(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t trunk_max,
+                         float confidence, float temperature, const float *d_u, int32_t *d_tokens,
+                         float *d_q, int32_t *d_xb, int32_t *h_chain, void *d_ws, size_t ws_bytes,
+                         hipStream_t stream);
+sb_status sb_draft_branches(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t chain,
+                            const int32_t *d_xb, int32_t k_max, int32_t mode, int32_t depth,
+                            float temperature, const float *d_u, int32_t *d_tokens, float *d_q,
+                            int32_t *h_parents, int32_t *h_branches, void *d_ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* The end of one SpecBranch round (Algorithm 2, verification phase;
+ * Section "Branch Resampling", "Branch Verification").  The round verified
+ * the chain [root, x_1 .. x_chain] with the target (d_walk: its
+ * sb_accept_resample result over that chain) and, when the whole chain is
+ * accepted, tests the `branches` candidates with Algorithm 1 at the chain's
+ * last row (d_select: sb_select_branch's {candidate or -1, token, flags};
+ * may be NULL when branches = 0).  Writes d_round: n_trunk = accepted
+ * chain drafts; with a rejection inside the chain, token = the walk's
+ * residual draw and kept = -1 (the branches are discarded); with the whole
+ * chain accepted, no bonus token is drawn: kept / token are Algorithm 1's
+ * (with no candidates, the token is the walk's draw from p at the last
+ * row).  d_draft_path: an sb_step_result whose path is the draft tree's
+ * kept rows -- the root, the accepted chain rows and, with a kept branch,
+ * that branch's rows at depths 1 .. depth - 1 (the ones the draft's cache
+ * holds KV for) -- for sb_kv_rollback of the draft's cache.  The target's
+ * cache is rolled back with d_walk itself.  0 <= chain, 0 <= branches,
+ * depth >= 1, 1 + chain + branches depth <= SB_MAX_ROWS. */
+sb_status sb_round_finish(int32_t chain, int32_t branches, int32_t depth,
+                          const sb_step_result *d_walk, const int32_t *d_select,
+                          sb_round_result *d_round, sb_step_result *d_draft_path,
+                          hipStream_t stream);
+
+/* ---- one whole SpecBranch round on two streams ------------------------ */
+
+/* Parameters of a round: the drafting phase's (sb_draft_round's k_max,
+ * mode, depth, trunk_max, confidence) and the temperature T >= 0 of both
+ * models' distributions. */
+typedef struct {
+  int32_t k_max, mode, depth, trunk_max;
+  float confidence, temperature;
+} sb_round_params;
+
+/* Workspace bytes of sb_spec_round (0 for arguments it rejects). */
+size_t sb_spec_round_workspace_bytes(const sb_model *target, const sb_model *draft,
+                                     const sb_round_params *p, int32_t t_len, int32_t d_len);
+
+/* One round of Algorithm 2 (a drafting phase, then the verification phase
+ * that consumes it; Section "Branch Resampling", "Branch Verification"):
+ *  1. on draft_stream, sb_draft_chain: the draft scores the root
+ *     (d_tokens[0] on entry, the last committed token, cached by neither
+ *     model) on its cache (d_len slots) and drafts the confident chain
+ *     x_1 .. x_c and the branch point x_b;
+ *  2. on verify_stream, once the chain is drafted: the target's
+ *     sb_verify_forward over [root, x_1 .. x_c] (rows 0 .. c of d_logits /
+ *     d_stats) and sb_accept_resample over that chain (d_walk; uniforms
+ *     d_u_walk[0 .. c]); meanwhile, on draft_stream, sb_draft_branches
+ *     spawns the candidates at x_b and extends them (d_u_draft +
+ *     trunk_max);
+ *  3. on verify_stream, once both are done: sb_select_branch at row c over
+ *     the candidates (d_select; uniforms d_u_sel[0 .. B]), sb_round_finish
+ *     (d_round), and the rollbacks of the target's cache (with d_walk) and
+ *     of the draft's cache (the rows sb_round_finish keeps); d_new_lens =
+ *     {target's new length, draft's new length}.
+ * Buffers: d_u_draft float32 [trunk_max + k_max depth]; d_u_walk float32
+ * [trunk_max + 1]; d_u_sel float32 [k_max + 1]; d_tokens int32 and d_q
+ * float32 [trunk_max + k_max depth]([vocab]) as sb_draft_round fills them;
+ * d_logits float32 [trunk_max][vocab]; d_stats [trunk_max]; d_walk one
+ * sb_step_result; d_select int32 [3] (written when B > 0); d_round one
+ * sb_round_result; d_new_lens int32 [2]; h_parents host int32
+ * [trunk_max + k_max depth] (the draft tree, 1 + c + B depth entries);
+ * *h_chain = c, *h_branches = B; d_ws of sb_spec_round_workspace_bytes.
+ * Needs t_len + trunk_max <= the target cache's capacity and d_len +
+ * trunk_max + k_max depth <= the draft cache's; both models share the
+ * vocabulary and are distinct objects.  The two streams may be the same
+ * stream (a serial round, same results bit for bit).  Blocks the host as
+ * sb_draft_chain and sb_draft_branches do.  On return every part of the
+ * round is ordered before verify_stream's later work; draft_stream holds
+ * none of it.  Errors as the calls it makes. */
+sb_status sb_spec_round(sb_model *target, const sb_kv_cache *t_kv, int32_t t_len, sb_model *draft,
+                        const sb_kv_cache *d_kv, int32_t d_len, const sb_round_params *p,
+                        const float *d_u_draft, const float *d_u_walk, const float *d_u_sel,
+                        int32_t *d_tokens, float *d_q, float *d_logits, sb_row_stats *d_stats,
+                        sb_step_result *d_walk, int32_t *d_select, sb_round_result *d_round,
+                        int32_t *d_new_lens, int32_t *h_parents, int32_t *h_chain,
+                        int32_t *h_branches, void *d_ws, size_t ws_bytes,
+                        hipStream_t verify_stream, hipStream_t draft_stream);
+
 
 /* ---- measurement ---------------------------------------------------- */
 

@@ -18,6 +18,9 @@ MI355X path computes, written from the paper:
 * ``oracle.drafting`` -- the draft side of a round: the draft's float32 q
   rows and their draws, and a drafting phase with a branch point after the
   root (Section "Branch Resampling") on the same decoder definition;
+* ``oracle.spec_round`` -- one whole round of Algorithm 2: the drafting
+  phase, the target's chain test over the confident drafts, Algorithm 1 at
+  the branch point when the chain is accepted, and both caches rolled back;
 * ``oracle.hrad``     -- H-RAD's length predictor (Section "H-RAD"): the
   last K layers' hidden states and the new token's embedding through a
   256/64/3 ReLU MLP, s_t = argmax.
@@ -32,4 +35,4 @@ output distribution, closed forms printed in the paper, hand-worked golden
 cases).  Nothing here is "parity unpinned".
 """
 
-from . import tree, decoder, sampling, rollback, hrad, branching, drafting  # noqa: F401
+from . import tree, decoder, sampling, rollback, hrad, branching, drafting, spec_round  # noqa: F401

@@ -41,10 +41,11 @@ import numpy as np
 from . import branching, decoder, sampling
 
 
-def sample(logits_row, T: float, u: float):
-    """(q float32 [V], token)."""
+def sample(logits_row, T: float, u: float, trace: list | None = None, u_index: int = 0):
+    """(q float32 [V], token).  With `trace`, the draw is recorded as
+    sampling.draw records it, under uniform index u_index."""
     q = sampling.target_probs(np.asarray(logits_row, dtype=np.float32), T).astype(np.float32)
-    return q, sampling.draw(q.astype(np.float64), float(u))
+    return q, sampling.draw(q.astype(np.float64), float(u), trace, u_index)
 
 
 @dataclass
@@ -63,7 +64,10 @@ def uniforms_needed(k_max: int, depth: int, trunk_max: int = 1) -> int:
 
 def draft_round(shape, weights: dict, prefix_k, prefix_v, kv_len: int, root_token: int,
                 k_max: int, mode: str, depth: int, T: float, u, prec: str = "f64",
-                trunk_max: int = 1, epsilon: float = float("inf")) -> DraftRound:
+                trunk_max: int = 1, epsilon: float = float("inf"),
+                trace: list | None = None) -> DraftRound:
+    """With `trace`, every draw is recorded (sampling.draw's events) under
+    the index of its uniform in u."""
     u = np.asarray(u, dtype=np.float32)
     assert depth >= 1 and trunk_max >= 1
     assert len(u) >= uniforms_needed(k_max, depth, trunk_max)
@@ -74,7 +78,7 @@ def draft_round(shape, weights: dict, prefix_k, prefix_v, kv_len: int, root_toke
     for t in range(1, trunk_max + 1):
         lg, _, _ = decoder.tree_forward(shape, weights, prefix_k, prefix_v, kv_len, toks, parents,
                                         prec)
-        q_t, x_t = sample(lg[t - 1], T, u[t - 1])
+        q_t, x_t = sample(lg[t - 1], T, u[t - 1], trace, t - 1)
         if t == trunk_max or q_t[x_t] < eps:
             q_b, x_b = q_t, x_t
             break
@@ -84,7 +88,10 @@ def draft_round(shape, weights: dict, prefix_k, prefix_v, kv_len: int, root_toke
     c = len(toks) - 1
     q[0] = q_b
     u0 = trunk_max
-    cand, rows = branching.candidates(q_b, x_b, k_max, mode, u[u0:u0 + k_max])
+    sub = [] if trace is not None else None
+    cand, rows = branching.candidates(q_b, x_b, k_max, mode, u[u0:u0 + k_max], sub)
+    if trace is not None:
+        trace += [(ev[0], u0 + ev[1]) + tuple(ev[2:]) for ev in sub]
     B = len(cand)
     q += list(rows)
     toks += [int(t) for t in cand]
@@ -94,7 +101,8 @@ def draft_round(shape, weights: dict, prefix_k, prefix_v, kv_len: int, root_toke
                                         prec)
         for i in range(B):
             r = c + 1 + (d - 2) * B + i
-            qi, t = sample(lg[r], T, u[u0 + k_max * (d - 1) + i])
+            ui = u0 + k_max * (d - 1) + i
+            qi, t = sample(lg[r], T, u[ui], trace, ui)
             toks.append(t)
             parents.append(r)
             q.append(qi)

@@ -34,7 +34,8 @@ EXPORTS = ("sb_status_string", "sb_version", "sb_packed_bytes", "sb_pack_weight"
            "sb_branch_workspace_bytes", "sb_branch_candidates", "sb_draft_sample",
            "sb_draft_sample_workspace_bytes",
            "sb_draft_round_workspace_bytes", "sb_draft_round", "sb_verify_forward_noalloc",
-           "sb_model_set_forward")
+           "sb_model_set_forward", "sb_draft_chain", "sb_draft_branches", "sb_round_finish",
+           "sb_spec_round_workspace_bytes", "sb_spec_round")
 SB_FWD_AUTO, SB_FWD_KERNELS, SB_FWD_PERSISTENT = 0, 1, 2
 
 SB_HRAD_H1, SB_HRAD_H2, SB_HRAD_CLASSES = 256, 64, 3
@@ -79,6 +80,12 @@ class HradWeights(C.Structure):
                 ("b2", C.c_void_p), ("w3", C.c_void_p), ("b3", C.c_void_p)]
 
 
+class RoundParams(C.Structure):
+    _fields_ = [("k_max", C.c_int32), ("mode", C.c_int32), ("depth", C.c_int32),
+                ("trunk_max", C.c_int32), ("confidence", C.c_float), ("temperature", C.c_float)]
+
+
+ROUND_RESULT_INTS = 8
 ROW_STATS_DTYPE = np.dtype([("zmax", "<f4"), ("argmax", "<i4"), ("total", "<f8")])
 STEP_RESULT_INTS = 8 + SB_MAX_ROWS
 
@@ -140,6 +147,21 @@ lib.sb_draft_round.restype = _i32
 lib.sb_draft_round.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _i32, _i32, _i32, _f, _f, _vp,
                                _vp, _vp, C.POINTER(_i32), C.POINTER(_i32), C.POINTER(_i32), _vp,
                                _sz, _vp]
+lib.sb_draft_chain.restype = _i32
+lib.sb_draft_chain.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _f, _f, _vp, _vp, _vp, _vp,
+                               C.POINTER(_i32), _vp, _sz, _vp]
+lib.sb_draft_branches.restype = _i32
+lib.sb_draft_branches.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _vp, _i32, _i32, _i32, _f,
+                                  _vp, _vp, _vp, C.POINTER(_i32), C.POINTER(_i32), _vp, _sz, _vp]
+lib.sb_round_finish.restype = _i32
+lib.sb_round_finish.argtypes = [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]
+lib.sb_spec_round_workspace_bytes.restype = _sz
+lib.sb_spec_round_workspace_bytes.argtypes = [_vp, _vp, C.POINTER(RoundParams), _i32, _i32]
+lib.sb_spec_round.restype = _i32
+lib.sb_spec_round.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, C.POINTER(KVCache), _i32,
+                              C.POINTER(RoundParams), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                              _vp, _vp, C.POINTER(_i32), C.POINTER(_i32), C.POINTER(_i32), _vp,
+                              _sz, _vp, _vp]
 lib.sb_hrad_predict.restype = _i32
 lib.sb_hrad_predict.argtypes = [_vp, _vp, _i32, _i32, _vp, C.POINTER(HradWeights), _vp, _vp,
                                 _vp, _sz, _vp]
@@ -243,6 +265,93 @@ def sb_accept_resample(tokens: torch.Tensor, parents, logits: torch.Tensor, stat
                                   result.data_ptr(), ws.data_ptr(),
                                   ws.numel() * ws.element_size(), _stream(stream)),
            "sb_accept_resample")
+
+
+def sb_round_finish(chain: int, branches: int, depth: int, walk: torch.Tensor, select,
+                    round_out: torch.Tensor, draft_path: torch.Tensor, stream=None) -> None:
+    """walk / draft_path: sb_step_result buffers (new_result()); select int32
+    [3] or None when branches = 0; round_out int32 [ROUND_RESULT_INTS]."""
+    _need(walk, STEP_RESULT_INTS * 4, "walk", torch.int32)
+    if select is not None:
+        _need(select, 12, "select", torch.int32)
+    _need(round_out, ROUND_RESULT_INTS * 4, "round_out", torch.int32)
+    _need(draft_path, STEP_RESULT_INTS * 4, "draft_path", torch.int32)
+    _check(lib.sb_round_finish(chain, branches, depth, walk.data_ptr(), _ptr(select),
+                               round_out.data_ptr(), draft_path.data_ptr(), _stream(stream)),
+           "sb_round_finish")
+
+
+def new_round_result(device="cuda") -> torch.Tensor:
+    return torch.full((ROUND_RESULT_INTS,), -7, dtype=torch.int32, device=device)
+
+
+def decode_round(r: torch.Tensor) -> dict:
+    a = r.cpu().numpy()
+    return {"n_trunk": int(a[0]), "kept": int(a[1]), "token": int(a[2]), "flags": int(a[3]),
+            "draft_len": int(a[4])}
+
+
+def round_params(k_max: int, mode: str, depth: int, trunk_max: int, confidence: float,
+                 temperature: float) -> RoundParams:
+    return RoundParams(k_max, BRANCH_MODES[mode], depth, trunk_max, confidence, temperature)
+
+
+def sb_spec_round_workspace_bytes(target, draft, params: RoundParams, t_len: int,
+                                  d_len: int) -> int:
+    return int(lib.sb_spec_round_workspace_bytes(target.handle, draft.handle, C.byref(params),
+                                                 t_len, d_len))
+
+
+class RoundBuffers:
+    """Device buffers of sb_spec_round for one parameter set."""
+
+    def __init__(self, target, draft, params: RoundParams, t_len: int, d_len: int,
+                 device="cuda"):
+        V = target.shape.vocab
+        R = params.trunk_max + params.k_max * params.depth
+        self.params = params
+        self.tokens = torch.zeros(R, dtype=torch.int32, device=device)
+        self.q = torch.zeros((R, V), dtype=torch.float32, device=device)
+        self.logits = torch.zeros((params.trunk_max, V), dtype=torch.float32, device=device)
+        self.stats = new_stats(params.trunk_max, device)
+        self.walk = new_result(device)
+        self.select = torch.full((3,), -7, dtype=torch.int32, device=device)
+        self.round = new_round_result(device)
+        self.new_lens = torch.zeros(2, dtype=torch.int32, device=device)
+        n = sb_spec_round_workspace_bytes(target, draft, params, t_len, d_len)
+        if n == 0:
+            raise ValueError("sb_spec_round_workspace_bytes: arguments rejected")
+        self.ws = torch.empty(n, dtype=torch.uint8, device=device)
+        self.parents = np.zeros(R, dtype=np.int32)
+
+
+def sb_spec_round(target, t_k: torch.Tensor, t_v: torch.Tensor, t_len: int, draft,
+                  d_k: torch.Tensor, d_v: torch.Tensor, d_len: int, u_draft: torch.Tensor,
+                  u_walk: torch.Tensor, u_sel: torch.Tensor, buf: RoundBuffers,
+                  verify_stream=None, draft_stream=None):
+    """One round (buf.tokens[0] = the root on entry).  Returns (c, B,
+    parents of the draft tree).  Both streams default to the current one."""
+    p = buf.params
+    target._check_kv(t_k, t_v)
+    draft._check_kv(d_k, d_v)
+    R = p.trunk_max + p.k_max * p.depth
+    _need(u_draft, R * 4, "u_draft", torch.float32)
+    _need(u_walk, (p.trunk_max + 1) * 4, "u_walk", torch.float32)
+    _need(u_sel, (p.k_max + 1) * 4, "u_sel", torch.float32)
+    tkv = KVCache(t_k.data_ptr(), t_v.data_ptr(), t_k.shape[2])
+    dkv = KVCache(d_k.data_ptr(), d_v.data_ptr(), d_k.shape[2])
+    nc, nb = C.c_int32(0), C.c_int32(0)
+    par = buf.parents
+    _check(lib.sb_spec_round(target.handle, C.byref(tkv), t_len, draft.handle, C.byref(dkv), d_len,
+                             C.byref(p), u_draft.data_ptr(), u_walk.data_ptr(), u_sel.data_ptr(),
+                             buf.tokens.data_ptr(), buf.q.data_ptr(), buf.logits.data_ptr(),
+                             buf.stats.data_ptr(), buf.walk.data_ptr(), buf.select.data_ptr(),
+                             buf.round.data_ptr(), buf.new_lens.data_ptr(),
+                             par.ctypes.data_as(C.POINTER(C.c_int32)), C.byref(nc), C.byref(nb),
+                             buf.ws.data_ptr(), buf.ws.numel(), _stream(verify_stream),
+                             _stream(draft_stream)), "sb_spec_round")
+    c, B = int(nc.value), int(nb.value)
+    return c, B, par[:1 + c + B * p.depth].copy()
 
 
 def sb_branch_workspace_bytes() -> int:
@@ -570,6 +679,55 @@ class Model:
                                   _stream(stream)), "sb_draft_round")
         B, c = int(nb.value), int(nc.value)
         return B, par[:1 + c + B * depth].copy(), c
+
+    def sb_draft_chain(self, k: torch.Tensor, v: torch.Tensor, kv_len: int, trunk_max: int,
+                       confidence: float, temperature: float, u: torch.Tensor,
+                       tokens: torch.Tensor, q: torch.Tensor, xb: torch.Tensor, ws: torch.Tensor,
+                       stream=None) -> int:
+        """tokens int32 / q float32 [>= trunk_max + 1]([vocab]), tokens[0] the
+        root; u float32 [trunk_max]; xb int32 [1]; ws of
+        draft_round_workspace(1, 1, kv_len, trunk_max).  Returns c."""
+        self._check_kv(k, v)
+        V = self.shape.vocab
+        _need(u, trunk_max * 4, "u", torch.float32)
+        _need(tokens, (trunk_max + 1) * 4, "tokens", torch.int32)
+        _need(q, (trunk_max + 1) * V * 4, "q", torch.float32)
+        _need(xb, 4, "xb", torch.int32)
+        nc = C.c_int32(0)
+        kv = KVCache(k.data_ptr(), v.data_ptr(), k.shape[2])
+        _check(lib.sb_draft_chain(self.handle, C.byref(kv), kv_len, trunk_max, confidence,
+                                  temperature, u.data_ptr(), tokens.data_ptr(), q.data_ptr(),
+                                  xb.data_ptr(), C.byref(nc), ws.data_ptr(),
+                                  ws.numel() * ws.element_size(), _stream(stream)),
+               "sb_draft_chain")
+        return int(nc.value)
+
+    def sb_draft_branches(self, k: torch.Tensor, v: torch.Tensor, kv_len: int, chain: int,
+                          xb: torch.Tensor, k_max: int, mode: str, depth: int,
+                          temperature: float, u: torch.Tensor, tokens: torch.Tensor,
+                          q: torch.Tensor, ws: torch.Tensor, stream=None):
+        """After sb_draft_chain: u float32 [k_max * depth]; tokens / q hold
+        at least 1 + chain + k_max * depth rows; ws of
+        draft_round_workspace(k_max, depth, kv_len, chain + 1).  Returns (B,
+        parents)."""
+        self._check_kv(k, v)
+        V = self.shape.vocab
+        R = 1 + chain + k_max * depth
+        _need(u, k_max * depth * 4, "u", torch.float32)
+        _need(tokens, R * 4, "tokens", torch.int32)
+        _need(q, R * V * 4, "q", torch.float32)
+        _need(xb, 4, "xb", torch.int32)
+        par = np.zeros(R, dtype=np.int32)
+        nb = C.c_int32(0)
+        kv = KVCache(k.data_ptr(), v.data_ptr(), k.shape[2])
+        _check(lib.sb_draft_branches(self.handle, C.byref(kv), kv_len, chain, xb.data_ptr(), k_max,
+                                     BRANCH_MODES[mode], depth, temperature, u.data_ptr(),
+                                     tokens.data_ptr(), q.data_ptr(),
+                                     par.ctypes.data_as(C.POINTER(C.c_int32)), C.byref(nb),
+                                     ws.data_ptr(), ws.numel() * ws.element_size(),
+                                     _stream(stream)), "sb_draft_branches")
+        B = int(nb.value)
+        return B, par[:1 + chain + B * depth].copy()
 
     def sb_kv_rollback(self, k: torch.Tensor, v: torch.Tensor, kv_len: int,
                        result: torch.Tensor, new_len: torch.Tensor, stream=None) -> None:

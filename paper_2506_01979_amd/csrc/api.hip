@@ -943,52 +943,51 @@ size_t sb_draft_round_workspace_bytes(const sb_model *draft, int32_t k_max, int3
   return round_layout(draft, k_max, depth, trunk_max, kv_len, &L) ? L.total : 0;
 }
 
-sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t k_max,
-                         int32_t mode, int32_t depth, int32_t trunk_max, float confidence,
-                         float temperature, const float *d_u, int32_t *d_tokens, float *d_q,
-                         int32_t *h_parents, int32_t *h_branches, int32_t *h_chain, void *d_ws,
-                         size_t ws_bytes, hipStream_t stream) {
-  if (!draft || !kv || !kv->k || !kv->v || !d_u || !d_tokens || !d_q || !h_parents ||
-      !h_branches || !h_chain || !d_ws)
-    return SB_ERR_INVALID_ARG;
-  if (mode != SB_BRANCH_TOPK && mode != SB_BRANCH_IID && mode != SB_BRANCH_WOR)
-    return SB_ERR_INVALID_ARG;
-  if (!temperature_ok(temperature) || isnan(confidence) || draft->cfg.vocab > SB_BRANCH_MAX_VOCAB)
+static bool draft_args_ok(sb_model *draft, const sb_kv_cache *kv, float temperature) {
+  return draft && kv && kv->k && kv->v && temperature_ok(temperature) &&
+         draft->cfg.vocab <= SB_BRANCH_MAX_VOCAB;
+}
+
+// Draws into logits rows of a drafting step (src -> dst rows of d_tokens /
+// d_q), from the round workspace's logits and statistics.
+static sb_status draft_sample_rows(const sb_model *draft, char *ws, const RoundLayout &L,
+                                   float temperature, int n_logit_rows, int n, const int32_t *src,
+                                   const int32_t *dst, int n_out, const float *u, int32_t *toks,
+                                   float *d_q, float *cf, hipStream_t stream) {
+  DraftRows rows{};
+  rows.n = n;
+  for (int i = 0; i < n; ++i) {
+    if (src[i] < 0 || src[i] >= n_logit_rows || dst[i] < 0 || dst[i] >= n_out)
+      return SB_ERR_INVALID_ARG;
+    rows.src[i] = src[i];
+    rows.dst[i] = dst[i];
+  }
+  return hip_status(launch_draft_sample(draft->cfg.vocab, rows, (const float *)(ws + L.logits),
+                                        (const sb_row_stats *)(ws + L.stats), temperature, u,
+                                        toks, d_q, ws + L.sample, stream, cf));
+}
+
+sb_status sb_draft_chain(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t trunk_max,
+                         float confidence, float temperature, const float *d_u, int32_t *d_tokens,
+                         float *d_q, int32_t *d_xb, int32_t *h_chain, void *d_ws, size_t ws_bytes,
+                         hipStream_t stream) {
+  if (!draft_args_ok(draft, kv, temperature) || !d_u || !d_tokens || !d_q || !d_xb || !h_chain ||
+      !d_ws || isnan(confidence))
     return SB_ERR_INVALID_ARG;
   RoundLayout L;
-  if (!round_layout(draft, k_max, depth, trunk_max, kv_len, &L)) return SB_ERR_INVALID_ARG;
+  if (!round_layout(draft, 1, 1, trunk_max, kv_len, &L)) return SB_ERR_INVALID_ARG;
   if (ws_bytes < L.total) return SB_ERR_CAPACITY;
-  const int R = trunk_max + k_max * depth;
-  if ((int64_t)kv_len + R > kv->capacity) return SB_ERR_CAPACITY;
+  if ((int64_t)kv_len + trunk_max > kv->capacity) return SB_ERR_CAPACITY;
   const int V = draft->cfg.vocab;
   char *ws = (char *)d_ws;
   float *logits = (float *)(ws + L.logits);
   sb_row_stats *stats = (sb_row_stats *)(ws + L.stats);
-  int32_t *xb = (int32_t *)(ws + L.ints);
-  int32_t *count = xb + 1;
-  float *conf = (float *)(xb + 2);
-  void *sws = ws + L.sample;
+  float *conf = (float *)((int32_t *)(ws + L.ints) + 2);
   const size_t fws = L.logits;
-  auto sample = [&](int n_logit_rows, int n, const int32_t *src, const int32_t *dst, int n_out,
-                    const float *u, int32_t *toks, float *cf) -> sb_status {
-    DraftRows rows{};
-    rows.n = n;
-    for (int i = 0; i < n; ++i) {
-      if (src[i] < 0 || src[i] >= n_logit_rows || dst[i] < 0 || dst[i] >= n_out)
-        return SB_ERR_INVALID_ARG;
-      rows.src[i] = src[i];
-      rows.dst[i] = dst[i];
-    }
-    return hip_status(
-        launch_draft_sample(V, rows, logits, stats, temperature, u, toks, d_q, sws, stream, cf));
-  };
-
-  // 1. the chain: x_t from row t - 1, until the first token below the
-  //    confidence threshold or x_trunk_max, which becomes x_b
+  // x_t from row t - 1, until the first token below the confidence
+  // threshold or x_trunk_max, which becomes x_b
   int32_t par[SB_MAX_ROWS];
   par[0] = -1;
-  int c = 0;
-  const int32_t *d_xb = xb;
   for (int t = 1; t <= trunk_max; ++t) {
     sb_status st = sb_verify_forward(draft, kv, kv_len, d_tokens, par, t, temperature, logits,
                                      stats, ws, fws, stream);
@@ -998,32 +997,64 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
       // the last allowed draft is the branch point: its row goes straight
       // to row 0, its token to x_b
       const int32_t zero = 0;
-      st = sample(t, 1, &src, &zero, R, d_u + (t - 1), xb, nullptr);
+      st = draft_sample_rows(draft, ws, L, temperature, t, 1, &src, &zero, trunk_max + 1,
+                             d_u + (t - 1), d_xb, d_q, nullptr, stream);
       if (st != SB_OK) return st;
-      c = t - 1;
-      break;
+      *h_chain = t - 1;
+      return SB_OK;
     }
     const int32_t dst = t;
-    st = sample(t, 1, &src, &dst, R, d_u + (t - 1), d_tokens, conf);
+    st = draft_sample_rows(draft, ws, L, temperature, t, 1, &src, &dst, trunk_max + 1,
+                           d_u + (t - 1), d_tokens, d_q, conf, stream);
     if (st != SB_OK) return st;
     float cf = 0.0f;
     if (hipMemcpyAsync(&cf, conf, sizeof(cf), hipMemcpyDeviceToHost, stream) != hipSuccess ||
         hipStreamSynchronize(stream) != hipSuccess)
       return SB_ERR_HIP;
     if (cf < confidence) {
-      // an unconfident draft: the branch point; its distribution to row 0
+      // an unconfident draft: the branch point; its distribution to row 0,
+      // its token to x_b
       if (hipMemcpyAsync(d_q, d_q + (size_t)t * V, (size_t)V * sizeof(float),
-                         hipMemcpyDeviceToDevice, stream) != hipSuccess)
+                         hipMemcpyDeviceToDevice, stream) != hipSuccess ||
+          hipMemcpyAsync(d_xb, d_tokens + t, sizeof(int32_t), hipMemcpyDeviceToDevice,
+                         stream) != hipSuccess)
         return SB_ERR_HIP;
-      d_xb = d_tokens + t;
-      c = t - 1;
-      break;
+      *h_chain = t - 1;
+      return SB_OK;
     }
     par[t] = t - 1;
   }
-  // 2. the branch-point candidates into rows c + 1 .. c + B
-  sb_status st = sb_branch_candidates(d_q, V, d_xb, k_max, mode, d_u + trunk_max, count,
-                                      d_tokens + c + 1, d_q + (size_t)(c + 1) * V, ws + L.branch,
+  return SB_ERR_INVALID_ARG;  // not reached: t == trunk_max returns
+}
+
+sb_status sb_draft_branches(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t chain,
+                            const int32_t *d_xb, int32_t k_max, int32_t mode, int32_t depth,
+                            float temperature, const float *d_u, int32_t *d_tokens, float *d_q,
+                            int32_t *h_parents, int32_t *h_branches, void *d_ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  if (!draft_args_ok(draft, kv, temperature) || !d_xb || !d_u || !d_tokens || !d_q ||
+      !h_parents || !h_branches || !d_ws || chain < 0)
+    return SB_ERR_INVALID_ARG;
+  if (mode != SB_BRANCH_TOPK && mode != SB_BRANCH_IID && mode != SB_BRANCH_WOR)
+    return SB_ERR_INVALID_ARG;
+  RoundLayout L;
+  if (!round_layout(draft, k_max, depth, chain + 1, kv_len, &L)) return SB_ERR_INVALID_ARG;
+  if (ws_bytes < L.total) return SB_ERR_CAPACITY;
+  const int c = chain;
+  const int R = 1 + c + k_max * depth;
+  if ((int64_t)kv_len + R > kv->capacity) return SB_ERR_CAPACITY;
+  const int V = draft->cfg.vocab;
+  char *ws = (char *)d_ws;
+  float *logits = (float *)(ws + L.logits);
+  sb_row_stats *stats = (sb_row_stats *)(ws + L.stats);
+  int32_t *count = (int32_t *)(ws + L.ints) + 1;
+  const size_t fws = L.logits;
+  int32_t par[SB_MAX_ROWS];
+  par[0] = -1;
+  for (int t = 1; t <= c; ++t) par[t] = t - 1;
+  // the branch-point candidates into rows c + 1 .. c + B
+  sb_status st = sb_branch_candidates(d_q, V, d_xb, k_max, mode, d_u, count, d_tokens + c + 1,
+                                      d_q + (size_t)(c + 1) * V, ws + L.branch,
                                       sb_branch_workspace_bytes(), stream);
   if (st != SB_OK) return st;
   int32_t B = 0;
@@ -1032,7 +1063,7 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
     return SB_ERR_HIP;
   if (B < 0 || B > k_max) return SB_ERR_HIP;
   for (int i = 0; i < B; ++i) par[c + 1 + i] = c;
-  // 3. continuations, one depth per step
+  // continuations, one depth per step
   int32_t src[SB_BRANCH_MAX_K], dst[SB_BRANCH_MAX_K];
   for (int d = 2; d <= depth && B > 0; ++d) {
     const int n = 1 + c + (d - 1) * B;
@@ -1044,13 +1075,170 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
       dst[i] = c + 1 + (d - 1) * B + i;
       par[dst[i]] = src[i];
     }
-    st = sample(n, B, src, dst, R, d_u + trunk_max + k_max * (d - 1), d_tokens, nullptr);
+    st = draft_sample_rows(draft, ws, L, temperature, n, B, src, dst, R, d_u + k_max * (d - 1),
+                           d_tokens, d_q, nullptr, stream);
     if (st != SB_OK) return st;
   }
   const int n_rows = 1 + c + B * depth;
   for (int i = 0; i < n_rows; ++i) h_parents[i] = par[i];
   *h_branches = B;
+  return SB_OK;
+}
+
+sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t k_max,
+                         int32_t mode, int32_t depth, int32_t trunk_max, float confidence,
+                         float temperature, const float *d_u, int32_t *d_tokens, float *d_q,
+                         int32_t *h_parents, int32_t *h_branches, int32_t *h_chain, void *d_ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  if (!draft_args_ok(draft, kv, temperature) || !d_u || !d_tokens || !d_q || !h_parents ||
+      !h_branches || !h_chain || !d_ws || isnan(confidence))
+    return SB_ERR_INVALID_ARG;
+  if (mode != SB_BRANCH_TOPK && mode != SB_BRANCH_IID && mode != SB_BRANCH_WOR)
+    return SB_ERR_INVALID_ARG;
+  RoundLayout L;
+  if (!round_layout(draft, k_max, depth, trunk_max, kv_len, &L)) return SB_ERR_INVALID_ARG;
+  if (ws_bytes < L.total) return SB_ERR_CAPACITY;
+  if ((int64_t)kv_len + trunk_max + k_max * depth > kv->capacity) return SB_ERR_CAPACITY;
+  // x_b lives in the workspace between the two phases, in the last int of
+  // this layout: the two phases lay out smaller rounds (trunk_max rows,
+  // then c + 1 <= trunk_max), whose areas end below it, or at its first
+  // three ints when the sizes coincide
+  int32_t *xb = (int32_t *)((char *)d_ws + L.ints) + 3;
+  int32_t c = 0;
+  sb_status st = sb_draft_chain(draft, kv, kv_len, trunk_max, confidence, temperature, d_u,
+                                d_tokens, d_q, xb, &c, d_ws, ws_bytes, stream);
+  if (st != SB_OK) return st;
+  st = sb_draft_branches(draft, kv, kv_len, c, xb, k_max, mode, depth, temperature,
+                         d_u + trunk_max, d_tokens, d_q, h_parents, h_branches, d_ws, ws_bytes,
+                         stream);
+  if (st != SB_OK) return st;
   *h_chain = c;
+  return SB_OK;
+}
+
+sb_status sb_round_finish(int32_t chain, int32_t branches, int32_t depth,
+                          const sb_step_result *d_walk, const int32_t *d_select,
+                          sb_round_result *d_round, sb_step_result *d_draft_path,
+                          hipStream_t stream) {
+  if (!d_walk || !d_round || !d_draft_path || chain < 0 || branches < 0 || depth < 1)
+    return SB_ERR_INVALID_ARG;
+  if (branches > 0 && !d_select) return SB_ERR_INVALID_ARG;
+  if ((int64_t)1 + chain + (int64_t)branches * depth > SB_MAX_ROWS) return SB_ERR_INVALID_ARG;
+  return hip_status(launch_round_finish(chain, branches, depth, d_walk,
+                                        branches > 0 ? d_select : nullptr, d_round, d_draft_path,
+                                        stream));
+}
+
+// Workspace of a whole round: the draft's round area (its forward, logits,
+// statistics, candidates, sampler and x_b), the target's chain forward, the
+// target's sampler and the draft's kept-row path.
+struct SpecLayout {
+  RoundLayout draft;
+  size_t target, sample, dpath, total;
+};
+static bool spec_layout(const sb_model *target, const sb_model *draft, const sb_round_params *p,
+                        int t_len, int d_len, SpecLayout *o) {
+  if (!target || !draft || !p || target->cfg.vocab != draft->cfg.vocab || t_len < 0) return false;
+  if (!round_layout(draft, p->k_max, p->depth, p->trunk_max, d_len, &o->draft)) return false;
+  const size_t tw = sb_workspace_bytes(target, p->trunk_max, t_len);
+  const size_t sw = sb_sample_workspace_bytes(target->cfg.vocab);
+  if (!tw || !sw) return false;
+  o->target = align_up(o->draft.total);
+  o->sample = o->target + align_up(tw);
+  o->dpath = o->sample + align_up(sw);
+  o->total = o->dpath + align_up(sizeof(sb_step_result));
+  return true;
+}
+
+size_t sb_spec_round_workspace_bytes(const sb_model *target, const sb_model *draft,
+                                     const sb_round_params *p, int32_t t_len, int32_t d_len) {
+  SpecLayout L;
+  return spec_layout(target, draft, p, t_len, d_len, &L) ? L.total : 0;
+}
+
+namespace {
+// An event that is destroyed with its scope (the work it marks may still
+// be pending; HIP releases it once that work completes).
+struct ScopedEvent {
+  hipEvent_t e = nullptr;
+  hipError_t make() { return hipEventCreateWithFlags(&e, hipEventDisableTiming); }
+  ~ScopedEvent() {
+    if (e) (void)hipEventDestroy(e);
+  }
+};
+}  // namespace
+
+sb_status sb_spec_round(sb_model *target, const sb_kv_cache *t_kv, int32_t t_len, sb_model *draft,
+                        const sb_kv_cache *d_kv, int32_t d_len, const sb_round_params *p,
+                        const float *d_u_draft, const float *d_u_walk, const float *d_u_sel,
+                        int32_t *d_tokens, float *d_q, float *d_logits, sb_row_stats *d_stats,
+                        sb_step_result *d_walk, int32_t *d_select, sb_round_result *d_round,
+                        int32_t *d_new_lens, int32_t *h_parents, int32_t *h_chain,
+                        int32_t *h_branches, void *d_ws, size_t ws_bytes,
+                        hipStream_t verify_stream, hipStream_t draft_stream) {
+  if (!target || !draft || target == draft || !t_kv || !d_kv || !p || !d_u_draft || !d_u_walk ||
+      !d_u_sel || !d_tokens || !d_q || !d_logits || !d_stats || !d_walk || !d_select ||
+      !d_round || !d_new_lens || !h_parents || !h_chain || !h_branches || !d_ws)
+    return SB_ERR_INVALID_ARG;
+  if (!t_kv->k || !t_kv->v || !temperature_ok(p->temperature) || isnan(p->confidence))
+    return SB_ERR_INVALID_ARG;
+  SpecLayout L;
+  if (!spec_layout(target, draft, p, t_len, d_len, &L)) return SB_ERR_INVALID_ARG;
+  if (ws_bytes < L.total) return SB_ERR_CAPACITY;
+  if ((int64_t)t_len + p->trunk_max > t_kv->capacity) return SB_ERR_CAPACITY;
+  const int V = target->cfg.vocab;
+  const float T = p->temperature;
+  char *ws = (char *)d_ws;
+  int32_t *xb = (int32_t *)(ws + L.draft.ints) + 3;  // as sb_draft_round keeps it
+  sb_step_result *dpath = (sb_step_result *)(ws + L.dpath);
+  ScopedEvent chain_done, branches_done;
+  if (chain_done.make() != hipSuccess || branches_done.make() != hipSuccess) return SB_ERR_HIP;
+
+  // drafting phase: the chain up to the branch point
+  int32_t c = 0;
+  sb_status st = sb_draft_chain(draft, d_kv, d_len, p->trunk_max, p->confidence, T, d_u_draft,
+                                d_tokens, d_q, xb, &c, ws, L.draft.total, draft_stream);
+  if (st != SB_OK) return st;
+  if (hipEventRecord(chain_done.e, draft_stream) != hipSuccess ||
+      hipStreamWaitEvent(verify_stream, chain_done.e, 0) != hipSuccess)
+    return SB_ERR_HIP;
+
+  // verification phase: the target scores and tests the chain ...
+  int32_t par[SB_MAX_ROWS];
+  par[0] = -1;
+  for (int t = 1; t <= c; ++t) par[t] = t - 1;
+  st = sb_verify_forward(target, t_kv, t_len, d_tokens, par, c + 1, T, d_logits, d_stats,
+                         ws + L.target, L.sample - L.target, verify_stream);
+  if (st != SB_OK) return st;
+  st = sb_accept_resample(V, c + 1, d_tokens, par, d_logits, d_stats, T, d_q, d_u_walk, d_walk,
+                          ws + L.sample, L.dpath - L.sample, verify_stream);
+  if (st != SB_OK) return st;
+  // ... while the draft branches at x_b on its own stream
+  int32_t B = 0;
+  st = sb_draft_branches(draft, d_kv, d_len, c, xb, p->k_max, p->mode, p->depth, T,
+                         d_u_draft + p->trunk_max, d_tokens, d_q, h_parents, &B, ws,
+                         L.draft.total, draft_stream);
+  if (st != SB_OK) return st;
+  if (hipEventRecord(branches_done.e, draft_stream) != hipSuccess ||
+      hipStreamWaitEvent(verify_stream, branches_done.e, 0) != hipSuccess)
+    return SB_ERR_HIP;
+
+  // Algorithm 1 at the chain's last row, then both rollbacks
+  if (B > 0) {
+    st = sb_select_branch(V, d_logits + (size_t)c * V, d_stats + c, T, B, d_tokens + c + 1,
+                          d_q + (size_t)(c + 1) * V, d_u_sel, d_select, ws + L.sample,
+                          L.dpath - L.sample, verify_stream);
+    if (st != SB_OK) return st;
+  }
+  st = sb_round_finish(c, B, p->depth, d_walk, B > 0 ? d_select : nullptr, d_round, dpath,
+                       verify_stream);
+  if (st != SB_OK) return st;
+  st = sb_kv_rollback(target, t_kv, t_len, d_walk, d_new_lens, verify_stream);
+  if (st != SB_OK) return st;
+  st = sb_kv_rollback(draft, d_kv, d_len, dpath, d_new_lens + 1, verify_stream);
+  if (st != SB_OK) return st;
+  *h_chain = c;
+  *h_branches = B;
   return SB_OK;
 }
 

@@ -98,7 +98,56 @@ __global__ __launch_bounds__(256) void k_rollback(int k_cols, int vec_per_row, i
   }
 }
 
+// The end of a SpecBranch round (Algorithm 2, verification phase): the
+// target's walk over the trunk chain [root, x_1 .. x_c] and Algorithm 1 at
+// the trunk's last row give the committed token; the draft cache keeps the
+// root, the accepted trunk rows and, with a kept branch, that branch's rows
+// whose KV the draft computed (depths 1 .. depth - 1).  One thread.
+__global__ void k_round_finish(int chain, int branches, int depth, const sb_step_result *walk,
+                               const int32_t *sel, sb_round_result *out, sb_step_result *dpath) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const int n = walk->n_accepted;
+  const bool whole = n >= chain;
+  int kept = -1, token = walk->next_token, flags = walk->flags;
+  if (whole && sel) {
+    kept = sel[0];
+    token = sel[1];
+    flags |= sel[2];
+  }
+  // the walk's bonus draw (a fully accepted trunk) is not a committed token
+  // here: with candidates, Algorithm 1 decides; with none, the draw from
+  // p at the trunk's last row is the token
+  int len = 0;
+  const int n_trunk = whole ? chain : n;
+  for (int j = 0; j <= n_trunk; ++j) dpath->path[len++] = j;
+  if (kept >= 0 && kept < branches)
+    for (int d = 1; d < depth; ++d) dpath->path[len++] = chain + 1 + (d - 1) * branches + kept;
+  for (int j = len; j < SB_MAX_ROWS; ++j) dpath->path[j] = -1;
+  dpath->n_accepted = len - 1;
+  dpath->branch = kept;
+  dpath->next_token = token;
+  dpath->path_len = len;
+  dpath->flags = flags;
+  dpath->n_rejected = 0;
+  dpath->bonus = 0;
+  dpath->reserved = 0;
+  out->n_trunk = n_trunk;
+  out->kept = kept;
+  out->token = token;
+  out->flags = flags;
+  out->draft_len = len;
+  out->reserved[0] = out->reserved[1] = out->reserved[2] = 0;
+}
+
 }  // namespace
+
+hipError_t launch_round_finish(int chain, int branches, int depth, const sb_step_result *walk,
+                               const int32_t *sel, sb_round_result *out, sb_step_result *dpath,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(k_round_finish, dim3(1), dim3(64), 0, s, chain, branches, depth, walk, sel,
+                     out, dpath);
+  return hipGetLastError();
+}
 
 hipError_t launch_rollback(int n_layers, int n_kv, int capacity, int head_dim, int elem_bytes,
                            void *k, void *v, int kv_len, const sb_step_result *res,

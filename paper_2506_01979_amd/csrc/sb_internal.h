@@ -38,6 +38,9 @@ hipError_t launch_draft_sample(int vocab, const DraftRows &rows, const float *lo
                                float *conf = nullptr);
 
 // ---- rollback (k_rollback.hip) ---------------------------------------------
+hipError_t launch_round_finish(int chain, int branches, int depth, const sb_step_result *walk,
+                               const int32_t *sel, sb_round_result *out, sb_step_result *dpath,
+                               hipStream_t s);
 hipError_t launch_rollback(int n_layers, int n_kv, int capacity, int head_dim, int elem_bytes,
                            void *k, void *v, int kv_len, const sb_step_result *res,
                            int32_t *new_len, hipStream_t s);

@@ -84,6 +84,9 @@ class Workload:
 SHAPES = {
     "tiny": Shape("tiny", 2, 256, 4, 4, 64, 688, 1024, "f32"),
     "exact": Shape("exact", 1, 64, 2, 2, 32, 172, 16, "f32"),
+    # a four-token vocabulary, small enough to enumerate a whole round's
+    # outcomes exactly
+    "enum": Shape("enum", 1, 32, 2, 2, 16, 64, 4, "f32"),
     "llama7b": Shape("llama7b", 32, 4096, 32, 32, 128, 11008, 32000, "bf16"),
     "llama13b": Shape("llama13b", 40, 5120, 40, 40, 128, 13824, 32000, "bf16"),
     "llama70b": Shape("llama70b", 80, 8192, 64, 8, 128, 28672, 128256, "bf16"),

@@ -1,0 +1,160 @@
+"""GPU parity of one whole SpecBranch round (Algorithm 2) against the oracle
+(oracle.spec_round), through sb_spec_round.
+
+The draft drafts its chain on one stream; the target verifies that chain on
+a second stream while the draft spawns and extends the branches on the
+first; Algorithm 1 at the chain's last row, the round's end and both
+rollbacks follow on the target's stream.  Float32 target and draft models
+(distinct weights, same shape) with prefixes from the oracle's prefill.
+
+Checked, on every case: the round run on two streams equals the round run
+on one stream bit for bit (tokens, q rows, logits, statistics, the walk,
+the selection, the round's result, both new lengths and both caches); and
+against the oracle -- chain length, branch count, draft tree and tokens,
+the walk, the round's result and the new lengths exactly; q rows within
+2e-5 relative, the target's logits and both caches' kept rows within
+1e-4 / 5e-4 of the float64 oracle (float32 GEMMs over K <= 688).  Each case
+is one whose every decision lies at least 2e-5 from its threshold in the
+oracle (checked first), so exact token agreement is the bar.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import decision_margin, row_relerr, say
+from oracle import decoder, spec_round
+from paper_2506_01979_amd import synth
+from test_gpu_draft import first_tie
+
+pytestmark = pytest.mark.gpu
+
+_M = {}
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2506_01979_amd import api as A
+    assert torch.cuda.is_available()
+    return A
+
+
+def weights(name):
+    if name not in _M:
+        sh = synth.SHAPES[name]
+        _M[name] = (synth.model_weights(sh, 0), synth.model_weights(sh, 1))
+    return _M[name]
+
+
+ROUND_CASES = [
+    # shape, prefix, k_max, mode, depth, T, seed, trunk_max, confidence
+    ("exact", 8, 4, "wor", 3, 0.25, 1, 5, 0.08),    # chain of 1 accepted, first candidate kept
+    ("exact", 8, 4, "wor", 3, 0.25, 3, 5, 0.08),    # chain of 2 rejected at its first token
+    ("exact", 8, 4, "iid", 3, 0.25, 8, 5, 0.08),    # chain of 3, one accepted
+    ("exact", 8, 4, "wor", 3, 0.25, 0, 5, 0.08),    # no chain, second candidate kept
+    ("exact", 8, 4, "iid", 3, 0.25, 9, 5, 0.08),    # no chain, every candidate rejected
+    ("exact", 8, 4, "topk", 3, 0.25, 1, 5, 0.08),   # chain accepted, top-k candidates rejected
+    ("exact", 8, 4, "topk", 3, 0.0, 2, 5, 0.5),     # greedy: chain of 4, one accepted
+    ("exact", 8, 6, "wor", 1, 0.25, 5, 5, 0.08),    # depth 1: the candidates alone
+    ("exact", 8, 4, "iid", 3, 0.25, 7, 1, float("inf")),  # trunk_max 1
+    ("tiny", 96, 4, "iid", 3, 0.6, 0, 5, 0.004),    # 2 layers, vocabulary 1024: third kept
+    ("tiny", 96, 4, "wor", 3, 0.1, 6, 5, 0.02),     # a chain of 4 on the wider model
+]
+
+
+def oracle_round(name, P, k_max, mode, depth, T, seed, trunk, eps):
+    sh = synth.SHAPES[name]
+    Wt, Wd = weights(name)
+    ptoks = synth.prefix_tokens(sh.vocab, P + 1, seed)
+    _, Kt, Vt = decoder.prefill(sh, Wt, ptoks[:-1])
+    _, Kd, Vd = decoder.prefill(sh, Wd, ptoks[:-1])
+    nd, nw, ns = spec_round.uniforms_needed(k_max, depth, trunk)
+    u = synth.uniforms(nd + nw + ns, seed=seed)
+    tr = []
+    r = spec_round.spec_round(sh, Wt, Kt, Vt, P, sh, Wd, Kd, Vd, P, int(ptoks[-1]), k_max, mode,
+                              depth, T, u[:nd], u[nd:nd + nw], u[nd + nw:], trunk, eps, trace=tr)
+    # every decision away from its threshold: the draft side's (draws,
+    # confidence tests, B, top-k order, greedy argmaxes) and the
+    # verification's (chain tests, Algorithm 1, draws)
+    stop, whole = first_tie(sh, Wd, Kd, Vd, P, r.draft, k_max, mode, depth, T, u[:nd], trunk, eps)
+    assert whole and stop == len(r.draft.tokens), "a draft-side decision within 2e-5"
+    assert decision_margin(tr, u) >= 2e-5, "a verification decision within 2e-5"
+    if T == 0:
+        for row in r.logits:
+            s = np.sort(row.astype(np.float64))
+            assert s[-1] - s[-2] > 2e-5 * max(1.0, abs(s[-1]))
+    return sh, ptoks, (Kt, Vt, Kd, Vd), u, (nd, nw, ns), r
+
+
+@pytest.mark.parametrize("name,P,k_max,mode,depth,T,seed,trunk,eps", ROUND_CASES)
+def test_round_matches_oracle_on_two_streams(api, name, P, k_max, mode, depth, T, seed, trunk,
+                                             eps):
+    sh, ptoks, (Kt, Vt, Kd, Vd), u, (nd, nw, ns), ref = oracle_round(name, P, k_max, mode, depth,
+                                                                      T, seed, trunk, eps)
+    Wt, Wd = weights(name)
+    tm = api.Model(sh, api.dict_tensors(Wt))
+    dm = api.Model(sh, api.dict_tensors(Wd))
+    R = trunk + k_max * depth
+    tk, tv = tm.new_kv(P + trunk)
+    dk, dv = dm.new_kv(P + R)
+    params = api.round_params(k_max, mode, depth, trunk, eps, T)
+    buf = api.RoundBuffers(tm, dm, params, P, P)
+    ud = torch.from_numpy(u[:nd]).cuda()
+    uw = torch.from_numpy(u[nd:nd + nw]).cuda()
+    us = torch.from_numpy(u[nd + nw:]).cuda()
+
+    def run(sv, sd):
+        tm.load_kv(tk, tv, Kt, Vt, P)
+        dm.load_kv(dk, dv, Kd, Vd, P)
+        buf.tokens.fill_(-5)
+        buf.tokens[0] = int(ptoks[-1])
+        buf.q.fill_(7.0)
+        buf.logits.fill_(7.0)
+        torch.cuda.synchronize()
+        c, B, par = api.sb_spec_round(tm, tk, tv, P, dm, dk, dv, P, ud, uw, us, buf, sv, sd)
+        sv.synchronize()
+        torch.cuda.synchronize()
+        n_t, n_d = (int(x) for x in buf.new_lens.cpu())
+        return {"c": c, "B": B, "par": par, "tokens": buf.tokens.cpu().numpy(),
+                "q": buf.q.cpu().numpy(), "logits": buf.logits.cpu().numpy(),
+                "stats": buf.stats.cpu().numpy(), "walk": api.decode_result(buf.walk),
+                "select": buf.select.cpu().tolist(), "round": api.decode_round(buf.round),
+                "lens": (n_t, n_d), "tkv": tm.read_kv(tk, tv, 0, n_t),
+                "dkv": dm.read_kv(dk, dv, 0, n_d)}
+
+    cur = torch.cuda.current_stream()
+    say(f"round {name} P={P} k_max={k_max} {mode} depth={depth} T={T} seed={seed} "
+        f"trunk={trunk}: one stream")
+    one = run(cur, cur)
+    sv, sd = torch.cuda.Stream(), torch.cuda.Stream()
+    for rep in range(2):
+        say(f"round {name} seed={seed}: two streams, repetition {rep}")
+        two = run(sv, sd)
+        for key in one:
+            a, b = one[key], two[key]
+            if isinstance(a, tuple) and isinstance(a[0], np.ndarray):
+                assert all(np.array_equal(x, y) for x, y in zip(a, b)), key
+            elif isinstance(a, np.ndarray):
+                assert np.array_equal(a, b), key
+            else:
+                assert a == b, key
+
+    got = one
+    c, B = ref.draft.chain, ref.draft.branches
+    n_rows = 1 + c + B * depth
+    assert (got["c"], got["B"]) == (c, B)
+    assert got["par"].tolist() == ref.draft.parents.tolist()
+    assert got["tokens"][:n_rows].tolist() == ref.draft.tokens.tolist()
+    np.testing.assert_allclose(got["q"][:n_rows], ref.draft.q, rtol=2e-5, atol=1e-12)
+    assert row_relerr(got["logits"][:c + 1], ref.logits) < 1e-4
+    w = got["walk"]
+    assert (w["n_accepted"], w["path"], w["next_token"], w["flags"], bool(w["bonus"])) == \
+        (ref.walk.n_accepted, ref.walk.path, ref.walk.next_token, ref.walk.flags, ref.walk.bonus)
+    assert got["round"] == {"n_trunk": ref.n_trunk, "kept": ref.kept, "token": ref.token,
+                            "flags": ref.flags, "draft_len": len(ref.draft_path)}
+    Kto, Vto, lt = ref.target_cache
+    Kdo, Vdo, ld = ref.draft_cache
+    assert got["lens"] == (lt, ld)
+    hd = sh.head_dim
+    for (Kg, Vg), Ko, Vo, ln in ((got["tkv"], Kto, Vto, lt), (got["dkv"], Kdo, Vdo, ld)):
+        assert row_relerr(Kg.reshape(-1, hd), Ko[:, :, :ln].reshape(-1, hd)) < 5e-4
+        assert row_relerr(Vg.reshape(-1, hd), Vo[:, :, :ln].reshape(-1, hd)) < 5e-4
