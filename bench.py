@@ -19,6 +19,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -46,18 +47,30 @@ GEMM_SOURCES = ("paper_2506_01979_amd/csrc/k_gemm.hip", "paper_2506_01979_amd/cs
 # O, [post-attention norm, unless O applies it], gate/up, down.
 
 
-def layer_classes(names):
-    """Kernel classes of one layer, read off the kernel names of a step
-    (names[0] is the embedding kernel)."""
-    pl, i = ["norm", "qkv", "attn"], 4
-    if "k_attn_merge" in names[i]:
-        pl.append("attn_merge")
-        i += 1
-    pl.append("o")
-    i += 1
-    if "k_rmsnorm_pack" in names[i]:
-        pl.append("norm")
-    return pl + ["gate_up", "down"]
+def kernel_class(name: str, prev: str) -> str:
+    """Class of a verify-step kernel from its name (prev: the class of the
+    kernel before it, which tells the O projection from the down one)."""
+    if "k_embed_meta" in name:
+        return "embed"
+    if "k_rmsnorm_pack" in name:
+        return "norm"
+    if "k_attn_merge" in name:
+        return "attn_merge"
+    if "k_attn" in name:
+        return "attn"
+    if "k_softmax_stats" in name:
+        return "stats"
+    if "k_walk" in name:
+        return "accept_walk"
+    if "k_rollback" in name:
+        return "rollback"
+    m = re.search(r"k_gemm<(\d+)", name)
+    if m:
+        epi = int(m.group(1))
+        if epi in (1, 4):  # residual projections
+            return "down" if prev == "gate_up" else "o"
+        return {0: "qkv", 2: "gate_up", 3: "lm_head"}.get(epi, "gemm")
+    return "other"
 
 
 def log(*a):
@@ -89,25 +102,37 @@ def _counter_rows(d):
     return [per[k] for k in sorted(per)]
 
 
+def _step_dispatches(rows, last):
+    """(class, record) of every dispatch of the last `last` complete verify
+    steps (k_embed_meta .. k_softmax_stats; the timed ones, since earlier
+    steps generate the drafts on partial trees)."""
+    steps = []
+    i = 0
+    while i < len(rows):
+        if "k_embed_meta" not in rows[i]["name"]:
+            i += 1
+            continue
+        j = i + 1
+        while j < len(rows) and "k_softmax_stats" not in rows[j]["name"] and \
+                "k_embed_meta" not in rows[j]["name"]:
+            j += 1
+        if j < len(rows) and "k_softmax_stats" in rows[j]["name"]:
+            prev, step = "", []
+            for r in rows[i:j + 1]:
+                prev = kernel_class(r["name"], prev)
+                step.append((prev, r))
+            steps.append(step)
+        i = j
+    return [x for st in steps[-last:] for x in st]
+
+
 def _gate_up_dispatches(rows, n_layers, last):
     """Dispatch records of the gate/up GEMM in the last `last` complete verify
-    steps (the timed ones; earlier steps generate the drafts on partial
-    trees)."""
-    out = []
-    for i, r in enumerate(rows):
-        if "k_embed_meta" not in r["name"] or i + 8 > len(rows):
-            continue
-        per_layer = layer_classes([x["name"] for x in rows[i:i + 8]])
-        nk = 1 + len(per_layer) * n_layers + 3
-        step = rows[i:i + nk]
-        if len(step) < nk or "k_softmax_stats" not in step[-1]["name"]:
-            continue
-        for l in range(n_layers):
-            g = step[1 + len(per_layer) * l + per_layer.index("gate_up")]
-            if "k_gemm" not in g["name"]:
-                raise RuntimeError(f"unexpected kernel order: {g['name']}")
-            out.append(g)
-    return out[-last * n_layers:]
+    steps."""
+    out = [r for c, r in _step_dispatches(rows, last) if c == "gate_up"]
+    if len(out) != last * n_layers:
+        raise RuntimeError(f"expected {last * n_layers} gate/up launches, found {len(out)}")
+    return out
 
 
 def pmc_summary(fetch_dir: str, write_dir: str) -> str:
@@ -190,26 +215,32 @@ def trace_summary(trace_dir: str) -> str:
     stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)[0]
     trace = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
     rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
-    starts = [i for i, r in enumerate(rows) if "k_embed_meta" in r["Kernel_Name"]]
-    per_layer = layer_classes([r["Kernel_Name"] for r in rows[starts[-1]:starts[-1] + 8]])
-    n_k = 1 + len(per_layer) * shape.n_layers + 3
-    steps = [i for i in starts if i + n_k <= len(rows) and
-             "k_softmax_stats" in rows[i + n_k - 1]["Kernel_Name"]][-5:]
-    cls = ["embed"] + per_layer * shape.n_layers + ["norm", "lm_head", "stats"]
-    # the bench step goes on with the accept walk and the rollback
-    tail = [c for c in ("k_walk", "k_rollback")]
-    n_s = n_k
-    if steps and all(steps[-1] + n_k + j < len(rows) and tail[j] in rows[steps[-1] + n_k + j]["Kernel_Name"]
-                     for j in range(len(tail))):
-        n_s = n_k + len(tail)
-        cls = cls + ["accept_walk", "rollback"]
+    # a step: k_embed_meta .. k_softmax_stats, then the accept walk and the
+    # rollback when they follow
+    steps = []
+    for i, r in enumerate(rows):
+        if "k_embed_meta" not in r["Kernel_Name"]:
+            continue
+        j = i + 1
+        while j < len(rows) and "k_softmax_stats" not in rows[j]["Kernel_Name"] and \
+                "k_embed_meta" not in rows[j]["Kernel_Name"]:
+            j += 1
+        if j >= len(rows) or "k_softmax_stats" not in rows[j]["Kernel_Name"]:
+            continue
+        for tail in ("k_walk", "k_rollback"):
+            if j + 1 < len(rows) and tail in rows[j + 1]["Kernel_Name"]:
+                j += 1
+        steps.append((i, j + 1))
+    steps = steps[-5:]
     agg, span = {}, []
-    for i in steps:
-        span.append((int(rows[i + n_s - 1]["End_Timestamp"]) - int(rows[i]["Start_Timestamp"])) / 1e3)
-        for j in range(n_s):
-            r = rows[i + j]
+    for i, e in steps:
+        span.append((int(rows[e - 1]["End_Timestamp"]) - int(rows[i]["Start_Timestamp"])) / 1e3)
+        prev = ""
+        for j in range(i, e):
+            r = rows[j]
             d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-            a = agg.setdefault(cls[j], {"name": set(), "us": []})
+            prev = kernel_class(r["Kernel_Name"], prev)
+            a = agg.setdefault(prev, {"name": set(), "us": []})
             a["name"].add(r["Kernel_Name"].replace("sb::(anonymous namespace)::", ""))
             a["us"].append(d)
     out = [f"# Kernel trace of the verify step, {WORKLOAD}", "",
