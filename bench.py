@@ -204,14 +204,12 @@ def measured_traffic(workload: str):
     return rec["traffic_bytes"]
 
 
-def trace_summary(trace_dir: str) -> str:
+def trace_summary(trace_dir: str, workload: str = WORKLOAD) -> str:
     """Markdown per-kernel summary of a rocprofv3 --kernel-trace --stats run
     of bench.py: the whole-run stats table, then the kernels of the last 5
     complete verify steps in launch order."""
     import csv
     import glob
-    from paper_2506_01979_amd import synth
-    shape = synth.WORKLOADS[WORKLOAD].shape
     stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)[0]
     trace = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
     rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
@@ -243,11 +241,12 @@ def trace_summary(trace_dir: str) -> str:
             a = agg.setdefault(prev, {"name": set(), "us": []})
             a["name"].add(r["Kernel_Name"].replace("sb::(anonymous namespace)::", ""))
             a["us"].append(d)
-    out = [f"# Kernel trace of the verify step, {WORKLOAD}", "",
+    wl = "" if workload == WORKLOAD else f" --workload {workload}"
+    out = [f"# Kernel trace of the verify step, {workload}", "",
            "Command: `cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats "
            "--output-format csv -d <repo>/out/prof_step -o run -- python3 <repo>/bench.py "
-           "--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-draft --no-graph`, then "
-           "`python3 bench.py --trace-summary out/prof_step`", "",
+           f"--steps 10 --warmup 3 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-draft --no-graph{wl}`, "
+           f"then `python3 bench.py --trace-summary out/prof_step{wl}`", "",
            f"Last {len(steps)} complete steps (embed .. stats, then the accept walk and the rollback "
            f"when traced): span "
            + ", ".join(f"{x:.1f}" for x in span) + " us", "",
@@ -470,6 +469,83 @@ def cpu_baseline(shape, host_bits, kv_host, kv_len, inp, n_layers_sample: int) -
             "kind": "oracle", "sample": sample, "step_s": step_s}
 
 
+SWEEP_PREFIXES = (512, 4096, 8192)
+SWEEP_TREES = [(b, k) for b in (1, 2, 4, 8) for k in (4, 8, 16)]
+
+
+def run_sweep(args, api, synth, m, shape, dev) -> None:
+    """One model, every (prefix, B, k) of the sweep: the prefix KV (seeded
+    N(0,1) bf16) filled once for the longest prefix and read in part for the
+    shorter ones; per configuration drafts mixed at --alpha, warmup, then
+    --steps timed verify steps (forward + accept walk + rollback).  Prints
+    one JSON line per configuration, then a markdown table."""
+    import torch
+    p_max = max(SWEEP_PREFIXES)
+    n_max = 1 + max(b * k for b, k in SWEEP_TREES)
+    k_, v_ = m.new_kv(p_max + n_max + 16)
+    t0 = time.time()
+    for l in range(shape.n_layers):
+        kb = synth.synthetic_kv(shape, l, p_max - 1, p_max - 1, 0, as_bits=True)
+        vb = synth.synthetic_kv(shape, l, p_max - 1, p_max - 1, 1, as_bits=True)
+        k_[l, :, :p_max - 1] = torch.from_numpy(kb.view(np.int16)).view(torch.bfloat16).to(dev)
+        v_[l, :, :, :p_max - 1] = torch.from_numpy(vb.view(np.int16)).view(torch.bfloat16).to(dev).transpose(1, 2)
+    log(f"prefix KV ready ({p_max - 1} slots) in {time.time() - t0:.1f}s")
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    rows = []
+    for P in SWEEP_PREFIXES:
+        kv_len = P - 1
+        root = int(synth.prefix_tokens(shape.vocab, P)[-1])
+        for B, kd in SWEEP_TREES:
+            parents = synth.branch_parents(B, kd)
+            n = len(parents)
+            tokens, q = make_drafts(api, synth, m, k_, v_, kv_len, root, parents, args.alpha,
+                                    0.7, 11)
+            d_tok = torch.from_numpy(tokens).to(dev)
+            d_q = torch.from_numpy(q).to(dev)
+            d_u = torch.from_numpy(synth.uniforms(n, 1)).to(dev)
+            logits = torch.empty((n, shape.vocab), dtype=torch.float32, device=dev)
+            stats = api.new_stats(n, dev)
+            ws = m.workspace(n, kv_len)
+            sws = torch.empty(api.sb_sample_workspace_bytes(shape.vocab), dtype=torch.uint8,
+                              device=dev)
+            res = api.new_result(dev)
+            new_len = torch.zeros(1, dtype=torch.int32, device=dev)
+
+            def step():
+                m.sb_verify_forward(k_, v_, kv_len, d_tok, parents, 1.0, logits, stats, ws, stream)
+                api.sb_accept_resample(d_tok, parents, logits, stats, 1.0, d_q, d_u, res, sws,
+                                       stream)
+                m.sb_kv_rollback(k_, v_, kv_len, res, new_len, stream)
+            for _ in range(args.warmup):
+                step()
+            torch.cuda.synchronize()
+            ev0.record(stream)
+            for _ in range(args.steps):
+                step()
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            ms = ev0.elapsed_time(ev1) / args.steps
+            nb = algorithmic_bytes(shape, kv_len, n)["step"]
+            r = api.decode_result(res)
+            rec = {"workload": f"{shape.name} B={B} k={kd} prefix {P}", "prefix": P,
+                   "branches": B, "depth": kd, "rows": n, "ms_per_step": round(ms, 4),
+                   "verified_tokens_per_s": round((n - 1) / (ms * 1e-3), 1),
+                   "step_bytes": nb, "step_hbm_frac": round(nb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                   "accepted": r["n_accepted"], "alpha": args.alpha}
+            rows.append(rec)
+            print(json.dumps(rec), flush=True)
+            del ws, logits
+    out = [f"| prefix | B | k | rows | ms/step | verified tok/s | GB/step | step HBM fraction |",
+           "|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append(f"| {r['prefix']} | {r['branches']} | {r['depth']} | {r['rows']} | "
+                   f"{r['ms_per_step']:.3f} | {r['verified_tokens_per_s']:.0f} | "
+                   f"{r['step_bytes'] / 1e9:.2f} | {r['step_hbm_frac']:.3f} |")
+    print("\n".join(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -500,12 +576,16 @@ def main():
                     help="print the draft-side summary of a rocprofv3 kernel trace and exit")
     ap.add_argument("--trace-summary", metavar="TRACE_DIR",
                     help="summarise a rocprofv3 --kernel-trace --stats run of this script and exit")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time the workload's shape over prefixes 512 / 4096 / 8192 and "
+                         "B in {1, 2, 4, 8} x k in {4, 8, 16} (one JSON line per configuration, "
+                         "then a markdown table) and exit")
     args = ap.parse_args()
     if args.pmc_summary:
         print(pmc_summary(*args.pmc_summary))
         return
     if args.trace_summary:
-        print(trace_summary(args.trace_summary))
+        print(trace_summary(args.trace_summary, args.workload))
         return
     if args.draft_trace_summary:
         print(draft_trace_summary(args.draft_trace_summary), end="")
@@ -547,6 +627,9 @@ def main():
 
     m = api.Model(shape, tensor_fn, device=dev)
     log(f"weights generated, uploaded and packed in {time.time() - t0:.1f}s")
+    if args.sweep:
+        run_sweep(args, api, synth, m, shape, dev)
+        return
 
     def fill_prefix(shp, kb_, vb_, keep=None):
         for l in range(shp.n_layers):

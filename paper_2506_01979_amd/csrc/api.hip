@@ -92,7 +92,7 @@ Layout make_layout(const sb_model_config &c, int n_rows, int kv_len) {
     L.ks_o = pack_geom(c, SB_W_O).ks;
     L.ks_f = pack_geom(c, SB_W_DOWN).ks;
     const int ksx = L.ks_h > L.ks_o ? L.ks_h : L.ks_o;
-    L.n_chunks = attn_splits(c.n_kv_heads, c.head_dim, kv_len + n_rows);
+    L.n_chunks = attn_splits(c.n_kv_heads, c.head_dim, kv_len + n_rows, n_rows * G);
     // key ranges of the persistent kernel's attention (one item per unit)
     L.pk_chunks = pk_attn_chunks(c.n_kv_heads, kv_len + n_rows, device_cus_host());
     const int chunks = L.n_chunks > L.pk_chunks ? L.n_chunks : L.pk_chunks;

@@ -8,10 +8,12 @@
 //
 // Flash-decoding split: the key range [0, kv_len + n_tok) of each KV head is
 // cut into n_chunks ranges of at most 2 NW 32-key steps (NW = head_dim / 16
-// waves per workgroup), one workgroup each, about one per compute unit.
-// The workgroup reads its K rows and rows of the transposed V cache once,
-// straight from HBM into registers, and keeps them for every block of query
-// rows of the KV group (GQA):
+// waves per workgroup); a workgroup takes one range and one block of at
+// most 64 query rows of the KV head's group (with grouped queries a head's
+// group has n_tok G rows; the workgroups of one range sit on one XCD, so
+// its K and V come from HBM once and from that XCD's L2 after).  About one
+// workgroup per compute unit.  The workgroup reads its K rows and rows of
+// the transposed V cache straight into registers and scores its row block:
 //   1. wave w scores steps w and w + NW: S^T = K Q^T, masked, row max into
 //      LDS;
 //   2. after a barrier, the block max M of each row gives p = exp(s - M);
@@ -115,10 +117,18 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15, lg = lane >> 4;
-  const int g = blockIdx.x / a.n_chunks, split = blockIdx.x % a.n_chunks;
   const int G = a.n_heads / a.n_kv;
   const float inv_g = 1.0f / (float)G;  // r / G = floor((r + 0.5) / G) for r < 2^20
   const int R = a.n_tok * G;
+  // Work unit (KV head g, key range split, row block): one block of query
+  // rows per workgroup.  Units are numbered XCD-major (workgroup b runs on
+  // XCD b % 8) with the row block fastest, so the workgroups that read the
+  // same key range of a grouped-query head sit on one XCD and share its L2.
+  const int n_rb = (R + RB - 1) / RB;
+  const int nb = gridDim.x;
+  const int unit = (nb & 7) == 0 ? (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+  const int rb0 = (unit % n_rb) * RB;
+  const int g = unit / n_rb / a.n_chunks, split = unit / n_rb % a.n_chunks;
   const int nkeys = a.kv_len + a.n_tok;
   const int n_steps = (nkeys + 31) >> 5;
   const int st0 = (n_steps * split) / a.n_chunks, st1 = (n_steps * (split + 1)) / a.n_chunks;
@@ -164,7 +174,7 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
       ast[j] = __builtin_amdgcn_raw_buffer_load_b32(ars, vo, 0, 0);
     }
   };
-  stage_loads(0);
+  stage_loads(rb0);
   __builtin_amdgcn_sched_barrier(0);  // issue order: staging, K (V after scoring)
 
   // ---- the workgroup's cache reads, once, into registers.  Lanes whose
@@ -241,7 +251,7 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
       mx = max_x32(max_x16(mx));
       if (lg == 0) smax[w][rt * 16 + lr] = mx;
     }
-    if (rb == 0) {
+    {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < MS; ++j) {
@@ -335,16 +345,10 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
         *(float2 *)&a.part_ml[(base + r) * 2] = make_float2(M == -INFINITY ? M : M * a.scale, L);
       }
     }
-    lds_barrier();  // sp, sq, sanc, smax, ssum free for the next row block
   };
-  // the first block straight after the cache reads (no loop around it, so
-  // the cache registers are not loop-carried and only the staging loads are
-  // waited for before scoring starts)
-  row_block(0);
-  for (int rb = RB; rb < R; rb += RB) {
-    stage_loads(rb);
-    row_block(rb);
-  }
+  // straight after the cache reads (only the staging loads are waited for
+  // before scoring starts)
+  row_block(rb0);
 }
 
 // Combines the key ranges of one (row t, query head) and writes the
@@ -522,24 +526,27 @@ __global__ __launch_bounds__(kMergeThreads) void k_attn_merge_reg(AttnArgs a,
 
 }  // namespace
 
-int attn_splits(int n_kv, int head_dim, int nkeys) {
+int attn_row_tiles(int rows) { return rows >= 16 * kAttnMaxRowTiles ? kAttnMaxRowTiles : (rows + 15) / 16; }
+
+int attn_splits(int n_kv, int head_dim, int nkeys, int rows) {
   // at most 2 head_dim / 16 steps of 32 keys per workgroup, and about
-  // kAttnTargetGroups workgroups in all while every one has a step
+  // kAttnTargetGroups workgroups in all (key ranges x row blocks) while
+  // every one has a step
   const int steps = (nkeys + 31) / 32;
   const int ms = 2 * (head_dim / 16);
+  const int n_rb = (rows + 16 * attn_row_tiles(rows) - 1) / (16 * attn_row_tiles(rows));
   int sp = (steps + ms - 1) / ms;
-  const int fill = (kAttnTargetGroups + n_kv - 1) / n_kv;
+  const int fill = (kAttnTargetGroups + n_kv * n_rb - 1) / (n_kv * n_rb);
   if (sp < fill) sp = fill < steps ? fill : steps;
   return sp < 1 ? 1 : sp;
 }
 
 template <int D>
 hipError_t launch_attn_d(const AttnArgs &a, hipStream_t s) {
-  // row tiles per block
-  constexpr int max_rt = 4;
   const int rows = a.n_tok * (a.n_heads / a.n_kv);
-  const int rt = rows >= 16 * max_rt ? max_rt : (rows + 15) / 16;
-  const dim3 grid(a.n_kv * a.n_chunks);
+  const int rt = attn_row_tiles(rows);
+  const int n_rb = (rows + 16 * rt - 1) / (16 * rt);
+  const dim3 grid(a.n_kv * a.n_chunks * n_rb);
   const dim3 block(D * 4);
   switch (rt) {
     case 1: hipLaunchKernelGGL((k_attn<D, 1>), grid, block, 0, s, a); break;
@@ -551,7 +558,9 @@ hipError_t launch_attn_d(const AttnArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s) {
-  if (a.n_chunks != attn_splits(a.n_kv, a.head_dim, a.kv_len + a.n_tok)) return hipErrorInvalidValue;
+  if (a.n_chunks != attn_splits(a.n_kv, a.head_dim, a.kv_len + a.n_tok,
+                                a.n_tok * (a.n_heads / a.n_kv)))
+    return hipErrorInvalidValue;
   if (a.head_dim == 128) return launch_attn_d<128>(a, s);
   if (a.head_dim == 64) return launch_attn_d<64>(a, s);
   return hipErrorInvalidValue;

@@ -214,9 +214,13 @@ extern thread_local LaunchEvents g_launch_events;
 bool resid_norm_fusable(int tiles, int ks, int n_tok, int *groups);
 
 // k_attn.hip
-// Key ranges per KV head: about kAttnTargetGroups workgroups in all.
+// Key ranges per KV head: about kAttnTargetGroups workgroups in all, one per
+// (KV head, key range, block of at most 16 kAttnMaxRowTiles query rows of
+// the head's group).
 constexpr int kAttnTargetGroups = 192;
-int attn_splits(int n_kv, int head_dim, int nkeys);
+constexpr int kAttnMaxRowTiles = 4;
+int attn_row_tiles(int rows);
+int attn_splits(int n_kv, int head_dim, int nkeys, int rows);
 hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s);
 hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,
                                   hipStream_t s);

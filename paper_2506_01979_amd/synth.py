@@ -112,8 +112,14 @@ WORKLOADS = {
     "exact": Workload("exact", SHAPES["exact"], 8, 3, 3, 1.0),
     "llama7b_b4k8_p2048": Workload("llama7b_b4k8_p2048", SHAPES["llama7b"], 2048, 4, 8, 0.7,
                                    kv_from_prefill=False),
+    "llama13b_b4k8_p512": Workload("llama13b_b4k8_p512", SHAPES["llama13b"], 512, 4, 8, 0.7,
+                                   kv_from_prefill=False),
     "llama13b_b4k8_p4096": Workload("llama13b_b4k8_p4096", SHAPES["llama13b"], 4096, 4, 8, 0.7,
                                     kv_from_prefill=False),
+    "llama13b_b4k8_p8192": Workload("llama13b_b4k8_p8192", SHAPES["llama13b"], 8192, 4, 8, 0.7,
+                                    kv_from_prefill=False),
+    "llama13b_b8k16_p8192": Workload("llama13b_b8k16_p8192", SHAPES["llama13b"], 8192, 8, 16, 0.7,
+                                     kv_from_prefill=False),
     "llama70b_b4k8_p4096": Workload("llama70b_b4k8_p4096", SHAPES["llama70b"], 4096, 4, 8, 0.7,
                                     kv_from_prefill=False),
 }
