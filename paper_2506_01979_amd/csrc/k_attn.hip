@@ -97,14 +97,18 @@ __device__ __forceinline__ uint32_t visible8(const uint32_t *anc, int k0, int kv
   return vis;
 }
 
-// D: head_dim; RT: 16-row query tiles per row block.
-template <int D, int RT>
-__global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
+// D: head_dim; RT: 16-row query tiles per row block; SW: 32-key steps per
+// wave (at most).  SW = 1 halves the keys, registers and LDS of a workgroup
+// so that two fit on a compute unit (launches of more workgroups than
+// compute units: one workgroup's scoring overlaps another's loads).
+// LOOP: the workgroup walks every row block of its key range (the launch
+// does not split the row blocks); otherwise it scores one.
+template <int D, int RT, int SW, bool LOOP>
+__global__ __launch_bounds__(D * 4, SW == 1 ? 4 : 2) void k_attn(AttnArgs a) {
   constexpr int NW = D / 16;   // waves: one per 16 output dimensions
   constexpr int NT = NW * 64;
   constexpr int KSD = D / 32;  // k-steps over head_dim (S)
   constexpr int RB = 16 * RT;  // rows per block
-  constexpr int SW = 2;        // steps per wave (at most)
   constexpr int MS = SW * NW;  // steps of a workgroup (at most)
   constexpr int KW = 32 * MS;  // keys of a workgroup (at most)
   __shared__ uint16_t sp[RB][KW + 8];  // probabilities, bf16 high part, row-major
@@ -120,11 +124,12 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
   const int G = a.n_heads / a.n_kv;
   const float inv_g = 1.0f / (float)G;  // r / G = floor((r + 0.5) / G) for r < 2^20
   const int R = a.n_tok * G;
-  // Work unit (KV head g, key range split, row block): one block of query
-  // rows per workgroup.  Units are numbered XCD-major (workgroup b runs on
+  // Work unit (KV head g, key range split, row block), or (g, split) with
+  // every row block in turn when the launch does not split the row blocks
+  // (a.rb_split = 0).  Units are numbered XCD-major (workgroup b runs on
   // XCD b % 8) with the row block fastest, so the workgroups that read the
-  // same key range of a grouped-query head sit on one XCD and share its L2.
-  const int n_rb = (R + RB - 1) / RB;
+  // same key range sit on one XCD and share its L2.
+  const int n_rb = LOOP ? 1 : (R + RB - 1) / RB;
   const int nb = gridDim.x;
   const int unit = (nb & 7) == 0 ? (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3) : blockIdx.x;
   const int rb0 = (unit % n_rb) * RB;
@@ -202,7 +207,7 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
   i32x4 vf[MS];
 
   // one block of query rows (its staging loads already issued)
-  auto row_block = [&](int rb) {
+  auto row_block = [&](int rb, bool first) {
     // ---- stage the block's query rows and ancestor masks
 #pragma unroll
     for (int j = 0; j < QPT; ++j) {
@@ -251,7 +256,7 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
       mx = max_x32(max_x16(mx));
       if (lg == 0) smax[w][rt * 16 + lr] = mx;
     }
-    {
+    if (first) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < MS; ++j) {
@@ -345,10 +350,17 @@ __global__ __launch_bounds__(D * 4, 2) void k_attn(AttnArgs a) {
         *(float2 *)&a.part_ml[(base + r) * 2] = make_float2(M == -INFINITY ? M : M * a.scale, L);
       }
     }
+    lds_barrier();  // sp, sq, sanc, smax, ssum free for the next row block
   };
-  // straight after the cache reads (only the staging loads are waited for
-  // before scoring starts)
-  row_block(rb0);
+  // the first block straight after the cache reads (no loop around it, so
+  // the cache registers are not loop-carried and only the staging loads are
+  // waited for before scoring starts)
+  row_block(rb0, true);
+  if constexpr (LOOP)
+    for (int rb = RB; rb < R; rb += RB) {
+      stage_loads(rb);
+      row_block(rb, false);
+    }
 }
 
 // Combines the key ranges of one (row t, query head) and writes the
@@ -526,35 +538,86 @@ __global__ __launch_bounds__(kMergeThreads) void k_attn_merge_reg(AttnArgs a,
 
 }  // namespace
 
-int attn_row_tiles(int rows) { return rows >= 16 * kAttnMaxRowTiles ? kAttnMaxRowTiles : (rows + 15) / 16; }
+int attn_row_tiles(int rows) {
+  // row blocks of at most kAttnMaxRowTiles tiles, as even as the tile count
+  // allows
+  const int tiles = (rows + 15) / 16;
+  const int n_rb = (tiles + kAttnMaxRowTiles - 1) / kAttnMaxRowTiles;
+  return (tiles + n_rb - 1) / n_rb;
+}
+
+bool attn_rb_split(int n_kv, int head_dim, int nkeys, int rows) {
+  // a workgroup per row block while the launch stays within a few rounds
+  // of workgroups; beyond that each workgroup walks its row blocks and
+  // reads its keys once
+  const int rt = attn_row_tiles(rows);
+  const int n_rb = (rows + 16 * rt - 1) / (16 * rt);
+  if (n_rb == 1) return true;
+  const int steps = (nkeys + 31) / 32;
+  const int ms2 = 2 * (head_dim / 16);
+  return (long long)n_kv * n_rb * ((steps + ms2 - 1) / ms2) <= 4LL * kAttnCUs;
+}
+
+int attn_steps_per_wave(int n_kv, int head_dim, int nkeys, int rows) {
+  // two steps per wave while the workgroups fit the compute units at one
+  // each; beyond that one step, two workgroups per unit (row blocks of up
+  // to 3 tiles: the LDS of a 4-tile block leaves room for one)
+  const int steps = (nkeys + 31) / 32;
+  const int rt = attn_row_tiles(rows);
+  const int n_rb = (rows + 16 * rt - 1) / (16 * rt);
+  // a workgroup that walks several row blocks keeps its keys in registers
+  // across them: two steps per wave (the one-step form spills there)
+  if (n_rb > 1 && !attn_rb_split(n_kv, head_dim, nkeys, rows)) return 2;
+  const int ms2 = 2 * (head_dim / 16);
+  const long long units2 = (long long)n_kv * n_rb * ((steps + ms2 - 1) / ms2);
+  return units2 > kAttnCUs && rt <= 3 ? 1 : 2;
+}
 
 int attn_splits(int n_kv, int head_dim, int nkeys, int rows) {
-  // at most 2 head_dim / 16 steps of 32 keys per workgroup, and about
+  // at most SW head_dim / 16 steps of 32 keys per workgroup, and about
   // kAttnTargetGroups workgroups in all (key ranges x row blocks) while
   // every one has a step
   const int steps = (nkeys + 31) / 32;
-  const int ms = 2 * (head_dim / 16);
-  const int n_rb = (rows + 16 * attn_row_tiles(rows) - 1) / (16 * attn_row_tiles(rows));
+  const int ms = attn_steps_per_wave(n_kv, head_dim, nkeys, rows) * (head_dim / 16);
+  const int n_rb = attn_rb_split(n_kv, head_dim, nkeys, rows)
+                       ? (rows + 16 * attn_row_tiles(rows) - 1) / (16 * attn_row_tiles(rows))
+                       : 1;
   int sp = (steps + ms - 1) / ms;
   const int fill = (kAttnTargetGroups + n_kv * n_rb - 1) / (n_kv * n_rb);
   if (sp < fill) sp = fill < steps ? fill : steps;
   return sp < 1 ? 1 : sp;
 }
 
+template <int D, int SW, bool LOOP>
+hipError_t launch_attn_dsw(const AttnArgs &a, int rt, const dim3 &grid, hipStream_t s) {
+  const dim3 block(D * 4);
+  switch (rt) {
+    case 1: hipLaunchKernelGGL((k_attn<D, 1, SW, LOOP>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_attn<D, 2, SW, LOOP>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_attn<D, 3, SW, LOOP>), grid, block, 0, s, a); break;
+    default:
+      if constexpr (SW == 2) {
+        hipLaunchKernelGGL((k_attn<D, 4, SW, LOOP>), grid, block, 0, s, a);
+        break;
+      } else {
+        return hipErrorInvalidValue;
+      }
+  }
+  return hipGetLastError();
+}
+
 template <int D>
 hipError_t launch_attn_d(const AttnArgs &a, hipStream_t s) {
   const int rows = a.n_tok * (a.n_heads / a.n_kv);
+  const int nkeys = a.kv_len + a.n_tok;
   const int rt = attn_row_tiles(rows);
   const int n_rb = (rows + 16 * rt - 1) / (16 * rt);
-  const dim3 grid(a.n_kv * a.n_chunks * n_rb);
-  const dim3 block(D * 4);
-  switch (rt) {
-    case 1: hipLaunchKernelGGL((k_attn<D, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_attn<D, 2>), grid, block, 0, s, a); break;
-    case 3: hipLaunchKernelGGL((k_attn<D, 3>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((k_attn<D, 4>), grid, block, 0, s, a); break;
-  }
-  return hipGetLastError();
+  const bool loop = n_rb > 1 && !attn_rb_split(a.n_kv, D, nkeys, rows);
+  const dim3 grid(a.n_kv * a.n_chunks * (loop ? 1 : n_rb));
+  const bool one = attn_steps_per_wave(a.n_kv, D, nkeys, rows) == 1;
+  if (loop)
+    return one ? launch_attn_dsw<D, 1, true>(a, rt, grid, s) : launch_attn_dsw<D, 2, true>(a, rt, grid, s);
+  return one ? launch_attn_dsw<D, 1, false>(a, rt, grid, s) : launch_attn_dsw<D, 2, false>(a, rt, grid, s);
 }
 
 hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s) {

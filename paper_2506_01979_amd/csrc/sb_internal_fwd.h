@@ -219,7 +219,10 @@ bool resid_norm_fusable(int tiles, int ks, int n_tok, int *groups);
 // the head's group).
 constexpr int kAttnTargetGroups = 192;
 constexpr int kAttnMaxRowTiles = 4;
+constexpr int kAttnCUs = 256;  // compute units the launch shape is planned for (MI355X)
 int attn_row_tiles(int rows);
+int attn_steps_per_wave(int n_kv, int head_dim, int nkeys, int rows);
+bool attn_rb_split(int n_kv, int head_dim, int nkeys, int rows);
 int attn_splits(int n_kv, int head_dim, int nkeys, int rows);
 hipError_t launch_attn_bf16(const AttnArgs &a, hipStream_t s);
 hipError_t launch_attn_merge_bf16(const AttnArgs &a, uint16_t *out_packed, int out_ks,

@@ -235,7 +235,7 @@ def test_llama7b_two_layers(api):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("prefix,B,k", [(512, 1, 4), (8192, 8, 16)])
+@pytest.mark.parametrize("prefix,B,k", [(512, 1, 4), (8192, 4, 8), (8192, 8, 16)])
 def test_llama13b_two_layers(api, prefix, B, k):
     shape = synth.SHAPES["llama13b"].with_layers(2)
     say(f"full-width 13B slice: prefix {prefix}, tree {B}x{k}")
