@@ -29,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, vendor figure
+MFMA_PEAK_TFS = 2500.0  # MI355X dense bf16 matrix-core peak, vendor figure
 DOMINANT = "gate_up"    # kernel class holding the most bytes per step
 
 
@@ -334,6 +335,117 @@ def algorithmic_bytes(shape, P_kv: int, n: int) -> dict:
             "prefix_kv": prefix_kv, "gate_up_launch": gate_up}
 
 
+def class_bytes(shape, P_kv: int, n: int, split_down: int = 4) -> dict:
+    """Algorithmic bytes of one launch per kernel class (the weight or KV
+    stream it must read once, plus its activation inputs and outputs)."""
+    H, F, V = shape.hidden, shape.ffn, shape.vocab
+    qd, kvd = shape.q_dim, shape.kv_dim
+    return {
+        "qkv": H * (qd + 2 * kvd) * 2 + n * H * 2 + n * (qd + 2 * kvd) * 2,
+        "o": qd * H * 2 + n * qd * 2 + n * H * 4 * 2 + n * H * 2,
+        "gate_up": 2 * F * H * 2 + n * H * 2 + n * F * 2,
+        "down": F * H * 2 + n * F * 2 + split_down * n * H * 4,
+        "lm_head": V * H * 2 + n * H * 2 + n * V * 4,
+        "attn": 2 * (P_kv + n) * kvd * 2 + n * qd * 2,
+    }
+
+
+def counter_summary(fetch_dir: str, write_dir: str, mfma_dir: str, workload: str = WORKLOAD) -> str:
+    """Markdown summary of three rocprofv3 --pmc runs of `bench.py
+    --copy-calibration` (FETCH_SIZE; WRITE_SIZE; SQ_VALU_MFMA_BUSY_CYCLES,
+    SQ_INSTS_VALU_MFMA_MOPS_BF16, GRBM_GUI_ACTIVE with --kernel-trace): per
+    kernel class of the last timed steps, HBM bytes per launch (each counter
+    scaled by what it reads for the final device copy of COPY_BYTES bytes)
+    against the class's algorithmic bytes, and the matrix cores' busy share
+    and bf16 FLOPs."""
+    import csv
+    import glob
+    from paper_2506_01979_amd import synth
+    w = synth.WORKLOADS[workload]
+    shape = w.shape
+    per = {}
+    scales = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _counter_rows(d)
+        copy = rows[-1]
+        if "copy" not in copy["name"].lower():
+            raise RuntimeError(f"last dispatch of {d} is not the calibration copy: {copy['name']}")
+        scales[counter] = (COPY_BYTES / (copy["values"][counter] * 1024.0), copy["name"],
+                           copy["values"][counter])
+        for c, r in _step_dispatches(rows, PMC_STEPS):
+            per.setdefault(c, {}).setdefault(counter, []).append(r["values"][counter])
+    rows = _counter_rows(mfma_dir)
+    names = {}
+    for c, r in _step_dispatches(rows, PMC_STEPS):
+        e = per.setdefault(c, {})
+        for k in ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "GRBM_GUI_ACTIVE"):
+            e.setdefault(k, []).append(r["values"].get(k, 0.0))
+        names[c] = r["name"].replace("sb::(anonymous namespace)::", "")
+    # kernel durations of the counter run (--kernel-trace in the same pass)
+    dur = {}
+    trace = glob.glob(os.path.join(mfma_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if trace:
+        tr = sorted(csv.DictReader(open(trace[0])), key=lambda r: int(r["Start_Timestamp"]))
+        recs = [{"name": r["Kernel_Name"], "d": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3}
+                for r in tr]
+        for c, r in _step_dispatches(recs, PMC_STEPS):
+            dur.setdefault(c, []).append(r["d"])
+    simds = 4 * 256
+    cb = class_bytes(shape, w.kv_len, w.n_rows)
+    mean = lambda xs: sum(xs) / len(xs) if xs else float("nan")
+    out = [f"# Hardware counters per kernel class of the verify step, {workload}", "",
+           "Commands (each its own run): `cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc FETCH_SIZE "
+           "--output-format csv -d <repo>/out/pmc_fetch -o run -- python3 <repo>/bench.py --steps 3 "
+           "--warmup 1 --no-cpu-baseline --no-alpha-sweep --no-hrad --no-draft --no-graph "
+           "--copy-calibration`; the same with `--pmc WRITE_SIZE` into out/pmc_write; the same with "
+           "`--kernel-trace --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 GRBM_GUI_ACTIVE` "
+           "into out/pmc_mfma; then `python3 bench.py --counter-summary out/pmc_fetch out/pmc_write "
+           "out/pmc_mfma`.", "",
+           f"HBM bytes: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) times the factor that makes a "
+           f"plain device copy of {COPY_BYTES} bytes read and write that many "
+           f"(FETCH x {scales['FETCH_SIZE'][0]:.4f}, WRITE x {scales['WRITE_SIZE'][0]:.4f}; "
+           f"copy kernel `{scales['FETCH_SIZE'][1]}`).  Matrix-core work: bf16 MFMA FLOPs = "
+           "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 per launch (padded token rows included; the "
+           "attention's P.V product counts twice, hi and lo parts), over the launch's duration in "
+           f"the same run: the MFMA utilisation is that rate against the dense bf16 peak "
+           f"({MFMA_PEAK_TFS:.0f} TFLOP/s).  Busy share: SQ_VALU_MFMA_BUSY_CYCLES / "
+           f"(GRBM_GUI_ACTIVE / 8 XCDs x {simds} SIMDs) (the counter file sums GRBM_GUI_ACTIVE over "
+           "the 8 XCDs).  The counter run serialises kernels, so its durations, and the rates, "
+           "are a little below the untraced run's.", "",
+           "| class | launches/step | HBM read MB | HBM write MB | algorithmic MB | traffic / algorithmic "
+           "| bf16 MFMA GFLOP per launch | TFLOP/s | MFMA utilisation % | MFMA busy % |",
+           "|---|---|---|---|---|---|---|---|---|---|"]
+    recs = {}
+    order = ["qkv", "attn", "attn_merge", "o", "norm", "gate_up", "down", "lm_head", "stats", "embed"]
+    for c in order:
+        e = per.get(c)
+        if not e or "FETCH_SIZE" not in e:
+            continue
+        n_l = len(e["FETCH_SIZE"]) / PMC_STEPS
+        rd = mean(e["FETCH_SIZE"]) * 1024 * scales["FETCH_SIZE"][0]
+        wr = mean(e["WRITE_SIZE"]) * 1024 * scales["WRITE_SIZE"][0]
+        busy = mean([b / (g / 8 * simds) * 100 if g else 0.0 for b, g in
+                     zip(e.get("SQ_VALU_MFMA_BUSY_CYCLES", []), e.get("GRBM_GUI_ACTIVE", []))])
+        flops = mean(e.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", [])) * 512
+        d = mean(dur.get(c, []))
+        tfs = flops / (d * 1e-6) / 1e12 if d == d and d > 0 else float("nan")
+        alg = cb.get(c)
+        ratio = (rd + wr) / alg if alg else None
+        out.append(f"| {c} | {n_l:.0f} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | "
+                   f"{alg / 1e6:.2f} | {ratio:.3f} | " if alg else
+                   f"| {c} | {n_l:.0f} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | — | — | ")
+        util = tfs / MFMA_PEAK_TFS * 100 if tfs == tfs else float("nan")
+        out[-1] += f"{flops / 1e9:.2f} | {tfs:.1f} | {util:.2f} | {busy:.2f} |"
+        recs[c] = {"read_bytes": int(rd), "write_bytes": int(wr), "algorithmic_bytes": alg,
+                   "bf16_flops": int(flops), "tflops": round(tfs, 2) if tfs == tfs else None,
+                   "mfma_util_pct": round(util, 3) if util == util else None,
+                   "mfma_busy_pct": round(busy, 3),
+                   "duration_us_counter_run": round(d, 2) if d == d else None}
+    out += ["", "Kernels: " + "; ".join(f"{c} `{names[c]}`" for c in order if c in names), "",
+            json.dumps({"workload": workload, "classes": recs, "gemm_source_sha256": gemm_source_sha()}), ""]
+    return "\n".join(out)
+
+
 def partial_tree(parents, depth: int):
     """Rows of the tree with depth < `depth`, in ascending row order, with
     parents re-indexed; returns (rows, parents)."""
@@ -572,6 +684,8 @@ def main():
                     help="end with a device copy of known size (for rocprofv3 --pmc runs)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs of this script and exit")
+    ap.add_argument("--counter-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "MFMA_DIR"),
+                    help="per-class summary of three rocprofv3 --pmc runs of this script and exit")
     ap.add_argument("--draft-trace-summary", metavar="TRACE_DIR",
                     help="print the draft-side summary of a rocprofv3 kernel trace and exit")
     ap.add_argument("--trace-summary", metavar="TRACE_DIR",
@@ -583,6 +697,9 @@ def main():
     args = ap.parse_args()
     if args.pmc_summary:
         print(pmc_summary(*args.pmc_summary))
+        return
+    if args.counter_summary:
+        print(counter_summary(*args.counter_summary, args.workload))
         return
     if args.trace_summary:
         print(trace_summary(args.trace_summary, args.workload))

@@ -576,15 +576,18 @@ int attn_steps_per_wave(int n_kv, int head_dim, int nkeys, int rows) {
 int attn_splits(int n_kv, int head_dim, int nkeys, int rows) {
   // at most SW head_dim / 16 steps of 32 keys per workgroup, and about
   // kAttnTargetGroups workgroups in all (key ranges x row blocks) while
-  // every one has a step
+  // every one has kAttnMinSteps steps (shorter ranges cost more in partials
+  // and merging than the extra workgroups gain)
   const int steps = (nkeys + 31) / 32;
   const int ms = attn_steps_per_wave(n_kv, head_dim, nkeys, rows) * (head_dim / 16);
   const int n_rb = attn_rb_split(n_kv, head_dim, nkeys, rows)
                        ? (rows + 16 * attn_row_tiles(rows) - 1) / (16 * attn_row_tiles(rows))
                        : 1;
   int sp = (steps + ms - 1) / ms;
-  const int fill = (kAttnTargetGroups + n_kv * n_rb - 1) / (n_kv * n_rb);
-  if (sp < fill) sp = fill < steps ? fill : steps;
+  int fill = (kAttnTargetGroups + n_kv * n_rb - 1) / (n_kv * n_rb);
+  const int most = (steps + kAttnMinSteps - 1) / kAttnMinSteps;
+  if (fill > most) fill = most;
+  if (sp < fill) sp = fill;
   return sp < 1 ? 1 : sp;
 }
 

@@ -217,7 +217,8 @@ bool resid_norm_fusable(int tiles, int ks, int n_tok, int *groups);
 // Key ranges per KV head: about kAttnTargetGroups workgroups in all, one per
 // (KV head, key range, block of at most 16 kAttnMaxRowTiles query rows of
 // the head's group).
-constexpr int kAttnTargetGroups = 192;
+constexpr int kAttnTargetGroups = 256;
+constexpr int kAttnMinSteps = 4;
 constexpr int kAttnMaxRowTiles = 4;
 constexpr int kAttnCUs = 256;  // compute units the launch shape is planned for (MI355X)
 int attn_row_tiles(int rows);
