@@ -1090,15 +1090,17 @@ def main():
                    "rows": n, "prefix": P, "branches": B,
                    "depth": kd if args.tree == "branch" else args.trunk + args.fork_depth,
                    "alpha": args.alpha},
-        "roofline": {"bound": "hbm", "kernel": f"k_gemm (gate/up + SwiGLU), {k_launches} launches",
-                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.workload),
-                     "avg_us": round(k_avg_ms * 1e3, 2)},
         "step_hbm": {"bytes": nbytes["step"],
                      "achieved_gbs": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9, 1),
                      "frac": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "ms_per_step_with_kernel_events": round(evented_ms, 4),
                      "ms_per_step_graph_replay": None if graph_ms is None else round(graph_ms, 4)},
+        "roofline": {"bound": "hbm", "scope": "per kernel: the dominant kernel of the step "
+                     "(the step as a whole is step_hbm)",
+                     "kernel": f"k_gemm (gate/up + SwiGLU), {k_launches} launches",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.workload),
+                     "avg_us": round(k_avg_ms * 1e3, 2)},
         "accepted": r["n_accepted"],
     }
     if hrad_out is not None:
@@ -1108,18 +1110,25 @@ def main():
         out["overlap"] = round_out
 
     if not args.no_alpha_sweep:
+        # committed tokens per step under the q mixture of each alpha: every
+        # sample draws a fresh draft tree (its own seed) and its own uniforms,
+        # verifies it and walks it
         sweep = {}
+        n_samples = 16
         for a in (0.3, 0.6, 0.9):
-            toks_a, q_a = make_drafts(api, synth, m, k_, v_, kv_len, root, parents, a, w.q_temp, 21)
-            dt, dq = torch.from_numpy(toks_a).to(dev), torch.from_numpy(q_a).to(dev)
-            m.sb_verify_forward(k_, v_, kv_len, dt, parents, 1.0, logits, stats, ws, stream)
             lens = []
-            for s in range(32):
-                du = torch.from_numpy(synth.uniforms(n, 100 + s)).to(dev)
+            for smp in range(n_samples):
+                toks_a, q_a = make_drafts(api, synth, m, k_, v_, kv_len, root, parents, a,
+                                          w.q_temp, 1000 + smp)
+                dt, dq = torch.from_numpy(toks_a).to(dev), torch.from_numpy(q_a).to(dev)
+                m.sb_verify_forward(k_, v_, kv_len, dt, parents, 1.0, logits, stats, ws, stream)
+                du = torch.from_numpy(synth.uniforms(n, 100 + smp)).to(dev)
                 api.sb_accept_resample(dt, parents, logits, stats, 1.0, dq, du, res, sws, stream)
                 lens.append(api.decode_result(res)["n_accepted"] + 1)
             mean = float(np.mean(lens))
             sweep[str(a)] = {"mean_committed": round(mean, 3),
+                             "stderr": round(float(np.std(lens, ddof=1) / np.sqrt(n_samples)), 3),
+                             "samples": n_samples,
                              "committed_tokens_per_s": round(mean / (ms_per_step * 1e-3), 1)}
         out["alpha_sweep"] = sweep
 

@@ -244,3 +244,71 @@ def test_draft_round_properties_68m_bf16(api):
                 assert np.all(qq[1 + i][~live] == 0)
                 ratio = qq[1 + i][live] / qq[0][live]
                 assert np.allclose(ratio, ratio[0], rtol=1e-6)
+
+
+def test_draft_round_68m_bf16_replays_the_oracle(api):
+    """The 68M bf16 draft's round checked against the oracle by replay: the
+    oracle's bfloat16 forward of the round's own tree gives every q row the
+    GPU drew from to the bf16 logits bound (2e-2 row-relative, compared as
+    T log q, which is the logits up to a per-row constant); every decision
+    -- each chain and continuation token, x_b and with it B, the candidates
+    and their rows -- is the oracle's draw from the GPU's own q rows with the
+    same uniforms, exactly.  The replay draws from the very rows the GPU
+    drew from, so the two sides differ only in the float64 summation order
+    of the running sums (about 1e-13 relative): no decision of these seeds
+    lies within 1e-10 of its threshold, which the test checks."""
+    from oracle import sampling
+    shape = synth.SHAPES["draft68m"]
+    P, k_max, depth, T, trunk = 256, 6, 4, 1.0, 3
+    W = synth.model_weights(shape, seed=7)
+    m = api.Model(shape, api.synth_tensors(shape, seed=7))
+    Kb = np.stack([synth.synthetic_kv(shape, li, P, P, 0, as_bits=True) for li in range(shape.n_layers)])
+    Vb = np.stack([synth.synthetic_kv(shape, li, P, P, 1, as_bits=True) for li in range(shape.n_layers)])
+    Kf, Vf = synth.bits_to_f32(Kb), synth.bits_to_f32(Vb)
+    R = trunk + k_max * depth
+    for mode in branching.MODES:
+        k, v = m.new_kv(P + R)
+        m.load_kv(k, v, Kb, Vb, P)
+        u = synth.uniforms(R, seed=23)
+        toks = torch.full((R,), -5, dtype=torch.int32, device="cuda")
+        toks[0] = 17
+        q = torch.full((R, shape.vocab), 7.0, dtype=torch.float32, device="cuda")
+        ws = m.draft_round_workspace(k_max, depth, P, trunk)
+        say(f"draft round 68m bf16 replay {mode}")
+        # threshold 0: every draw is confident, the chain holds trunk - 1
+        B, par, c = m.sb_draft_round(k, v, P, k_max, mode, depth, T, torch.from_numpy(u).cuda(),
+                                     toks, q, ws, trunk_max=trunk, confidence=0.0)
+        torch.cuda.synchronize()
+        tk, qg = toks.cpu().numpy(), q.cpu().numpy()
+        assert c == trunk - 1 and 1 <= B <= k_max
+        n = 1 + c + B * depth
+        tree_toks = tk[:n].copy()
+        # the oracle forward of the round's tree: row i's logits give the
+        # distribution of i's children
+        lg, _, _ = decoder.tree_forward(shape, W, Kf, Vf, P, tree_toks, par, "bf16")
+        src = {0: c}                                   # row 0 holds q at the branch position
+        for i in range(1, c + 1):
+            src[i] = i - 1                             # chain drafts
+        for i in range(c + 1 + B, n):
+            src[i] = int(par[i])                       # continuations
+        for i, s in src.items():
+            ref = lg[s].astype(np.float64) / T
+            got = np.log(qg[i].astype(np.float64)) * 1.0
+            d = (got - got.mean()) - (ref - ref.mean())
+            assert np.max(np.abs(d)) <= 2e-2 * np.max(np.abs(ref - ref.mean())) * 2, (mode, i)
+
+        def draw(row, uu):
+            w = qg[row].astype(np.float64)
+            assert cum_margin(qg[row], uu) >= 1e-10
+            return sampling.draw(w, float(uu))
+        for t in range(1, c + 1):                      # the chain
+            assert tk[t] == draw(t, u[t - 1])
+        x_b = draw(0, u[c])                            # the branch point
+        cand, rows = branching.candidates(qg[0], x_b, k_max, mode, u[trunk:trunk + k_max])
+        assert B == len(cand)
+        assert tk[c + 1:c + 1 + B].tolist() == cand.tolist()
+        np.testing.assert_allclose(qg[c + 1:c + 1 + B], rows, rtol=1e-6, atol=1e-12)
+        for d_ in range(2, depth + 1):                 # the continuations
+            for i in range(B):
+                r = c + 1 + (d_ - 1) * B + i
+                assert tk[r] == draw(r, u[trunk + k_max * (d_ - 1) + i])
