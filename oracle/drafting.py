@@ -34,6 +34,7 @@ far with decoder.tree_forward; a row's logits do not depend on later rows.
 """
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass
 
 import numpy as np
@@ -62,12 +63,29 @@ def uniforms_needed(k_max: int, depth: int, trunk_max: int = 1) -> int:
     return trunk_max + k_max * depth
 
 
+def confident_row(q_row, epsilon: float) -> np.ndarray:
+    """q conditioned on confidence: q(v) / q(C) on C = {v : q(v) >= epsilon}
+    (float32 comparisons, q(C) the float64 sum of the float32 values), zero
+    elsewhere, stored as float32.  A chain draft was kept because its own
+    probability reached epsilon, so it was in effect drawn from this row."""
+    q = np.asarray(q_row, dtype=np.float32)
+    keep = q >= np.float32(epsilon)
+    mass = math.fsum(q[keep].astype(np.float64).tolist())
+    out = np.zeros(len(q), dtype=np.float32)
+    if mass > 0.0:
+        out[keep] = (q[keep].astype(np.float64) / mass).astype(np.float32)
+    return out
+
+
 def draft_round(shape, weights: dict, prefix_k, prefix_v, kv_len: int, root_token: int,
                 k_max: int, mode: str, depth: int, T: float, u, prec: str = "f64",
                 trunk_max: int = 1, epsilon: float = float("inf"),
-                trace: list | None = None) -> DraftRound:
+                trace: list | None = None, exact_chain: bool = False) -> DraftRound:
     """With `trace`, every draw is recorded (sampling.draw's events) under
-    the index of its uniform in u."""
+    the index of its uniform in u.  With `exact_chain`, a chain draft carries
+    confident_row(q, epsilon) as the row its test divides by, instead of q
+    (the variant that keeps the round exactly lossless when the chain's
+    length depends on the drafts' own probabilities)."""
     u = np.asarray(u, dtype=np.float32)
     assert depth >= 1 and trunk_max >= 1
     assert len(u) >= uniforms_needed(k_max, depth, trunk_max)
@@ -84,7 +102,7 @@ def draft_round(shape, weights: dict, prefix_k, prefix_v, kv_len: int, root_toke
             break
         toks.append(x_t)
         parents.append(t - 1)
-        q.append(q_t)
+        q.append(confident_row(q_t, epsilon) if exact_chain else q_t)
     c = len(toks) - 1
     q[0] = q_b
     u0 = trunk_max

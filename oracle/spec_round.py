@@ -33,6 +33,13 @@ Resampling"):
 The committed tokens of the round are x_1 .. x_n and the token; with a kept
 branch, its later drafts (depths 2 .. depth) are what the next verification
 phase checks (Algorithm 2 stays in VERIFICATION).
+
+Algorithm 2 tests a chain draft against its q row as drawn.  A draft stays
+in the chain only when its own probability reaches epsilon, so a chain cut
+by that test holds drafts drawn, in effect, from q restricted to the
+confident tokens; with exact_chain each chain draft carries that
+conditioned row instead, which keeps the committed tokens distributed as p
+for any threshold (both forms are pinned by exact enumeration).
 """
 from __future__ import annotations
 
@@ -70,12 +77,14 @@ def spec_round(tshape, tweights: dict, t_prefix_k, t_prefix_v, t_len: int,
                dshape, dweights: dict, d_prefix_k, d_prefix_v, d_len: int, root: int,
                k_max: int, mode: str, depth: int, T: float, u_draft, u_walk, u_sel,
                trunk_max: int = 1, epsilon: float = float("inf"), capacity: int | None = None,
-               prec: str = "f64", trace: list | None = None) -> RoundResult:
+               prec: str = "f64", trace: list | None = None,
+               exact_chain: bool = False) -> RoundResult:
     """One round.  The prefix caches are [n_layers][n_kv][>= len][d]; the
     returned caches have `capacity` slots (default: prefix + every tree
     row).  With `trace`, every decision against a uniform is recorded
     (sampling.draw / branch_select events) with the uniform's index in the
-    concatenation u_draft + u_walk + u_sel."""
+    concatenation u_draft + u_walk + u_sel.  exact_chain: the chain drafts
+    are tested against q conditioned on confidence (drafting.confident_row)."""
     nd, nw, ns = uniforms_needed(k_max, depth, trunk_max)
     u_walk = np.asarray(u_walk, dtype=np.float32)
     u_sel = np.asarray(u_sel, dtype=np.float32)
@@ -89,7 +98,7 @@ def spec_round(tshape, tweights: dict, t_prefix_k, t_prefix_v, t_len: int,
 
     # 1. drafting
     dr = drafting.draft_round(dshape, dweights, d_prefix_k, d_prefix_v, d_len, root, k_max, mode,
-                              depth, T, u_draft, prec, trunk_max, epsilon, sub)
+                              depth, T, u_draft, prec, trunk_max, epsilon, sub, exact_chain)
     record(sub, 0)
     c, B = dr.chain, dr.branches
     n_rows = len(dr.tokens)

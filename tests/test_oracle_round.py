@@ -37,11 +37,12 @@ def models(name, P, seed=2):
     return sh, Wt, Wd, ptoks, Kt, Vt, Kd, Vd
 
 
-def run_round(m, k_max, mode, depth, T, u_d, u_w, u_s, trunk, eps, trace=None):
+def run_round(m, k_max, mode, depth, T, u_d, u_w, u_s, trunk, eps, trace=None, exact=False):
     sh, Wt, Wd, ptoks, Kt, Vt, Kd, Vd = m
     P = len(ptoks) - 1
     return spec_round.spec_round(sh, Wt, Kt, Vt, P, sh, Wd, Kd, Vd, P, int(ptoks[-1]), k_max, mode,
-                                 depth, T, u_d, u_w, u_s, trunk, eps, trace=trace)
+                                 depth, T, u_d, u_w, u_s, trunk, eps, trace=trace,
+                                 exact_chain=exact)
 
 
 @pytest.fixture
@@ -99,13 +100,13 @@ def test_round_is_the_tree_walk_over_chain_and_candidates():
     assert kinds == {"kept", "chain rejected", "candidates rejected"}
 
 
-def enumerate_round(m, k_max, mode, depth, T, trunk, eps):
+def enumerate_round(m, k_max, mode, depth, T, trunk, eps, exact=False):
     nd, nw, ns = spec_round.uniforms_needed(k_max, depth, trunk)
 
     def run(u):
         tr = []
         r = run_round(m, k_max, mode, depth, T, u[:nd], u[nd:nd + nw], u[nd + nw:], trunk, eps,
-                      tr)
+                      tr, exact)
         return r, tr
 
     out = enumerate_outcomes(run, nd + nw + ns, lambda r: tuple(r.committed[:2]))
@@ -162,6 +163,29 @@ def test_confidence_gated_chain_deviates_from_the_target(memo_forward):
 # a chain of 3 accepted and a kept branch; a chain of 2 rejected at its
 # second token; no chain and a kept branch (the second candidate); no chain
 # and every candidate rejected
+@pytest.mark.parametrize("mode", branching.MODES)
+@pytest.mark.parametrize("eps", [0.2, 0.35])
+def test_conditioned_chain_is_lossless_at_any_threshold(memo_forward, mode, eps):
+    # each chain draft tested against q conditioned on confidence: the first
+    # and second committed tokens follow p exactly, with the chain's length
+    # set by the drafts' own probabilities
+    m = models("enum", 4)
+    vol, err1, err2, p2 = enumerate_round(m, 3, mode, 1, 0.3, 3, eps, exact=True)
+    assert vol < 1e-12 and err1 < ENUM_TOL and err2 < ENUM_TOL
+    assert p2 > 0.02                           # the second position is reached
+
+
+def test_confident_row_is_q_restricted_and_renormalised():
+    q = np.array([0.5, 0.05, 0.3, 0.15], dtype=np.float32)
+    from oracle import drafting
+    r = drafting.confident_row(q, 0.15)
+    assert r.dtype == np.float32
+    np.testing.assert_allclose(r, [0.5 / 0.95, 0.0, 0.3 / 0.95, 0.15 / 0.95], rtol=1e-7)
+    assert np.all(drafting.confident_row(q, 0.9) == 0.0)
+    np.testing.assert_allclose(drafting.confident_row(q, 0.0), q / q.astype(np.float64).sum(),
+                               rtol=1e-7)
+
+
 ROLLBACK_CASES = [("wor", 9, 6, 0.08), ("iid", 7, 6, 0.08), ("topk", 1, 1, float("inf")),
                   ("topk", 3, 1, float("inf"))]
 
