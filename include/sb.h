@@ -471,11 +471,21 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
  *   *h_branches = B; d_ws of sb_draft_round_workspace_bytes(draft, k_max,
  *   depth, chain + 1, kv_len) bytes.  Blocks the host once, to read B.
  * The draft's cache slots kv_len .. are written by both, as sb_draft_round
- * writes them.  Errors as sb_draft_round. */
+ * writes them.  Errors as sb_draft_round.
+ * flags of sb_draft_chain: 0, or SB_CHAIN_CONDITIONED: each confident chain
+ *   draft's q row is replaced by q conditioned on confidence, q(v) / q(C) on
+ *   C = {v : q(v) >= confidence} and 0 elsewhere (q(C) the float64 sum of
+ *   C's float32 values, each quotient rounded once to float32).  A draft is
+ *   kept in the chain only when its own probability reaches the threshold,
+ *   so it was in effect drawn from that row; testing it against the row
+ *   keeps the round exactly lossless at any threshold, where Algorithm 2's
+ *   test against the unconditioned q row does not when the chain's length
+ *   depends on the drafts.  Other bits: SB_ERR_INVALID_ARG. */
+#define SB_CHAIN_CONDITIONED 1
 sb_status sb_draft_chain(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t trunk_max,
-                         float confidence, float temperature, const float *d_u, int32_t *d_tokens,
-                         float *d_q, int32_t *d_xb, int32_t *h_chain, void *d_ws, size_t ws_bytes,
-                         hipStream_t stream);
+                         float confidence, int32_t flags, float temperature, const float *d_u,
+                         int32_t *d_tokens, float *d_q, int32_t *d_xb, int32_t *h_chain,
+                         void *d_ws, size_t ws_bytes, hipStream_t stream);
 sb_status sb_draft_branches(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t chain,
                             const int32_t *d_xb, int32_t k_max, int32_t mode, int32_t depth,
                             float temperature, const float *d_u, int32_t *d_tokens, float *d_q,
@@ -507,11 +517,13 @@ sb_status sb_round_finish(int32_t chain, int32_t branches, int32_t depth,
 /* ---- one whole SpecBranch round on two streams ------------------------ */
 
 /* Parameters of a round: the drafting phase's (sb_draft_round's k_max,
- * mode, depth, trunk_max, confidence) and the temperature T >= 0 of both
- * models' distributions. */
+ * mode, depth, trunk_max, confidence), the temperature T >= 0 of both
+ * models' distributions, and flags for sb_draft_chain (0 or
+ * SB_CHAIN_CONDITIONED). */
 typedef struct {
   int32_t k_max, mode, depth, trunk_max;
   float confidence, temperature;
+  int32_t flags;
 } sb_round_params;
 
 /* Workspace bytes of sb_spec_round (0 for arguments it rejects). */

@@ -80,9 +80,13 @@ class HradWeights(C.Structure):
                 ("b2", C.c_void_p), ("w3", C.c_void_p), ("b3", C.c_void_p)]
 
 
+SB_CHAIN_CONDITIONED = 1
+
+
 class RoundParams(C.Structure):
     _fields_ = [("k_max", C.c_int32), ("mode", C.c_int32), ("depth", C.c_int32),
-                ("trunk_max", C.c_int32), ("confidence", C.c_float), ("temperature", C.c_float)]
+                ("trunk_max", C.c_int32), ("confidence", C.c_float), ("temperature", C.c_float),
+                ("flags", C.c_int32)]
 
 
 ROUND_RESULT_INTS = 8
@@ -148,8 +152,8 @@ lib.sb_draft_round.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _i32, _i32, 
                                _vp, _vp, C.POINTER(_i32), C.POINTER(_i32), C.POINTER(_i32), _vp,
                                _sz, _vp]
 lib.sb_draft_chain.restype = _i32
-lib.sb_draft_chain.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _f, _f, _vp, _vp, _vp, _vp,
-                               C.POINTER(_i32), _vp, _sz, _vp]
+lib.sb_draft_chain.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _f, _i32, _f, _vp, _vp, _vp,
+                               _vp, C.POINTER(_i32), _vp, _sz, _vp]
 lib.sb_draft_branches.restype = _i32
 lib.sb_draft_branches.argtypes = [_vp, C.POINTER(KVCache), _i32, _i32, _vp, _i32, _i32, _i32, _f,
                                   _vp, _vp, _vp, C.POINTER(_i32), C.POINTER(_i32), _vp, _sz, _vp]
@@ -292,8 +296,9 @@ def decode_round(r: torch.Tensor) -> dict:
 
 
 def round_params(k_max: int, mode: str, depth: int, trunk_max: int, confidence: float,
-                 temperature: float) -> RoundParams:
-    return RoundParams(k_max, BRANCH_MODES[mode], depth, trunk_max, confidence, temperature)
+                 temperature: float, conditioned: bool = False) -> RoundParams:
+    return RoundParams(k_max, BRANCH_MODES[mode], depth, trunk_max, confidence, temperature,
+                       SB_CHAIN_CONDITIONED if conditioned else 0)
 
 
 def sb_spec_round_workspace_bytes(target, draft, params: RoundParams, t_len: int,
@@ -683,7 +688,7 @@ class Model:
     def sb_draft_chain(self, k: torch.Tensor, v: torch.Tensor, kv_len: int, trunk_max: int,
                        confidence: float, temperature: float, u: torch.Tensor,
                        tokens: torch.Tensor, q: torch.Tensor, xb: torch.Tensor, ws: torch.Tensor,
-                       stream=None) -> int:
+                       stream=None, conditioned: bool = False) -> int:
         """tokens int32 / q float32 [>= trunk_max + 1]([vocab]), tokens[0] the
         root; u float32 [trunk_max]; xb int32 [1]; ws of
         draft_round_workspace(1, 1, kv_len, trunk_max).  Returns c."""
@@ -696,6 +701,7 @@ class Model:
         nc = C.c_int32(0)
         kv = KVCache(k.data_ptr(), v.data_ptr(), k.shape[2])
         _check(lib.sb_draft_chain(self.handle, C.byref(kv), kv_len, trunk_max, confidence,
+                                  SB_CHAIN_CONDITIONED if conditioned else 0,
                                   temperature, u.data_ptr(), tokens.data_ptr(), q.data_ptr(),
                                   xb.data_ptr(), C.byref(nc), ws.data_ptr(),
                                   ws.numel() * ws.element_size(), _stream(stream)),

@@ -968,11 +968,11 @@ static sb_status draft_sample_rows(const sb_model *draft, char *ws, const RoundL
 }
 
 sb_status sb_draft_chain(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t trunk_max,
-                         float confidence, float temperature, const float *d_u, int32_t *d_tokens,
-                         float *d_q, int32_t *d_xb, int32_t *h_chain, void *d_ws, size_t ws_bytes,
-                         hipStream_t stream) {
+                         float confidence, int32_t flags, float temperature, const float *d_u,
+                         int32_t *d_tokens, float *d_q, int32_t *d_xb, int32_t *h_chain,
+                         void *d_ws, size_t ws_bytes, hipStream_t stream) {
   if (!draft_args_ok(draft, kv, temperature) || !d_u || !d_tokens || !d_q || !d_xb || !h_chain ||
-      !d_ws || isnan(confidence))
+      !d_ws || isnan(confidence) || (flags & ~SB_CHAIN_CONDITIONED) != 0)
     return SB_ERR_INVALID_ARG;
   RoundLayout L;
   if (!round_layout(draft, 1, 1, trunk_max, kv_len, &L)) return SB_ERR_INVALID_ARG;
@@ -1022,6 +1022,11 @@ sb_status sb_draft_chain(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
       *h_chain = t - 1;
       return SB_OK;
     }
+    // a confident draft: with SB_CHAIN_CONDITIONED its row becomes q
+    // conditioned on confidence, the row its test divides by
+    if ((flags & SB_CHAIN_CONDITIONED) &&
+        launch_confident_row(d_q + (size_t)t * V, V, confidence, stream) != hipSuccess)
+      return SB_ERR_HIP;
     par[t] = t - 1;
   }
   return SB_ERR_INVALID_ARG;  // not reached: t == trunk_max returns
@@ -1105,7 +1110,7 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
   // three ints when the sizes coincide
   int32_t *xb = (int32_t *)((char *)d_ws + L.ints) + 3;
   int32_t c = 0;
-  sb_status st = sb_draft_chain(draft, kv, kv_len, trunk_max, confidence, temperature, d_u,
+  sb_status st = sb_draft_chain(draft, kv, kv_len, trunk_max, confidence, 0, temperature, d_u,
                                 d_tokens, d_q, xb, &c, d_ws, ws_bytes, stream);
   if (st != SB_OK) return st;
   st = sb_draft_branches(draft, kv, kv_len, c, xb, k_max, mode, depth, temperature,
@@ -1180,7 +1185,8 @@ sb_status sb_spec_round(sb_model *target, const sb_kv_cache *t_kv, int32_t t_len
       !d_u_sel || !d_tokens || !d_q || !d_logits || !d_stats || !d_walk || !d_select ||
       !d_round || !d_new_lens || !h_parents || !h_chain || !h_branches || !d_ws)
     return SB_ERR_INVALID_ARG;
-  if (!t_kv->k || !t_kv->v || !temperature_ok(p->temperature) || isnan(p->confidence))
+  if (!t_kv->k || !t_kv->v || !temperature_ok(p->temperature) || isnan(p->confidence) ||
+      (p->flags & ~SB_CHAIN_CONDITIONED) != 0)
     return SB_ERR_INVALID_ARG;
   SpecLayout L;
   if (!spec_layout(target, draft, p, t_len, d_len, &L)) return SB_ERR_INVALID_ARG;
@@ -1196,8 +1202,8 @@ sb_status sb_spec_round(sb_model *target, const sb_kv_cache *t_kv, int32_t t_len
 
   // drafting phase: the chain up to the branch point
   int32_t c = 0;
-  sb_status st = sb_draft_chain(draft, d_kv, d_len, p->trunk_max, p->confidence, T, d_u_draft,
-                                d_tokens, d_q, xb, &c, ws, L.draft.total, draft_stream);
+  sb_status st = sb_draft_chain(draft, d_kv, d_len, p->trunk_max, p->confidence, p->flags, T,
+                                d_u_draft, d_tokens, d_q, xb, &c, ws, L.draft.total, draft_stream);
   if (st != SB_OK) return st;
   if (hipEventRecord(chain_done.e, draft_stream) != hipSuccess ||
       hipStreamWaitEvent(verify_stream, chain_done.e, 0) != hipSuccess)

@@ -1066,7 +1066,30 @@ __global__ __launch_bounds__(kDraftThreads) void k_draft_draw(int vocab, int nbl
   }
 }
 
+// A chain draft's q row conditioned on confidence, in place: q(v) / q(C)
+// on C = {v : q(v) >= eps} (float32 comparisons), zero elsewhere, with q(C)
+// the float64 sum of C's float32 values and each quotient rounded once to
+// float32.  A row with no confident token is left all zero.
+__global__ __launch_bounds__(kWalkThreads) void k_confident_row(float *q, int vocab, float eps) {
+  __shared__ double red[kWaves + 1];
+  double part = 0.0;
+  for (int v = threadIdx.x; v < vocab; v += kWalkThreads) {
+    const float x = q[v];
+    if (x >= eps) part += (double)x;
+  }
+  const double mass = block_sum<kWaves>(part, red);
+  for (int v = threadIdx.x; v < vocab; v += kWalkThreads) {
+    const float x = q[v];
+    q[v] = x >= eps && mass > 0.0 ? (float)((double)x / mass) : 0.0f;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_confident_row(float *q, int vocab, float eps, hipStream_t s) {
+  hipLaunchKernelGGL(k_confident_row, dim3(1), dim3(kWalkThreads), 0, s, q, vocab, eps);
+  return hipGetLastError();
+}
 
 size_t sample_ws_bytes(int vocab) { return (size_t)2 * (size_t)vocab * sizeof(double); }
 

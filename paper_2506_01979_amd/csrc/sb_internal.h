@@ -36,6 +36,8 @@ hipError_t launch_draft_sample(int vocab, const DraftRows &rows, const float *lo
                                const sb_row_stats *stats, float temperature, const float *u,
                                int32_t *tokens, float *q, void *ws, hipStream_t s,
                                float *conf = nullptr);
+// A q row conditioned on confidence, in place (q / q(C) on C = {q >= eps}).
+hipError_t launch_confident_row(float *q, int vocab, float eps, hipStream_t s);
 
 // ---- rollback (k_rollback.hip) ---------------------------------------------
 hipError_t launch_round_finish(int chain, int branches, int depth, const sb_step_result *walk,

@@ -59,9 +59,16 @@ ROUND_CASES = [
     ("tiny", 96, 4, "iid", 3, 0.6, 0, 5, 0.004),    # 2 layers, vocabulary 1024: third kept
     ("tiny", 96, 4, "wor", 3, 0.1, 6, 5, 0.02),     # a chain of 4 on the wider model
 ]
+# chain drafts tested against q conditioned on confidence (SB_CHAIN_CONDITIONED)
+COND_CASES = [
+    ("exact", 8, 4, "wor", 3, 0.25, 1, 5, 0.08),
+    ("exact", 8, 4, "iid", 3, 0.25, 8, 5, 0.08),
+    ("exact", 8, 4, "topk", 3, 0.25, 1, 5, 0.08),
+    ("tiny", 96, 4, "wor", 3, 0.1, 6, 5, 0.02),
+]
 
 
-def oracle_round(name, P, k_max, mode, depth, T, seed, trunk, eps):
+def oracle_round(name, P, k_max, mode, depth, T, seed, trunk, eps, cond=False):
     sh = synth.SHAPES[name]
     Wt, Wd = weights(name)
     ptoks = synth.prefix_tokens(sh.vocab, P + 1, seed)
@@ -71,11 +78,17 @@ def oracle_round(name, P, k_max, mode, depth, T, seed, trunk, eps):
     u = synth.uniforms(nd + nw + ns, seed=seed)
     tr = []
     r = spec_round.spec_round(sh, Wt, Kt, Vt, P, sh, Wd, Kd, Vd, P, int(ptoks[-1]), k_max, mode,
-                              depth, T, u[:nd], u[nd:nd + nw], u[nd + nw:], trunk, eps, trace=tr)
+                              depth, T, u[:nd], u[nd:nd + nw], u[nd + nw:], trunk, eps, trace=tr,
+                              exact_chain=cond)
     # every decision away from its threshold: the draft side's (draws,
-    # confidence tests, B, top-k order, greedy argmaxes) and the
-    # verification's (chain tests, Algorithm 1, draws)
-    stop, whole = first_tie(sh, Wd, Kd, Vd, P, r.draft, k_max, mode, depth, T, u[:nd], trunk, eps)
+    # confidence tests, B, top-k order, greedy argmaxes; taken on the rows
+    # the drafts were drawn from, which the conditioning does not change)
+    # and the verification's (chain tests, Algorithm 1, draws)
+    drawn = r.draft if not cond else spec_round.spec_round(
+        sh, Wt, Kt, Vt, P, sh, Wd, Kd, Vd, P, int(ptoks[-1]), k_max, mode, depth, T, u[:nd],
+        u[nd:nd + nw], u[nd + nw:], trunk, eps).draft
+    assert drawn.tokens.tolist() == r.draft.tokens.tolist()
+    stop, whole = first_tie(sh, Wd, Kd, Vd, P, drawn, k_max, mode, depth, T, u[:nd], trunk, eps)
     assert whole and stop == len(r.draft.tokens), "a draft-side decision within 2e-5"
     assert decision_margin(tr, u) >= 2e-5, "a verification decision within 2e-5"
     if T == 0:
@@ -85,18 +98,19 @@ def oracle_round(name, P, k_max, mode, depth, T, seed, trunk, eps):
     return sh, ptoks, (Kt, Vt, Kd, Vd), u, (nd, nw, ns), r
 
 
-@pytest.mark.parametrize("name,P,k_max,mode,depth,T,seed,trunk,eps", ROUND_CASES)
+@pytest.mark.parametrize("name,P,k_max,mode,depth,T,seed,trunk,eps,cond",
+                         [c + (False,) for c in ROUND_CASES] + [c + (True,) for c in COND_CASES])
 def test_round_matches_oracle_on_two_streams(api, name, P, k_max, mode, depth, T, seed, trunk,
-                                             eps):
+                                             eps, cond):
     sh, ptoks, (Kt, Vt, Kd, Vd), u, (nd, nw, ns), ref = oracle_round(name, P, k_max, mode, depth,
-                                                                      T, seed, trunk, eps)
+                                                                      T, seed, trunk, eps, cond)
     Wt, Wd = weights(name)
     tm = api.Model(sh, api.dict_tensors(Wt))
     dm = api.Model(sh, api.dict_tensors(Wd))
     R = trunk + k_max * depth
     tk, tv = tm.new_kv(P + trunk)
     dk, dv = dm.new_kv(P + R)
-    params = api.round_params(k_max, mode, depth, trunk, eps, T)
+    params = api.round_params(k_max, mode, depth, trunk, eps, T, conditioned=cond)
     buf = api.RoundBuffers(tm, dm, params, P, P)
     ud = torch.from_numpy(u[:nd]).cuda()
     uw = torch.from_numpy(u[nd:nd + nw]).cuda()
