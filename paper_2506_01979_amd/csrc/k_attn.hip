@@ -9,7 +9,7 @@
 // Flash-decoding split: the key range [0, kv_len + n_tok) of each KV head is
 // cut into n_chunks ranges of at most 2 NW 32-key steps (NW = head_dim / 16
 // waves per workgroup); a workgroup takes one range and one block of at
-// most 64 query rows of the KV head's group (with grouped queries a head's
+// most 48 query rows of the KV head's group (with grouped queries a head's
 // group has n_tok G rows; the workgroups of one range sit on one XCD, so
 // its K and V come from HBM once and from that XCD's L2 after).  About one
 // workgroup per compute unit.  The workgroup reads its K rows and rows of
@@ -560,8 +560,7 @@ bool attn_rb_split(int n_kv, int head_dim, int nkeys, int rows) {
 
 int attn_steps_per_wave(int n_kv, int head_dim, int nkeys, int rows) {
   // two steps per wave while the workgroups fit the compute units at one
-  // each; beyond that one step, two workgroups per unit (row blocks of up
-  // to 3 tiles: the LDS of a 4-tile block leaves room for one)
+  // each; beyond that one step, two workgroups per unit
   const int steps = (nkeys + 31) / 32;
   const int rt = attn_row_tiles(rows);
   const int n_rb = (rows + 16 * rt - 1) / (16 * rt);
@@ -570,7 +569,7 @@ int attn_steps_per_wave(int n_kv, int head_dim, int nkeys, int rows) {
   if (n_rb > 1 && !attn_rb_split(n_kv, head_dim, nkeys, rows)) return 2;
   const int ms2 = 2 * (head_dim / 16);
   const long long units2 = (long long)n_kv * n_rb * ((steps + ms2 - 1) / ms2);
-  return units2 > kAttnCUs && rt <= 3 ? 1 : 2;
+  return units2 > kAttnCUs ? 1 : 2;
 }
 
 int attn_splits(int n_kv, int head_dim, int nkeys, int rows) {
@@ -598,13 +597,7 @@ hipError_t launch_attn_dsw(const AttnArgs &a, int rt, const dim3 &grid, hipStrea
     case 1: hipLaunchKernelGGL((k_attn<D, 1, SW, LOOP>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_attn<D, 2, SW, LOOP>), grid, block, 0, s, a); break;
     case 3: hipLaunchKernelGGL((k_attn<D, 3, SW, LOOP>), grid, block, 0, s, a); break;
-    default:
-      if constexpr (SW == 2) {
-        hipLaunchKernelGGL((k_attn<D, 4, SW, LOOP>), grid, block, 0, s, a);
-        break;
-      } else {
-        return hipErrorInvalidValue;
-      }
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

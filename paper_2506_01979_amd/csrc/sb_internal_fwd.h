@@ -219,7 +219,7 @@ bool resid_norm_fusable(int tiles, int ks, int n_tok, int *groups);
 // the head's group).
 constexpr int kAttnTargetGroups = 256;
 constexpr int kAttnMinSteps = 4;
-constexpr int kAttnMaxRowTiles = 4;
+constexpr int kAttnMaxRowTiles = 3;  // 48-row blocks (64: 70B step 0.36 ms slower)
 constexpr int kAttnCUs = 256;  // compute units the launch shape is planned for (MI355X)
 int attn_row_tiles(int rows);
 int attn_steps_per_wave(int n_kv, int head_dim, int nkeys, int rows);
