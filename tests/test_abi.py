@@ -224,3 +224,77 @@ def test_noalloc_rejects_a_step_larger_than_its_scratch_without_device(api):
                                              None) == 1
     finally:
         lib.sb_model_destroy(h)
+
+
+def _fake_model(api, shape_name, n_layers=None):
+    """A model handle over placeholder weight pointers (host arithmetic only:
+    nothing here launches)."""
+    from paper_2506_01979_amd import synth
+    sh = synth.SHAPES[shape_name]
+    L = n_layers or sh.n_layers
+    w = api.ModelWeights(1, 1, 1, (api.LayerWeights * L)(*[api.LayerWeights(1, 1, 1, 1, 1, 1)] * L))
+    c = api.make_config(sh.with_layers(L) if n_layers else sh)
+    h = C.c_void_p()
+    assert api.lib.sb_model_create(C.byref(c), C.byref(w), C.byref(h)) == 0
+    return h, w
+
+
+@pytest.mark.parametrize("shape,rows,prefixes", [
+    ("llama7b", 129, (512, 2048, 4096, 8192)),
+    ("llama13b", 129, (512, 2048, 4096)),
+    ("llama13b", 65, (8192,)),
+    ("llama70b", 33, (512, 4096, 8192)),
+])
+def test_noalloc_scratch_covers_the_stated_steps(api, shape, rows, prefixes):
+    """The allocation-free entry point's 64 MiB array holds the forward's
+    workspace of the steps its documentation names."""
+    h, _w = _fake_model(api, shape)
+    try:
+        for P in prefixes:
+            assert 0 < api.lib.sb_workspace_bytes(h, rows, P - 1) <= api.SB_NOALLOC_SCRATCH_BYTES
+    finally:
+        api.lib.sb_model_destroy(h)
+
+
+def test_round_host_validation_without_device(api):
+    """sb_round_finish and sb_spec_round reject bad arguments before any
+    launch; the round's workspace size is host arithmetic."""
+    lib = api.lib
+    # sb_round_finish: null buffers, negative counts, too many rows, no
+    # selection with candidates
+    assert lib.sb_round_finish(2, 3, 4, None, 1, 1, 1, None) == 1
+    assert lib.sb_round_finish(2, 3, 4, 1, None, 1, 1, None) == 1
+    assert lib.sb_round_finish(-1, 3, 4, 1, 1, 1, 1, None) == 1
+    assert lib.sb_round_finish(2, 3, 0, 1, 1, 1, 1, None) == 1
+    assert lib.sb_round_finish(10, 16, 16, 1, 1, 1, 1, None) == 1     # 1 + 10 + 256 rows
+    t, _wt = _fake_model(api, "small_bf16")
+    d, _wd = _fake_model(api, "small_bf16")
+    try:
+        p = api.RoundParams(4, 2, 3, 4, 0.1, 1.0, 0)
+        wb = lib.sb_spec_round_workspace_bytes(t, d, C.byref(p), 100, 100)
+        assert wb > 0
+        assert lib.sb_spec_round_workspace_bytes(t, None, C.byref(p), 100, 100) == 0
+        bad = api.RoundParams(0, 2, 3, 4, 0.1, 1.0, 0)
+        assert lib.sb_spec_round_workspace_bytes(t, d, C.byref(bad), 100, 100) == 0
+        tkv, dkv = api.KVCache(1, 1, 128), api.KVCache(1, 1, 128)
+        par = (C.c_int32 * 64)()
+        nc, nb = C.c_int32(0), C.c_int32(0)
+
+        def rnd(tm=t, dm=d, prm=p, ws=wb, tcap=128, flags=None):
+            tkv.capacity = tcap
+            if flags is not None:
+                prm = api.RoundParams(prm.k_max, prm.mode, prm.depth, prm.trunk_max,
+                                      prm.confidence, prm.temperature, flags)
+            return lib.sb_spec_round(tm, C.byref(tkv), 100, dm, C.byref(dkv), 100, C.byref(prm),
+                                     1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, par, C.byref(nc),
+                                     C.byref(nb), 1, ws, None, None)
+        assert rnd(dm=None) == 1
+        assert rnd(dm=t) == 1                       # the target and the draft are one model
+        assert rnd(flags=2) == 1                     # unknown flag
+        assert rnd(prm=api.RoundParams(4, 2, 3, 4, float("nan"), 1.0, 0)) == 1
+        assert rnd(prm=api.RoundParams(4, 2, 3, 4, 0.1, -1.0, 0)) == 1
+        assert rnd(ws=wb - 1) == 3
+        assert rnd(tcap=100) == 3                    # no room for the chain's rows
+    finally:
+        lib.sb_model_destroy(t)
+        lib.sb_model_destroy(d)
