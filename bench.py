@@ -804,6 +804,30 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
 
+    # per-step times (an event pair around each step: their median) and the
+    # step without the rollback (forward + accept walk, the verify-and-accept
+    # time), each over K more steps
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record(stream)
+        step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms_median = float(np.median([e0.elapsed_time(e1) for e0, e1 in evs]))
+
+    def step_no_rollback():
+        m.sb_verify_forward(k_, v_, kv_len, d_tok, parents, 1.0, logits, stats, ws, stream)
+        api.sb_accept_resample(d_tok, parents, logits, stats, 1.0, d_q, d_u, res, sws, stream)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step_no_rollback()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_no_rollback = ev0.elapsed_time(ev1) / args.steps
+
     # the same K steps again with HIP events around every launch of the
     # dominant kernel (its average duration for the roofline); the events
     # cost time of their own, so this loop is not the step time
@@ -1093,6 +1117,8 @@ def main():
         "step_hbm": {"bytes": nbytes["step"],
                      "achieved_gbs": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9, 1),
                      "frac": round(nbytes["step"] / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "ms_per_step_median": round(ms_median, 4),
+                     "ms_forward_and_accept": round(ms_no_rollback, 4),
                      "ms_per_step_with_kernel_events": round(evented_ms, 4),
                      "ms_per_step_graph_replay": None if graph_ms is None else round(graph_ms, 4)},
         "roofline": {"bound": "hbm", "scope": "per kernel: the dominant kernel of the step "
