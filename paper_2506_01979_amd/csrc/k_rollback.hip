@@ -110,7 +110,7 @@ __global__ void k_round_finish(int chain, int branches, int depth, const sb_step
   const bool whole = n >= chain;
   int kept = -1, token = walk->next_token, flags = walk->flags;
   if (whole && sel) {
-    kept = sel[0];
+    kept = sel[0] >= 0 && sel[0] < branches ? sel[0] : -1;
     token = sel[1];
     flags |= sel[2];
   }
@@ -120,7 +120,7 @@ __global__ void k_round_finish(int chain, int branches, int depth, const sb_step
   int len = 0;
   const int n_trunk = whole ? chain : n;
   for (int j = 0; j <= n_trunk; ++j) dpath->path[len++] = j;
-  if (kept >= 0 && kept < branches)
+  if (kept >= 0)
     for (int d = 1; d < depth; ++d) dpath->path[len++] = chain + 1 + (d - 1) * branches + kept;
   for (int j = len; j < SB_MAX_ROWS; ++j) dpath->path[j] = -1;
   dpath->n_accepted = len - 1;

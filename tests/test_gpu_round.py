@@ -172,3 +172,38 @@ def test_round_matches_oracle_on_two_streams(api, name, P, k_max, mode, depth, T
     for (Kg, Vg), Ko, Vo, ln in ((got["tkv"], Kto, Vto, lt), (got["dkv"], Kdo, Vdo, ld)):
         assert row_relerr(Kg.reshape(-1, hd), Ko[:, :, :ln].reshape(-1, hd)) < 5e-4
         assert row_relerr(Vg.reshape(-1, hd), Vo[:, :, :ln].reshape(-1, hd)) < 5e-4
+
+
+@pytest.mark.parametrize("chain,branches,depth,n_acc,sel,want", [
+    # a rejection inside the chain: the walk's draw, the branches dropped
+    (3, 4, 5, 1, (2, 77, 0), {"n_trunk": 1, "kept": -1, "token": 31, "path": [0, 1]}),
+    # the chain accepted, candidate 2 kept: its rows at depths 1 .. depth - 1
+    (3, 4, 5, 3, (2, 77, 2), {"n_trunk": 3, "kept": 2, "token": 77,
+                              "path": [0, 1, 2, 3, 6, 10, 14, 18]}),
+    # the chain accepted, every candidate rejected: the final residual draw
+    (3, 4, 5, 3, (-1, 55, 4), {"n_trunk": 3, "kept": -1, "token": 55, "path": [0, 1, 2, 3]}),
+    # no chain, depth 1: the candidate alone, no deeper rows
+    (0, 3, 1, 0, (1, 9, 0), {"n_trunk": 0, "kept": 1, "token": 9, "path": [0]}),
+    # no candidates: the walk's draw from p at the chain's last row
+    (2, 0, 3, 2, None, {"n_trunk": 2, "kept": -1, "token": 31, "path": [0, 1, 2]}),
+    # a selection naming no candidate of this round is not a kept branch
+    (1, 2, 3, 1, (5, 12, 0), {"n_trunk": 1, "kept": -1, "token": 12, "path": [0, 1]}),
+])
+def test_round_finish_cases(api, chain, branches, depth, n_acc, sel, want):
+    """sb_round_finish on hand-made walk results and selections."""
+    walk = api.new_result()
+    w = walk.cpu().numpy()
+    w[0], w[1], w[2], w[3], w[4] = n_acc, 0 if n_acc else -1, 31, n_acc + 1, 1
+    w[8:8 + n_acc + 1] = np.arange(n_acc + 1)
+    walk.copy_(torch.from_numpy(w))
+    s = None if sel is None else torch.tensor(sel, dtype=torch.int32, device="cuda")
+    out, dpath = api.new_round_result(), api.new_result()
+    say(f"round finish chain={chain} B={branches} depth={depth} n={n_acc} sel={sel}")
+    api.sb_round_finish(chain, branches, depth, walk, s, out, dpath)
+    torch.cuda.synchronize()
+    got = api.decode_round(out)
+    flags = 1 | (0 if sel is None or n_acc < chain else sel[2])
+    assert got == {"n_trunk": want["n_trunk"], "kept": want["kept"], "token": want["token"],
+                   "flags": flags, "draft_len": len(want["path"])}
+    dp = api.decode_result(dpath)
+    assert dp["path"] == want["path"] and dp["n_accepted"] == len(want["path"]) - 1
