@@ -22,7 +22,7 @@ import pytest
 import torch
 
 from gpu_util import decision_margin, row_relerr, say
-from oracle import decoder, spec_round
+from oracle import decoder, sampling, spec_round
 from paper_2506_01979_amd import synth
 from test_gpu_draft import first_tie
 
@@ -207,3 +207,94 @@ def test_round_finish_cases(api, chain, branches, depth, n_acc, sel, want):
                    "flags": flags, "draft_len": len(want["path"])}
     dp = api.decode_result(dpath)
     assert dp["path"] == want["path"] and dp["n_accepted"] == len(want["path"]) - 1
+
+
+
+BF16_SEEDS = (3, 4, 5, 6)
+TIE = 1e-6
+
+
+@pytest.mark.parametrize("mode", ["wor", "iid", "topk"])
+def test_bf16_round_replays_the_oracle(api, mode):
+    """A round of bfloat16 models (the small bf16 shape as target and draft,
+    distinct weights, prefix 200, chain of 3, four candidates of depth 3,
+    T = 1), checked by replay on the GPU's own drafts: the target's chain
+    logits against the oracle's bf16 forward (2e-2 row-relative); the chain
+    test and Algorithm 1 taken by the oracle on the GPU's logits, q rows
+    and uniforms give the round's result exactly (seeds with a decision
+    within 1e-6 of its threshold are skipped, at least three of four are
+    checked); both new lengths; the kept rows of both caches against the
+    oracle's bf16 forwards of the chain and of the draft tree."""
+    sh = synth.SHAPES["small_bf16"]
+    Wt, Wd = weights("small_bf16")
+    P, k_max, depth, T, trunk = 200, 4, 3, 1.0, 4
+    tm = api.Model(sh, api.dict_tensors(Wt))
+    dm = api.Model(sh, api.dict_tensors(Wd))
+    R = trunk + k_max * depth
+    tk, tv = tm.new_kv(P + trunk)
+    dk, dv = dm.new_kv(P + R)
+    buf = api.RoundBuffers(tm, dm, api.round_params(k_max, mode, depth, trunk, 0.0, T), P, P)
+    sv, sd = torch.cuda.Stream(), torch.cuda.Stream()
+    nd, nw, ns = spec_round.uniforms_needed(k_max, depth, trunk)
+    hd = sh.head_dim
+    checked = 0
+    for seed in BF16_SEEDS:
+        ptoks = synth.prefix_tokens(sh.vocab, P + 1, seed)
+        _, Kt, Vt = decoder.prefill(sh, Wt, ptoks[:-1], "bf16")
+        _, Kd, Vd = decoder.prefill(sh, Wd, ptoks[:-1], "bf16")
+        tm.load_kv(tk, tv, Kt, Vt, P)
+        dm.load_kv(dk, dv, Kd, Vd, P)
+        u = synth.uniforms(nd + nw + ns, seed=seed)
+        uw, us = u[nd:nd + nw], u[nd + nw:]
+        buf.tokens.fill_(-5)
+        buf.tokens[0] = int(ptoks[-1])
+        torch.cuda.synchronize()
+        say(f"bf16 round {mode} seed={seed}")
+        c, B, par = api.sb_spec_round(tm, tk, tv, P, dm, dk, dv, P,
+                                      torch.from_numpy(u[:nd]).cuda(), torch.from_numpy(uw).cuda(),
+                                      torch.from_numpy(us).cuda(), buf, sv, sd)
+        sv.synchronize()
+        torch.cuda.synchronize()
+        assert c == trunk - 1 and 1 <= B <= k_max
+        n_rows = 1 + c + B * depth
+        toks = buf.tokens.cpu().numpy()[:n_rows]
+        q = buf.q.cpu().numpy()[:n_rows]
+        lg = buf.logits.cpu().numpy()[:c + 1]
+        ref, kt, vt = decoder.tree_forward(sh, Wt, Kt, Vt, P, toks[:c + 1], par[:c + 1], "bf16")
+        assert row_relerr(lg, ref) < 2e-2
+        # the verification taken by the oracle on the GPU's rows
+        tw, ts = [], []
+        walk = sampling.accept_resample(toks[:c + 1], par[:c + 1], lg, T, q[:c + 1], uw[:c + 1],
+                                        None, tw)
+        kept, token, flags = -1, walk.next_token, walk.flags
+        if walk.n_accepted == c:
+            res = sampling.branch_select(sampling.target_probs(lg[c], T), toks[c + 1:c + 1 + B],
+                                         q[c + 1:c + 1 + B], us[:B], ts)
+            flags |= res.flags
+            if res.accepted is not None:
+                kept, token = res.accepted, int(toks[c + 1 + res.accepted])
+            else:
+                token = sampling.draw(res.p_tilde, float(us[B]), ts, B)
+        if min(decision_margin(tw, uw), decision_margin(ts, us)) < TIE:
+            say(f"  seed {seed}: a decision within {TIE} of its threshold, not compared")
+            continue
+        dpath = list(range(walk.n_accepted + 1))
+        if kept >= 0:
+            dpath += [c + 1 + (d - 1) * B + kept for d in range(1, depth)]
+        assert api.decode_round(buf.round) == {"n_trunk": walk.n_accepted, "kept": kept,
+                                               "token": token, "flags": flags,
+                                               "draft_len": len(dpath)}
+        n_t, n_d = (int(x) for x in buf.new_lens.cpu())
+        assert (n_t, n_d) == (P + walk.n_accepted + 1, P + len(dpath))
+        # kept rows: the target's chain path, the draft's path through the tree
+        n_kv = 1 + c + B * (depth - 1)
+        _, kd, vd = decoder.tree_forward(sh, Wd, Kd, Vd, P, toks[:n_kv], par[:n_kv], "bf16")
+        for m, k, v, K, V, kr, vr, path in ((tm, tk, tv, Kt, Vt, kt, vt, walk.path),
+                                            (dm, dk, dv, Kd, Vd, kd, vd, dpath)):
+            Kg, Vg = m.read_kv(k, v, 0, P + len(path))
+            assert np.array_equal(Kg[:, :, :P], np.asarray(K, np.float32)[:, :, :P])
+            assert np.array_equal(Vg[:, :, :P], np.asarray(V, np.float32)[:, :, :P])
+            assert row_relerr(Kg[:, :, P:].reshape(-1, hd), kr[:, :, path].reshape(-1, hd)) < 1e-1
+            assert row_relerr(Vg[:, :, P:].reshape(-1, hd), vr[:, :, path].reshape(-1, hd)) < 1e-1
+        checked += 1
+    assert checked >= 3
