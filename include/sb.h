@@ -20,9 +20,13 @@
  *    workspace, results); the library keeps only the pointers it is given
  *    and, in sb_model_create, a small host-side model record.
  *  - Every call is asynchronous on the given HIP stream and allocates no
- *    device memory (sb_draft_round alone blocks the host, to read back the
- *    few values that shape its tree).  A model handle must not be used from two streams at
- *    once, and two calls that share a workspace must not overlap.
+ *    device memory.  The drafting calls alone block the host
+ *    (sb_draft_round, sb_draft_chain, sb_draft_branches, sb_spec_round): they
+ *    read back the few values that shape the draft tree -- each chain
+ *    draft's probability against the confidence threshold, and B -- since
+ *    the next launches' shapes depend on them.  A model handle must not be
+ *    used from two streams at once, and two calls that share a workspace
+ *    must not overlap.
  *  - Errors a host can detect (null pointers, bad sizes, a malformed tree,
  *    too little KV capacity or workspace, unsupported shapes) return an
  *    SB_ERR_* code before anything is enqueued.  SB_ERR_HIP reports a failed
