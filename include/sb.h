@@ -120,7 +120,11 @@ typedef struct {
  *   T = 0: zmax = max_v l_v, total = 1.
  * argmax is the lowest index of the largest logit.  The target
  * distribution is p(v) = fl32(exp(z_v - zmax)) / total (T > 0) or the one-hot
- * at argmax (T = 0). */
+ * at argmax (T = 0).  sb_verify_forward on a bf16 model takes the same terms
+ * relative to the largest scaled logit of each 16-column block and rescales
+ * them to zmax in float64 (its statistics are computed in the LM head's
+ * epilogue): total then agrees with the sum above to about 1e-7 relative;
+ * zmax and argmax are identical. */
 typedef struct {
   float zmax;
   int32_t argmax;
@@ -229,8 +233,9 @@ sb_status sb_verify_forward_noalloc(sb_model *m, const sb_kv_cache *kv, int32_t 
                                     int32_t n_rows, float temperature, float *d_logits,
                                     sb_row_stats *d_stats, hipStream_t stream);
 
-/* Row softmax statistics of [n_rows][vocab] float32 logits at T >= 0 (the
- * fused LM-head softmax of the verify step, callable on its own). */
+/* Row softmax statistics of [n_rows][vocab] float32 logits at T >= 0, as a
+ * pass of its own over given logits (the verify step computes them in its
+ * LM head's epilogue). */
 sb_status sb_softmax_stats(int32_t vocab, int32_t n_rows, const float *d_logits,
                            float temperature, sb_row_stats *d_stats, hipStream_t stream);
 

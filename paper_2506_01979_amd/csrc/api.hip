@@ -351,8 +351,26 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   ga.X = xa;
   ga.ks = gl.ks;
   ga.out_rows = c.vocab;
+  // The row softmax statistics come out of the LM head's epilogue as
+  // per-(row, workgroup) partials, kept in the delta buffer (free once the
+  // final norm has summed it), and one short pass combines them; the
+  // logits are not read again.  Shapes whose partials do not fit there run
+  // the statistics pass over the logits.
+  const GemmPlan lp = plan_gemm(EPI_LOGITS, gl.tiles, gl.ks, n);
+  const bool fuse_stats = lp.groups <= kSsGroups &&
+                          (size_t)n * lp.groups * sizeof(LmPart) <=
+                              (size_t)kMaxSplit * L.np * H * sizeof(float);
+  if (fuse_stats) {
+    ga.lm_part = (LmPart *)delta;
+    ga.lm_greedy = temperature <= 0.0f ? 1 : 0;
+    ga.lm_inv_t = ga.lm_greedy ? 1.0f : 1.0f / temperature;
+  }
   SB_TIMED(SB_KC_LM_HEAD, launch_gemm(EPI_LOGITS, ga, gl.tiles, nullptr, s));
-  SB_TIMED(SB_KC_STATS, launch_softmax_stats(c.vocab, n, logits, temperature, stats, s));
+  if (fuse_stats)
+    SB_TIMED(SB_KC_STATS, launch_stats_finish((const LmPart *)delta, lp.groups, n, temperature,
+                                              stats, s));
+  else
+    SB_TIMED(SB_KC_STATS, launch_softmax_stats(c.vocab, n, logits, temperature, stats, s));
   return SB_OK;
 }
 

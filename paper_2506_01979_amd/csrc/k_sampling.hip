@@ -557,6 +557,60 @@ __global__ __launch_bounds__(1024) void k_softmax_stats_reg(const float *__restr
   }
 }
 
+// The statistics of row blockIdx.x from its groups' partials (the LM
+// head's workgroups, at most 256): the largest logit and its lowest index
+// over the groups, zmax = fl32(lmax / T) (rounding is monotone, so this is
+// the largest scaled logit), and total = the float64 sum over groups of
+// sum_g exp(m_g - zmax), m_g = fl32(lmax_g / T), in a fixed order.  A row
+// with nothing above -inf has a NaN total at T > 0, as exp(-inf - -inf).
+__global__ __launch_bounds__(256) void k_softmax_stats_finish(const LmPart *__restrict__ part,
+                                                             int groups, float inv_t, int greedy,
+                                                             sb_row_stats *__restrict__ out) {
+  constexpr int NW = 256 / 64;
+  __shared__ float sbest[NW];
+  __shared__ int sarg[NW];
+  __shared__ double red[NW + 1];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  LmPart p{-INFINITY, INT_MAX, 0.0};
+  if ((int)threadIdx.x < groups) p = part[(size_t)blockIdx.x * groups + threadIdx.x];
+  float best = p.lmax;
+  int arg = p.arg;
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o, 64);
+    const int oa = __shfl_xor(arg, o, 64);
+    if (ob > best || (ob == best && oa < arg)) {
+      best = ob;
+      arg = oa;
+    }
+  }
+  if (lane == 0) {
+    sbest[w] = best;
+    sarg[w] = arg;
+  }
+  __syncthreads();
+  best = sbest[0];
+  arg = sarg[0];
+  for (int i = 1; i < NW; ++i)
+    if (sbest[i] > best || (sbest[i] == best && sarg[i] < arg)) {
+      best = sbest[i];
+      arg = sarg[i];
+    }
+  const float zmax = greedy ? best : best * inv_t;
+  double term = p.sum;
+  if (!greedy && p.sum != 0.0) term = p.sum * exp((double)(p.lmax * inv_t) - (double)zmax);
+  const double s = block_sum<NW>(term, red);
+  if (threadIdx.x == 0) {
+    sb_row_stats st;
+    st.zmax = zmax;
+    st.argmax = arg == INT_MAX ? 0 : arg;
+    if (greedy)
+      st.total = isnan(s) ? (double)NAN : 1.0;
+    else
+      st.total = best == -INFINITY ? (double)NAN : s;
+    out[blockIdx.x] = st;
+  }
+}
+
 __global__ __launch_bounds__(1024) void k_softmax_stats(const float *__restrict__ logits,
                                                         int vocab, float inv_t, int greedy,
                                                         sb_row_stats *__restrict__ out,
@@ -1116,6 +1170,17 @@ hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, floa
   }
   hipLaunchKernelGGL(k_softmax_stats, dim3(n_rows), dim3(1024), 0, s, logits, vocab, inv_t, greedy,
                      stats, invalid);
+  return hipGetLastError();
+}
+
+hipError_t launch_stats_finish(const LmPart *part, int groups, int n_rows, float temperature,
+                               sb_row_stats *stats, hipStream_t s) {
+  if (groups < 1 || groups > 256 || n_rows < 1) return hipErrorInvalidValue;
+  float inv_t;
+  int greedy;
+  temp_args(temperature, &inv_t, &greedy);
+  hipLaunchKernelGGL(k_softmax_stats_finish, dim3(n_rows), dim3(256), 0, s, part, groups, inv_t,
+                     greedy, stats);
   return hipGetLastError();
 }
 

@@ -11,6 +11,7 @@
 // registers of its own epilogue only.
 #pragma once
 
+#include <limits.h>
 #include <math.h>
 
 #include <hip/hip_ext.h>
@@ -143,6 +144,7 @@ constexpr int kStageBytes = 32768;
 constexpr int kRopeLds = kStageBytes / 8;  // float2 entries
 constexpr int kStageGain = 16384;          // RESID_NORM: gains (1 KB)
 constexpr int kStageSq = 17408;            // RESID_NORM: per-(tile, token) sums of squares
+constexpr int kStageLmSlot = 0;            // LOGITS: statistics per (part, token), 8 KB
 
 // Workgroup barrier for LDS traffic only (does not wait for global loads).
 __device__ __forceinline__ void lds_barrier() {
@@ -193,6 +195,63 @@ __device__ __forceinline__ float resid_norm4(const GemmArgs &a, const float *hro
       }
   }
   return sq;
+}
+
+// LOGITS with fused softmax statistics: the partial statistics of 16
+// consecutive logits x[0 .. 15] of one token row, columns c0 .. c0 + 15
+// (columns past the vocabulary are not logits).
+__device__ __forceinline__ LmPart lm_cols(const GemmArgs &a, const float (&x)[16], int c0) {
+  float best = -INFINITY;
+  int arg = INT_MAX;
+  bool bad = false;
+  float v[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    v[j] = c0 + j < a.out_rows ? x[j] : -INFINITY;
+    bad |= isnan(v[j]) || v[j] == INFINITY;
+    const bool take = v[j] > best;  // in column order: the lowest index of the largest
+    best = take ? v[j] : best;
+    arg = take ? c0 + j : arg;
+  }
+  double sum = bad ? (double)NAN : 0.0;
+  if (!bad && !a.lm_greedy && best > -INFINITY) {
+    const float m = best * a.lm_inv_t;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sum += (double)expf(v[j] * a.lm_inv_t - m);
+  }
+  return LmPart{best, arg, sum};
+}
+
+// exp(x - y) for floats x <= y to about float precision: the difference is
+// exact in float64; its float part goes through the float exponential and
+// the remainder d - fl32(d), below half an ulp of d, through 1 + r.
+// Below -104 (-inf included) the float exponential is 0; two infinities of
+// one sign give NaN, as exp(inf - inf).
+__device__ __forceinline__ double exp_diff(float x, float y) {
+  const double d = (double)x - (double)y;
+  if (d < -104.0) return 0.0;
+  const float dh = (float)d;
+  return (double)expf(dh) * (1.0 + (d - (double)dh));
+}
+
+// Running statistics r (sum relative to fl32(r.lmax / T)) merged with a
+// partial p (sum relative to fl32(p.lmax / T)).
+__device__ __forceinline__ void lm_merge(LmPart &r, const LmPart &p, float inv_t, int greedy) {
+  const float old = r.lmax;
+  if (p.lmax > r.lmax || (p.lmax == r.lmax && p.arg < r.arg)) {
+    r.lmax = p.lmax;
+    r.arg = p.arg;
+  }
+  if (greedy) {
+    r.sum += p.sum;  // NaN marks a row with a NaN or +inf logit
+    return;
+  }
+  if (p.sum == 0.0) return;  // nothing above -inf
+  const float mo = old * inv_t, mp = p.lmax * inv_t;
+  if (mp > mo)
+    r.sum = r.sum * exp_diff(mo, mp) + p.sum;
+  else
+    r.sum += p.sum * exp_diff(mp, mo);
 }
 
 template <int EPI, int TT, int NT>
@@ -442,6 +501,57 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
         const int pad = a.xn_ks * 32 - a.out_rows;
         for (int i = threadIdx.x; i < a.n_tok * pad; i += kGemmThreads)
           a.xn[packed_index(i / pad, a.out_rows + i % pad, a.xn_ks)] = 0;
+      }
+    }
+  }
+  // LOGITS with fused softmax statistics: the group's logits have been
+  // written by its own threads; after the barrier they read them back (from
+  // L2, where the stores went) 16 columns at a time: with parts = min(512 /
+  // n_tok, the group's tiles), thread i < parts n_tok takes token row
+  // i % n_tok and every parts-th tile of the group from tile i / n_tok,
+  // leaves its statistics in an LDS slot, and thread t (t < n_tok) combines
+  // row t's slots into the group's partial.
+  if constexpr (EPI == EPI_LOGITS) {
+    if (a.lm_part) {
+      __syncthreads();
+      LmPart *slot = (LmPart *)(stage + kStageLmSlot);
+      const int n_tok = a.n_tok, V = a.out_rows;
+      static_assert(kGemmThreads >= 2 * SB_MAX_ROWS && kGemmThreads * 16 <= kStageBytes,
+                    "every token row has a slot of at least two parts in the stage");
+      const int nt = t_hi - t_lo;
+      const int parts = kGemmThreads / n_tok < nt ? kGemmThreads / n_tok : (nt > 0 ? nt : 1);
+      const int t = (int)threadIdx.x % n_tok, part = (int)threadIdx.x / n_tok;
+      if (part < parts) {
+        const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)a.logits, 0, n_tok * V * 4, kBufferDword3);
+        LmPart r{-INFINITY, INT_MAX, 0.0};
+        for (int tile = t_lo + part; tile < t_hi; tile += parts) {
+          const int c0 = tile * 16, off = (t * V + c0) * 4;
+          float x[16];
+          if ((V & 3) == 0) {  // rows 16-byte aligned
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const f32x4 q = __builtin_bit_cast(
+                  f32x4, __builtin_amdgcn_raw_buffer_load_b128(lrs, off + 16 * j, 0, 0));
+              x[4 * j] = q[0];
+              x[4 * j + 1] = q[1];
+              x[4 * j + 2] = q[2];
+              x[4 * j + 3] = q[3];
+            }
+          } else {
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+              x[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(lrs, off + 4 * j, 0, 0));
+          }
+          lm_merge(r, lm_cols(a, x, c0), a.lm_inv_t, a.lm_greedy);
+        }
+        slot[part * n_tok + t] = r;
+      }
+      lds_barrier();
+      if ((int)threadIdx.x < n_tok) {
+        LmPart r{-INFINITY, INT_MAX, 0.0};
+        for (int pp = 0; pp < parts; ++pp) lm_merge(r, slot[pp * n_tok + threadIdx.x], a.lm_inv_t, a.lm_greedy);
+        a.lm_part[(size_t)threadIdx.x * a.groups + grp] = r;
       }
     }
   }

@@ -19,6 +19,21 @@ struct TreeArg {
 hipError_t launch_softmax_stats(int vocab, int n_rows, const float *logits, float temperature,
                                 sb_row_stats *stats, hipStream_t s,
                                 const unsigned *invalid = nullptr);
+// Softmax statistics of logits rows whose columns are split over groups
+// (the LM head's workgroups): for row t and group g, the largest logit of
+// the group's columns, its lowest index (INT_MAX when none is above -inf)
+// and, at T > 0, the float64 sum of fl32(exp(z_v - m)) over the group's
+// columns with m = fl32(lmax / T) (0 when lmax is -inf).  A NaN or +inf
+// logit makes sum NaN (at T = 0 too).
+struct LmPart {
+  float lmax;
+  int32_t arg;
+  double sum;
+};
+// One row per workgroup: the statistics of rows 0 .. n_rows - 1 from their
+// groups' partials, part[row][groups] (at most 256 groups).
+hipError_t launch_stats_finish(const LmPart *part, int groups, int n_rows, float temperature,
+                               sb_row_stats *stats, hipStream_t s);
 hipError_t launch_walk(int vocab, const TreeArg &tree, const int32_t *tokens, const float *logits,
                        const sb_row_stats *stats, float temperature, const float *q,
                        const float *u, sb_step_result *result, void *ws, hipStream_t s);

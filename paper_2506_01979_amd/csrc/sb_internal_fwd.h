@@ -122,6 +122,12 @@ struct GemmArgs {
   // Otherwise, consumer of an RMSNorm kernel (X = bf16(h g)): every output
   // of token t is multiplied by rs_in[t] = 1/rms (QKV, SWIGLU, LOGITS).
   const float *rs_in;
+  // LOGITS with the softmax statistics fused (lm_part not null): the
+  // group's partial statistics of every token row, lm_part[t][groups], at
+  // inverse temperature lm_inv_t (lm_greedy: T = 0).
+  LmPart *lm_part;
+  float lm_inv_t;
+  int lm_greedy;
 };
 
 // Row stride of the per-(token, group) sums of squares of a RESID_NORM

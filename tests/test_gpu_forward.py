@@ -18,7 +18,7 @@ import pytest
 import torch
 
 from gpu_util import row_relerr, say
-from oracle import decoder
+from oracle import decoder, sampling
 from paper_2506_01979_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -54,7 +54,9 @@ def mode(shape):
     return "bf16" if shape.dtype == "bf16" else "f64"
 
 
-def gpu_forward(api, m, Kp, Vp, kv_len, tokens, parents, T=1.0, cap=None):
+def gpu_forward(api, m, Kp, Vp, kv_len, tokens, parents, T=1.0, cap=None, stats_out=None):
+    """Logits and cache of one sb_verify_forward call; the row statistics
+    are appended to stats_out when given."""
     n = len(parents)
     cap = cap or kv_len + n + 8
     k, v = m.new_kv(cap)
@@ -66,7 +68,23 @@ def gpu_forward(api, m, Kp, Vp, kv_len, tokens, parents, T=1.0, cap=None):
     toks = torch.from_numpy(np.asarray(tokens, np.int32)).cuda()
     m.sb_verify_forward(k, v, kv_len, toks, parents, T, logits, stats, ws)
     torch.cuda.synchronize()
+    if stats_out is not None:
+        stats_out.append(api.decode_stats(stats))
     return logits.cpu().numpy(), k, v
+
+
+def check_stats(st, logits, T):
+    """The forward's row statistics against the oracle's on the same logits:
+    zmax and argmax exact, total within 1e-6 relative (NaN where the
+    oracle's is NaN)."""
+    for i in range(logits.shape[0]):
+        rs = sampling.row_stats(logits[i], T)
+        assert st["argmax"][i] == rs.argmax, (i, st["argmax"][i], rs.argmax)
+        assert np.float32(st["zmax"][i]) == np.float32(rs.zmax), i
+        if np.isnan(rs.total):
+            assert np.isnan(st["total"][i]), i
+        else:
+            assert abs(st["total"][i] - rs.total) <= 1e-6 * rs.total, (i, st["total"][i], rs.total)
 
 
 CASES = [
@@ -114,10 +132,12 @@ def test_verify_forward_parity(api, sname, P, spec):
     toks[0] = ptoks[-1]
     ref, kt, vt = decoder.tree_forward(shape, W, Kp, Vp, kv_len, toks, parents, mode(shape))
     m = model(api, shape)
-    got, k, v = gpu_forward(api, m, Kp, Vp, kv_len, toks, parents)
+    st = []
+    got, k, v = gpu_forward(api, m, Kp, Vp, kv_len, toks, parents, stats_out=st)
     err = row_relerr(got, ref)
     say(f"  logits row-relative error {err:.3e}")
     assert err < tol(shape)
+    check_stats(st[0], got, 1.0)
     kg, vg = m.read_kv(k, v, kv_len, n)
     assert row_relerr(kg.reshape(-1, shape.head_dim), kt.reshape(-1, shape.head_dim)) < tol(shape) * 5
     assert row_relerr(vg.reshape(-1, shape.head_dim), vt.reshape(-1, shape.head_dim)) < tol(shape) * 5
@@ -126,6 +146,45 @@ def test_verify_forward_parity(api, sname, P, spec):
         kp, vp = m.read_kv(k, v, 0, kv_len)
         assert np.array_equal(kp, np.asarray(Kp[:, :, :kv_len], np.float32))
         assert np.array_equal(vp, np.asarray(Vp[:, :, :kv_len], np.float32))
+
+
+@pytest.mark.parametrize("sname,kind,T", [
+    ("small_bf16", "ties", 1.0), ("small_bf16", "ties", 0.0), ("ragged_bf16", "ties", 0.7),
+    ("small_bf16", "nonfinite", 1.0), ("small_bf16", "nonfinite", 0.0),
+    ("ragged_bf16", "nonfinite", 1.3),
+])
+def test_forward_statistics_special_rows(api, sname, kind, T):
+    """The statistics computed with the LM head on logits with ties and
+    non-finite values.  ties: every LM-head row zero except rows 100 .. 199,
+    which share one vector, so each row of logits is 0 except one value
+    repeated 100 times (the largest is tied, its lowest index wins, and the
+    1000-odd equal zeros enter the total).  nonfinite: row 7 of the LM head
+    +inf, so column 7 of every row is +inf or NaN (the row's total is NaN,
+    its argmax ignores NaN)."""
+    shape = synth.SHAPES[sname]
+    W = dict(weights(shape))
+    lm = np.array(W["lm_head"], dtype=np.float32, copy=True)
+    if kind == "ties":
+        row = lm[100].copy()
+        lm[:] = 0.0
+        lm[100:200] = row
+    else:
+        lm[7] = np.inf
+    W["lm_head"] = lm
+    say(f"forward statistics {sname} {kind} T={T}")
+    m = api.Model(shape, api.dict_tensors(W))
+    P, parents = 60, synth.branch_parents(3, 4)
+    ptoks = synth.prefix_tokens(shape.vocab, P)
+    _, Kp, Vp = decoder.prefill(shape, weights(shape), ptoks[:-1], "bf16")
+    toks = np.random.default_rng(5).integers(0, shape.vocab, len(parents)).astype(np.int32)
+    toks[0] = ptoks[-1]
+    st = []
+    got, _, _ = gpu_forward(api, m, Kp, Vp, P - 1, toks, parents, T=T, stats_out=st)
+    if kind == "ties":
+        assert np.all(np.sum(got == got.max(axis=1, keepdims=True), axis=1) >= 100)
+    else:
+        assert np.all(~np.isfinite(got[:, 7]))
+    check_stats(st[0], got, T)
 
 
 @pytest.mark.parametrize("sname", ["tiny", "small_bf16", "small_gqa_bf16"])
