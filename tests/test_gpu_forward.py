@@ -103,6 +103,10 @@ CASES = [
     ("heads32_bf16", 90, ("branch", 8, 7)),
     ("small_bf16", 300, ("fork", 4, 4, 7)),
     ("tiny", 64, ("fork", 6, 3, 1)),
+    # the largest trees (SB_MAX_ROWS = 256 rows): 15 x 17 branches, a
+    # 256-row chain (ancestor bit 255)
+    ("small_bf16", 64, ("branch", 15, 17)),
+    ("small_gqa_bf16", 8, ("chain", 256)),
 ]
 
 

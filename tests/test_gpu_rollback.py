@@ -31,12 +31,14 @@ def result_tensor(api, path):
 
 
 @pytest.mark.parametrize("sname", ["tiny", "small_bf16", "small_gqa_bf16"])
-@pytest.mark.parametrize("path", [[0, 1, 2, 3], [0, 9, 10, 11], [0, 2, 3], [0], [0, 17, 18]])
+@pytest.mark.parametrize("path", [[0, 1, 2, 3], [0, 9, 10, 11], [0, 2, 3], [0], [0, 17, 18],
+                                  list(range(64)), [0, 128, 200, 255]])
 def test_rollback_bytes(api, sname, path):
     shape = synth.SHAPES[sname]
     say(f"rollback bytes {sname} path={path}")
     m = api.Model(shape.with_layers(2), api.synth_tensors(shape.with_layers(2)))
-    kv_len, cap = 37, 80
+    # rows up to 255 of a 256-row tree behind the prefix
+    kv_len, cap = 37, max(80, (37 + max(path) + 1 + 7) // 8 * 8)
     g = np.random.default_rng(len(path))
     L = 2
     K = g.standard_normal((L, shape.n_kv_heads, cap, shape.head_dim)).astype(np.float32)

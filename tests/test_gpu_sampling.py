@@ -162,6 +162,9 @@ TREES = [
     ("fork6x5x1", synth.fork_parents(6, 5, 1)),
     ("random60", _random_tree(60, 3)),
     ("root_only", np.array([-1], dtype=np.int32)),
+    # SB_MAX_ROWS = 256 rows: 15 branches of 17, and a random tree
+    ("b15k17", synth.branch_parents(15, 17)),
+    ("random256", _random_tree(256, 7)),
 ]
 
 
