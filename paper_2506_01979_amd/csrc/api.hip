@@ -206,11 +206,11 @@ struct TimedLaunch {
     if (gemm)
       g_launch_events = LaunchEvents{t.start[t.used], t.stop[t.used], false};
     else
-      hipEventRecord(t.start[t.used], s);
+      (void)hipEventRecord(t.start[t.used], s);  // timing only: a failure costs a figure
   }
   ~TimedLaunch() {
     if (!on) return;
-    if (!gemm) hipEventRecord(t.stop[t.used], s);
+    if (!gemm) (void)hipEventRecord(t.stop[t.used], s);
     g_launch_events.taken = true;
     ++t.used;
   }
@@ -644,8 +644,8 @@ sb_status sb_model_create(const sb_model_config *cfg, const sb_model_weights *w,
 }
 
 static void timer_release(sb_timer &t) {
-  for (hipEvent_t e : t.start) hipEventDestroy(e);
-  for (hipEvent_t e : t.stop) hipEventDestroy(e);
+  for (hipEvent_t e : t.start) (void)hipEventDestroy(e);
+  for (hipEvent_t e : t.stop) (void)hipEventDestroy(e);
   t.start.clear();
   t.stop.clear();
   t.active = 0;
