@@ -451,7 +451,8 @@ size_t sb_draft_round_workspace_bytes(const sb_model *draft, int32_t k_max, int3
  * *h_branches = B, *h_chain = c.  The draft's cache slots kv_len .. are
  * written (capacity at least kv_len + trunk_max + k_max depth).  d_u:
  * float32 [trunk_max + k_max depth].  Blocks the host once per chain draft
- * before the last allowed one (to read its probability) and once to read B.
+ * before the last allowed one (to read its probability; not when confidence
+ * <= 0, which every draft meets) and once to read B.
  * 1 <= k_max <= SB_BRANCH_MAX_K, depth >= 1, trunk_max >= 1, trunk_max +
  * k_max depth <= SB_MAX_ROWS, confidence not NaN. */
 sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len, int32_t k_max,
@@ -470,7 +471,7 @@ sb_status sb_draft_round(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
  *   *h_chain = c; d_u float32 [trunk_max]; d_tokens and d_q have at least
  *   trunk_max + 1 rows; d_ws of sb_draft_round_workspace_bytes(draft, 1, 1,
  *   trunk_max, kv_len) bytes.  Blocks the host once per chain draft before
- *   the last allowed one.
+ *   the last allowed one when confidence > 0.
  * sb_draft_branches: steps 2 and 3 of sb_draft_round after a chain of
  *   `chain` rows (rows 0 .. chain of d_tokens, row 0 of d_q as
  *   sb_draft_chain leaves them, d_xb): the candidates into rows chain + 1

@@ -1025,11 +1025,14 @@ sb_status sb_draft_chain(sb_model *draft, const sb_kv_cache *kv, int32_t kv_len,
     st = draft_sample_rows(draft, ws, L, temperature, t, 1, &src, &dst, trunk_max + 1,
                            d_u + (t - 1), d_tokens, d_q, conf, stream);
     if (st != SB_OK) return st;
+    // A probability is never below a threshold <= 0 (a NaN one is not below
+    // any): then every draft is confident and the host reads nothing.
     float cf = 0.0f;
-    if (hipMemcpyAsync(&cf, conf, sizeof(cf), hipMemcpyDeviceToHost, stream) != hipSuccess ||
-        hipStreamSynchronize(stream) != hipSuccess)
+    if (confidence > 0.0f &&
+        (hipMemcpyAsync(&cf, conf, sizeof(cf), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+         hipStreamSynchronize(stream) != hipSuccess))
       return SB_ERR_HIP;
-    if (cf < confidence) {
+    if (confidence > 0.0f && cf < confidence) {
       // an unconfident draft: the branch point; its distribution to row 0,
       // its token to x_b
       if (hipMemcpyAsync(d_q, d_q + (size_t)t * V, (size_t)V * sizeof(float),
