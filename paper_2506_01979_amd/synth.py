@@ -100,6 +100,8 @@ SHAPES = {
     "ragged_bf16": Shape("ragged_bf16", 2, 328, 4, 2, 64, 600, 1001, "bf16"),
     # 32 KV heads on a narrow model: few key ranges per head
     "heads32_bf16": Shape("heads32_bf16", 2, 256, 32, 32, 64, 512, 1000, "bf16"),
+    # head_dim 128 with grouped queries (two query heads per KV head)
+    "gqa128_bf16": Shape("gqa128_bf16", 2, 512, 4, 2, 128, 1024, 1000, "bf16"),
     # grouped queries at head width 128 (8 query heads per KV head, like the
     # 70B shape) on a narrow model
     "small_gqa128_bf16": Shape("small_gqa128_bf16", 2, 1024, 16, 2, 128, 2752, 2000, "bf16"),

@@ -103,6 +103,15 @@ CASES = [
     ("heads32_bf16", 90, ("branch", 8, 7)),
     ("small_bf16", 300, ("fork", 4, 4, 7)),
     ("tiny", 64, ("fork", 6, 3, 1)),
+    # head_dim 128 with every row of a KV head in one block of at most 48
+    # rows (the 7B step's attention shape): ranges of 4 steps, 8 ranges, a
+    # key count that ends inside a 16-byte V^T chunk, grouped queries
+    ("small_h128_bf16", 200, ("branch", 4, 8)),
+    ("small_h128_bf16", 1000, ("branch", 2, 4)),
+    ("small_h128_bf16", 37, ("chain", 20)),
+    ("small_h128_bf16", 2047, ("branch", 4, 8)),
+    ("gqa128_bf16", 300, ("branch", 4, 4)),
+    ("gqa128_bf16", 1, ("chain", 9)),
     # the largest trees (SB_MAX_ROWS = 256 rows): 15 x 17 branches, a
     # 256-row chain (ancestor bit 255)
     ("small_bf16", 64, ("branch", 15, 17)),
