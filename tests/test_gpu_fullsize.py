@@ -120,6 +120,16 @@ def run_case(api, m, bits, shape, prefix, B, k, seed, full_depth=False, check_wa
     torch.cuda.synchronize()
     lg = logits.cpu().numpy()
     st = api.decode_stats(stats)
+    if full_depth:
+        # the allocation-free entry point on the same step (it rewrites the
+        # same tree slots with the same values): identical bytes
+        say(f"  allocation-free forward {shape.name}")
+        lg2 = torch.full_like(logits, 7.0)
+        st2 = api.new_stats(n)
+        m.sb_verify_forward_noalloc(kc, vc, kv_len, d_tok, parents, 1.0, lg2, st2)
+        torch.cuda.synchronize()
+        assert np.array_equal(lg2.cpu().numpy(), lg)
+        assert np.array_equal(st2.cpu().numpy(), stats.cpu().numpy())
     tree_k, tree_v = {}, {}
     for l in sorted({0, L - 1}):
         tree_k[l] = kc[l, :, kv_len:kv_len + n].float().cpu().numpy()
