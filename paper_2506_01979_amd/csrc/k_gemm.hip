@@ -31,9 +31,22 @@ constexpr int kNTs[] = {1, 2, 3, 4, 6, 8};
 
 GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
   GemmPlan p{};
-  const int cus = device_cus();
   const int nc = ks / 8;
-  const int tt = (n_tok + 15) / 16;
+  // Wide trees: past 8 token tiles a workgroup holds accumulators for only
+  // 1-2 weight tiles per pass, keeps one chunk of loads in flight and
+  // re-reads the whole activation per pass.  The residual projections (whose
+  // activation outweighs their weights per workgroup) and gate/up split the
+  // token tiles over workgroups of 3 each instead, the workgroups that read
+  // the same weights on one XCD (13B at 129 rows: down 79 -> 61 us, O 34 ->
+  // 25, gate/up 126 -> 120; QKV and the LM head ran slower split).
+  const int tt_all = (n_tok + 15) / 16;
+  p.tgroups = (tt_all > 8 && (epi == EPI_RESID || epi == EPI_SWIGLU)) ? (tt_all + 2) / 3 : 1;
+  // each token group's share of the compute units, a multiple of 8 so that
+  // the token groups of one unit fall on one XCD
+  const int cus = p.tgroups == 1 ? device_cus() : ((device_cus() / p.tgroups) & ~7) > 8
+                                                      ? (device_cus() / p.tgroups) & ~7
+                                                      : 8;
+  const int tt = (tt_all + p.tgroups - 1) / p.tgroups;
   for (int v : kTTs)
     if (v >= tt) {
       p.tt = v;
@@ -60,7 +73,7 @@ GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
     }
   p.split = S;
   p.groups = groups;
-  p.grid = groups * S;
+  p.grid = groups * S * p.tgroups;
   return p;
 }
 
@@ -85,6 +98,7 @@ hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int *split, hipStr
   b.tiles = tiles;
   b.split = p.split;
   b.groups = p.groups;
+  b.tgroups = p.tgroups;
   if (split) *split = p.split;
   switch (epi) {
     case EPI_QKV: return launch_gemm_qkv(b, p, s);

@@ -269,8 +269,14 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
   // XCD b % 8).  Work unit u = (tile group, K range) is numbered XCD-major,
   // so each XCD streams one contiguous eighth of the weights: the XCDs move
   // equal bytes even when the groups' tile counts differ by one.
+  // Wide trees (more than 8 token tiles) split the token tiles over
+  // tgroups workgroups per (tile group, K range), fastest in the unit
+  // order, so the workgroups that read the same weights sit on one XCD.
   const int nb = gridDim.x;
-  const int u = (nb & 7) == 0 ? (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+  const int uu = (nb & 7) == 0 ? (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+  const int tgs = a.tgroups > 0 ? a.tgroups : 1;
+  const int u = uu / tgs;
+  const int tb = (uu - u * tgs) * TT * 16;  // first token row of the workgroup
   const int split = u % S, grp = u / S;
   const int t_lo = (int)(((long long)a.tiles * grp) / a.groups);
   const int t_hi = (int)(((long long)a.tiles * (grp + 1)) / a.groups);
@@ -285,8 +291,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
   int xvo[TT];
 #pragma unroll
   for (int tt = 0; tt < TT; ++tt)
-    xvo[tt] = (tt * 16 + (lane & 15)) < a.n_tok
-                  ? tt * ks * 1024 + (lane & 15) * 64 + (lane >> 4) * 16
+    xvo[tt] = (tb + tt * 16 + (lane & 15)) < a.n_tok
+                  ? ((tb >> 4) + tt) * ks * 1024 + (lane & 15) * 64 + (lane >> 4) * 16
                   : xbytes;
 
   // Operands of the epilogue go to LDS by direct-to-LDS loads issued now (no
@@ -309,7 +315,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
         (void *)a.h, 0, a.n_tok * a.out_rows * 4, kBufferDword3);
     for (int b = w; b < (t_hi - t_lo) * TT; b += kGemmWaves) {
       const int tl = b / TT, tt = b - tl * TT;
-      const int tok = tt * 16 + (lane >> 2), row = (t_lo + tl) * 16 + 4 * (lane & 3);
+      const int tok = tb + tt * 16 + (lane >> 2), row = (t_lo + tl) * 16 + 4 * (lane & 3);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(hrs, (lds_void *)(stage + b * 1024), 16,
                                                (tok * a.out_rows + row) * 4, 0, 0, 0);
     }
@@ -447,7 +453,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
         for (int it = threadIdx.x; it < items; it += kGemmThreads) {
           const int tok16 = it & 15, g = (it >> 4) & 1, pr = it >> 5;
           const int tl = pr / TT, tt = pr - tl * TT;
-          const int tok = tt * 16 + tok16;
+          const int tok = tb + tt * 16 + tok16;  // token row
           float sq = 0.0f;
           if (tok < a.n_tok) {
             const int l1 = tok16 + 16 * g;
@@ -477,7 +483,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
           if constexpr (EPI == EPI_RESID_NORM) {
             // the two halves (g = 0, 1) of (tile, token): lanes it, it ^ 16
             sq += __shfl_xor(sq, 16, 64);
-            if (g == 0) ssq[tl * (TT * 16) + tok] = sq;
+            if (g == 0) ssq[tl * (TT * 16) + tt * 16 + tok16] = sq;
           }
         }
         lds_barrier();
@@ -515,15 +521,17 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
     if (a.lm_part) {
       __syncthreads();
       LmPart *slot = (LmPart *)(stage + kStageLmSlot);
-      const int n_tok = a.n_tok, V = a.out_rows;
+      const int n_tok = a.n_tok - tb < TT * 16 ? a.n_tok - tb : TT * 16;  // the group's rows
+      const int V = a.out_rows;
       static_assert(kGemmThreads >= 2 * SB_MAX_ROWS && kGemmThreads * 16 <= kStageBytes,
                     "every token row has a slot of at least two parts in the stage");
       const int nt = t_hi - t_lo;
-      const int parts = kGemmThreads / n_tok < nt ? kGemmThreads / n_tok : (nt > 0 ? nt : 1);
-      const int t = (int)threadIdx.x % n_tok, part = (int)threadIdx.x / n_tok;
-      if (part < parts) {
+      const int nl = n_tok > 0 ? n_tok : 1;
+      const int parts = kGemmThreads / nl < nt ? kGemmThreads / nl : (nt > 0 ? nt : 1);
+      const int t = (int)threadIdx.x % nl, part = (int)threadIdx.x / nl;
+      if (n_tok > 0 && part < parts) {
         const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)a.logits, 0, n_tok * V * 4, kBufferDword3);
+            (void *)(a.logits + (size_t)tb * V), 0, n_tok * V * 4, kBufferDword3);
         LmPart r{-INFINITY, INT_MAX, 0.0};
         for (int tile = t_lo + part; tile < t_hi; tile += parts) {
           const int c0 = tile * 16, off = (t * V + c0) * 4;
@@ -551,7 +559,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
       if ((int)threadIdx.x < n_tok) {
         LmPart r{-INFINITY, INT_MAX, 0.0};
         for (int pp = 0; pp < parts; ++pp) lm_merge(r, slot[pp * n_tok + threadIdx.x], a.lm_inv_t, a.lm_greedy);
-        a.lm_part[(size_t)threadIdx.x * a.groups + grp] = r;
+        a.lm_part[(size_t)(tb + threadIdx.x) * a.groups + grp] = r;
       }
     }
   }
