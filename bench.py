@@ -65,7 +65,7 @@ def kernel_class(name: str, prev: str) -> str:
         return "accept_walk"
     if "k_rollback" in name:
         return "rollback"
-    m = re.search(r"k_gemm<(\d+)", name)
+    m = re.search(r"k_gemm(?:_wide)?<(\d+)", name)
     if m:
         epi = int(m.group(1))
         if epi in (1, 4):  # residual projections

@@ -32,23 +32,33 @@ constexpr int kNTs[] = {1, 2, 3, 4, 6, 8};
 GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
   GemmPlan p{};
   const int nc = ks / 8;
-  // Wide trees: past 8 token tiles a workgroup holds accumulators for only
-  // 1-2 weight tiles per pass, keeps one chunk of loads in flight and
-  // re-reads the whole activation per pass.  The residual projections (whose
-  // activation outweighs their weights per workgroup) and gate/up split the
-  // token tiles over workgroups of 3 each instead, the workgroups that read
-  // the same weights on one XCD (13B at 129 rows: down 79 -> 61 us, O 34 ->
-  // 25, gate/up 126 -> 120; QKV and the LM head ran slower split).
   const int tt_all = (n_tok + 15) / 16;
-  p.tgroups = (tt_all > 8 && (epi == EPI_RESID || epi == EPI_SWIGLU)) ? (tt_all + 2) / 3 : 1;
-  // each token group's share of the compute units, a multiple of 8 so that
-  // the token groups of one unit fall on one XCD
-  const int cus = p.tgroups == 1 ? device_cus() : ((device_cus() / p.tgroups) & ~7) > 8
-                                                      ? (device_cus() / p.tgroups) & ~7
-                                                      : 8;
-  const int tt = (tt_all + p.tgroups - 1) / p.tgroups;
+  // Wide trees: k_gemm_wide (a wave owns a tile pair over one of KS parts
+  // of the workgroup's K range; the activation is staged once per 16 / KS
+  // tiles through LDS).  QKV, with the fewest tiles, takes KS = 4; the
+  // residual projections split K over up to kMaxSplit workgroups per tile
+  // group as well.  13B at 129 rows: gate/up 120 -> 78 us, QKV 69 -> 61,
+  // down 61 -> 50, O 25 -> 26.
+  if (tt_all > 8 && (epi == EPI_QKV || epi == EPI_SWIGLU || epi == EPI_RESID)) {
+    const int KS = epi == EPI_QKV ? 4 : 2;
+    p.wide = KS;
+    p.tt = tt_all <= 9 ? 9 : tt_all <= 12 ? 12 : 16;
+    p.nt = 2;
+    p.groups = (tiles + 16 / KS - 1) / (16 / KS);
+    int S = 1;
+    if (epi == EPI_RESID) {
+      S = device_cus() / p.groups;
+      if (S > kMaxSplit) S = kMaxSplit;
+      if (S * KS > ks) S = ks / KS;
+      if (S < 1) S = 1;
+    }
+    p.split = S;
+    p.grid = p.groups * S;
+    return p;
+  }
+  const int cus = device_cus();
   for (int v : kTTs)
-    if (v >= tt) {
+    if (v >= tt_all) {
       p.tt = v;
       break;
     }
@@ -73,7 +83,7 @@ GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
     }
   p.split = S;
   p.groups = groups;
-  p.grid = groups * S * p.tgroups;
+  p.grid = groups * S;
   return p;
 }
 
@@ -98,7 +108,6 @@ hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int *split, hipStr
   b.tiles = tiles;
   b.split = p.split;
   b.groups = p.groups;
-  b.tgroups = p.tgroups;
   if (split) *split = p.split;
   switch (epi) {
     case EPI_QKV: return launch_gemm_qkv(b, p, s);

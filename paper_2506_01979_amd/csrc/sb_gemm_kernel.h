@@ -269,14 +269,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
   // XCD b % 8).  Work unit u = (tile group, K range) is numbered XCD-major,
   // so each XCD streams one contiguous eighth of the weights: the XCDs move
   // equal bytes even when the groups' tile counts differ by one.
-  // Wide trees (more than 8 token tiles) split the token tiles over
-  // tgroups workgroups per (tile group, K range), fastest in the unit
-  // order, so the workgroups that read the same weights sit on one XCD.
   const int nb = gridDim.x;
-  const int uu = (nb & 7) == 0 ? (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3) : blockIdx.x;
-  const int tgs = a.tgroups > 0 ? a.tgroups : 1;
-  const int u = uu / tgs;
-  const int tb = (uu - u * tgs) * TT * 16;  // first token row of the workgroup
+  const int u = (nb & 7) == 0 ? (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3) : blockIdx.x;
   const int split = u % S, grp = u / S;
   const int t_lo = (int)(((long long)a.tiles * grp) / a.groups);
   const int t_hi = (int)(((long long)a.tiles * (grp + 1)) / a.groups);
@@ -291,8 +285,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
   int xvo[TT];
 #pragma unroll
   for (int tt = 0; tt < TT; ++tt)
-    xvo[tt] = (tb + tt * 16 + (lane & 15)) < a.n_tok
-                  ? ((tb >> 4) + tt) * ks * 1024 + (lane & 15) * 64 + (lane >> 4) * 16
+    xvo[tt] = (tt * 16 + (lane & 15)) < a.n_tok
+                  ? tt * ks * 1024 + (lane & 15) * 64 + (lane >> 4) * 16
                   : xbytes;
 
   // Operands of the epilogue go to LDS by direct-to-LDS loads issued now (no
@@ -315,7 +309,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
         (void *)a.h, 0, a.n_tok * a.out_rows * 4, kBufferDword3);
     for (int b = w; b < (t_hi - t_lo) * TT; b += kGemmWaves) {
       const int tl = b / TT, tt = b - tl * TT;
-      const int tok = tb + tt * 16 + (lane >> 2), row = (t_lo + tl) * 16 + 4 * (lane & 3);
+      const int tok = tt * 16 + (lane >> 2), row = (t_lo + tl) * 16 + 4 * (lane & 3);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(hrs, (lds_void *)(stage + b * 1024), 16,
                                                (tok * a.out_rows + row) * 4, 0, 0, 0);
     }
@@ -453,7 +447,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
         for (int it = threadIdx.x; it < items; it += kGemmThreads) {
           const int tok16 = it & 15, g = (it >> 4) & 1, pr = it >> 5;
           const int tl = pr / TT, tt = pr - tl * TT;
-          const int tok = tb + tt * 16 + tok16;  // token row
+          const int tok = tt * 16 + tok16;  // token row
           float sq = 0.0f;
           if (tok < a.n_tok) {
             const int l1 = tok16 + 16 * g;
@@ -521,7 +515,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
     if (a.lm_part) {
       __syncthreads();
       LmPart *slot = (LmPart *)(stage + kStageLmSlot);
-      const int n_tok = a.n_tok - tb < TT * 16 ? a.n_tok - tb : TT * 16;  // the group's rows
+      const int n_tok = a.n_tok;
       const int V = a.out_rows;
       static_assert(kGemmThreads >= 2 * SB_MAX_ROWS && kGemmThreads * 16 <= kStageBytes,
                     "every token row has a slot of at least two parts in the stage");
@@ -531,7 +525,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
       const int t = (int)threadIdx.x % nl, part = (int)threadIdx.x / nl;
       if (n_tok > 0 && part < parts) {
         const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)(a.logits + (size_t)tb * V), 0, n_tok * V * 4, kBufferDword3);
+            (void *)a.logits, 0, n_tok * V * 4, kBufferDword3);
         LmPart r{-INFINITY, INT_MAX, 0.0};
         for (int tile = t_lo + part; tile < t_hi; tile += parts) {
           const int c0 = tile * 16, off = (t * V + c0) * 4;
@@ -559,7 +553,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
       if ((int)threadIdx.x < n_tok) {
         LmPart r{-INFINITY, INT_MAX, 0.0};
         for (int pp = 0; pp < parts; ++pp) lm_merge(r, slot[pp * n_tok + threadIdx.x], a.lm_inv_t, a.lm_greedy);
-        a.lm_part[(size_t)(tb + threadIdx.x) * a.groups + grp] = r;
+        a.lm_part[(size_t)threadIdx.x * a.groups + grp] = r;
       }
     }
   }
@@ -567,6 +561,208 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
   if (t_lo >= t_hi) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+
+// Wide GEMM (trees of more than 8 token tiles).
+//
+// A wave owns two 16-row weight tiles (a tile pair) over one of KS parts of
+// the workgroup's K range; the 8 / KS pairs of a workgroup (16 / KS tiles)
+// share the activation, staged through LDS one chunk at a time: chunk c
+// holds k-step c of every K part for all TT token tiles (KS TT fragments of
+// 1 KB; the waves load them into registers L chunks ahead, with the
+// weights, and write each chunk to one of two LDS buffers when it is due).
+// Each fragment read from LDS feeds both tiles of the pair, each weight
+// fragment all TT token tiles.  At the end the KS partial sums of each tile
+// meet in LDS and the owner wave of the tile runs the epilogue.  Split-K
+// launches (the residual projections, whose tile groups are too few to fill
+// the chip) also give each of `split` workgroups per tile group a
+// contiguous K range; the unit order is K-range-major, so each XCD caches
+// one range of the activation.  (Direct-to-LDS loads move the activation at
+// about 7 bytes per clock per compute unit, which bounded every variant
+// that used them.)
+template <int TT, int KS>
+struct WideCfg {
+  static constexpr int PAIRS = kGemmWaves / KS;                     // tile pairs per workgroup
+  static constexpr int FRAG = KS * TT;                              // fragments per chunk
+  static constexpr int FPW = (FRAG + kGemmWaves - 1) / kGemmWaves;  // per wave, at most
+  static constexpr int FULL = FRAG % kGemmWaves == 0 ? kGemmWaves : FRAG % kGemmWaves;
+  static constexpr int L = FRAG <= 18 ? 6 : FRAG <= 36 ? 4 : 2;     // chunks in flight
+  static constexpr int LDS = 2 * FRAG > kGemmWaves * TT ? 2 * FRAG : kGemmWaves * TT;  // KB
+  static_assert(L % 2 == 0, "the unrolled chunk steps cover both LDS buffers");
+  static_assert(LDS <= 160, "the chunk buffers and the reduction fit LDS");
+};
+
+template <int EPI, int TT, int KS>
+__global__ __launch_bounds__(kGemmThreads, 1) void k_gemm_wide(GemmArgs a) {
+  using C = WideCfg<TT, KS>;
+  constexpr int L = C::L, FPW = C::FPW;
+  constexpr int NW = 2;  // weight loads per wave per chunk (one per tile)
+  __shared__ __attribute__((aligned(16))) char abuf[C::LDS * 1024];
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int ks = a.ks;
+  const int nb = gridDim.x;
+  const int u = (nb & 7) == 0 ? (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+  const int split = u / a.groups, grp = u - split * a.groups;
+  const int pw = w % C::PAIRS, kp = w / C::PAIRS;  // tile pair, K part
+  const int tile0 = (grp * C::PAIRS + pw) * 2;
+  const bool has = tile0 < a.tiles;  // wave-uniform
+  // K part q of the Q = split KS parts of the launch: k-steps [kb(q), kb(q+1))
+  const int Q = a.split * KS;
+  auto kb = [&](int q) { return ks * q / Q; };
+  const int nchunk = (ks + Q - 1) / Q;  // chunks: one k-step of every part
+  const int xbytes = ((a.n_tok + 15) >> 4) * ks * 1024;
+  const __amdgpu_buffer_rsrc_t xrs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.X, 0, xbytes, kBufferDword3);
+  const int wbytes = a.tiles * ks * 1024;
+  const __amdgpu_buffer_rsrc_t wrs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.W, 0, wbytes, kBufferDword3);
+  const int qw = split * KS + kp;  // this wave's K part
+  const int kw0 = kb(qw), kwn = kb(qw + 1) - kw0;
+  int wvo[NW];
+#pragma unroll
+  for (int j = 0; j < NW; ++j)
+    wvo[j] = tile0 + j < a.tiles ? (tile0 + j) * ks * 1024 + lane * 16 : wbytes;
+  // waves w < FULL move FPW fragments per chunk, the others FPW - 1
+  const bool full = w < C::FULL;
+
+  // Chunk c's fragment f = p TT + tt (K part p, token tile tt) sits at KB f
+  // of its buffer; wave w moves fragments w + 8 j.  Lane l loads bytes
+  // 16 l .. of a fragment (token row r = l / 4, k 8 (l % 4) ..) and stores
+  // them at slot 4 r + ((l % 4) ^ (r / 4 % 4)), so the 8 lanes an LDS read
+  // serves together fall on 8 different bank groups.
+  const int wsw = ((lane >> 2) * 4 + ((lane & 3) ^ ((lane >> 4) & 3))) * 16;
+  const int rsw = ((lane & 15) * 4 + ((lane >> 4) ^ ((lane >> 2) & 3))) * 16;
+  // per fragment of this wave: its lane offset at k-step 0 of its K part
+  // and the part's length (the loop below only adds the chunk)
+  int xoff[FPW], xlen[FPW];
+#pragma unroll
+  for (int j = 0; j < FPW; ++j) {
+    const int f = w + kGemmWaves * j;
+    const int p = f / TT, tt = f - p * TT;
+    const int q = split * KS + p;
+    const int k0 = kb(q);
+    xoff[j] = (tt * ks + k0) * 1024 + lane * 16;
+    xlen[j] = kb(q + 1) - k0;
+  }
+  i32x4 xr[L][FPW], wr[L][NW];
+  auto issue = [&](int c, int slot) {
+#pragma unroll
+    for (int j = 0; j < FPW; ++j)
+      if (j < FPW - 1 || full)
+        xr[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(
+            xrs, c < xlen[j] ? xoff[j] + c * 1024 : xbytes, 0, 0);
+    const bool in = c < kwn;
+#pragma unroll
+    for (int j = 0; j < NW; ++j)
+      wr[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(wrs, in ? wvo[j] : wbytes,
+                                                          (kw0 + (in ? c : 0)) * 1024, kNonTemporal);
+  };
+  auto stage = [&](int slot, int buf) {
+#pragma unroll
+    for (int j = 0; j < FPW; ++j)
+      if (j < FPW - 1 || full)
+        *(i32x4 *)(abuf + (buf * C::FRAG + w + kGemmWaves * j) * 1024 + wsw) = xr[slot][j];
+  };
+  f32x4 acc[NW][TT];
+#pragma unroll
+  for (int j = 0; j < NW; ++j)
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) acc[j][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto mac = [&](int buf, int slot) {
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      // operand B: token row lane % 16, k 8 (lane / 16) .. of the fragment
+      const uint4 xv = *(const uint4 *)(abuf + (buf * C::FRAG + kp * TT + tt) * 1024 + rsw);
+#pragma unroll
+      for (int j = 0; j < NW; ++j)
+        acc[j][tt] = mfma16(__builtin_bit_cast(bf16x8, wr[slot][j]), as_bf16x8(xv), acc[j][tt]);
+    }
+  };
+  // One group of loads per chunk (its activation, then its weights), L
+  // groups ahead: at chunk c the loads issued after its group are L - 1
+  // whole groups.
+  constexpr int AFTER_FULL = (L - 1) * (FPW + NW), AFTER_SHORT = (L - 1) * (FPW - 1 + NW);
+#pragma unroll
+  for (int c = 0; c < L; ++c) issue(c, c);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int c0 = 0; c0 < nchunk; c0 += L) {
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const int c = c0 + i;
+      if (c >= nchunk) break;  // uniform
+      if (full)
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(AFTER_FULL) : "memory");
+      else
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(AFTER_SHORT) : "memory");
+      // buffer i % 2 was last read at chunk c - 2, which every wave finished
+      // before the barrier of chunk c - 1
+      stage(i, i % 2);
+      lds_barrier();
+      if (has) mac(i % 2, i);
+      __builtin_amdgcn_sched_barrier(0);
+      issue(c + L, i);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // Reduction, one tile of the pairs per round: every wave leaves its
+  // partial sums of the pair's tile j in LDS; the wave of K part j adds the
+  // KS partials of its pair in part order and runs the epilogue.
+  f32x4(*red)[64] = (f32x4(*)[64])abuf;  // [wave][tt][lane]
+#pragma unroll
+  for (int j = 0; j < NW; ++j) {
+    lds_barrier();
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) red[w * TT + tt][lane] = acc[j][tt];
+    lds_barrier();
+    const int tile = tile0 + j;
+    if (kp == j && tile < a.tiles) {
+#pragma unroll 1
+      for (int tt = 0; tt < TT; ++tt) {
+        f32x4 v = red[pw * TT + tt][lane];
+#pragma unroll
+        for (int p = 1; p < KS; ++p) v += red[(p * C::PAIRS + pw) * TT + tt][lane];
+        // lane l holds rows 4 (l / 16) .. + 3 of the tile for token row
+        // l % 16; lanes l < 32 take rows p0 = 4 (l / 16) .. + 3 and
+        // p0 + 8 .. + 3 (from lane l + 32)
+        f32x4 v2;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v2[i] = __shfl_down(v[i], 32, 64);
+        const int tok = tt * 16 + (lane & 15);
+        if (lane < 32 && tok < a.n_tok) {
+          if ((EPI == EPI_QKV || EPI == EPI_SWIGLU) && a.rs_in) {
+            const float r = a.rs_in[tok];
+            v *= r;
+            v2 *= r;
+          }
+          epilogue4<EPI>(a, a.rope, split, tile, 4 * (lane >> 4), tok, v, v2);
+        }
+      }
+    }
+  }
+}
+
+template <int EPI, int TT, int KS>
+hipError_t launch_wide_tt(const GemmArgs &a, int grid, hipStream_t s) {
+  LaunchEvents &ev = g_launch_events;
+  if (!ev.taken) {
+    ev.taken = true;
+    hipExtLaunchKernelGGL((k_gemm_wide<EPI, TT, KS>), dim3(grid), dim3(kGemmThreads), 0, s,
+                          ev.start, ev.stop, 0, a);
+  } else {
+    hipLaunchKernelGGL((k_gemm_wide<EPI, TT, KS>), dim3(grid), dim3(kGemmThreads), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+template <int EPI, int KS>
+hipError_t launch_wide_ks(const GemmArgs &a, int tt, int grid, hipStream_t s) {
+  switch (tt) {
+    case 9: return launch_wide_tt<EPI, 9, KS>(a, grid, s);
+    case 12: return launch_wide_tt<EPI, 12, KS>(a, grid, s);
+    case 16: return launch_wide_tt<EPI, 16, KS>(a, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 template <int EPI, int TT, int NT>
 hipError_t launch_tt_nt(const GemmArgs &a, int grid, hipStream_t s) {
@@ -602,6 +798,13 @@ hipError_t launch_tt(const GemmArgs &a, int nt, int grid, hipStream_t s) {
 // tiles and tiles per pass).
 template <int EPI>
 hipError_t launch_epi(const GemmArgs &b, const GemmPlan &p, hipStream_t s) {
+  if constexpr (EPI == EPI_SWIGLU || EPI == EPI_RESID) {
+    if (p.wide == 2) return launch_wide_ks<EPI, 2>(b, p.tt, p.grid, s);
+  }
+  if constexpr (EPI == EPI_QKV) {
+    if (p.wide == 4) return launch_wide_ks<EPI, 4>(b, p.tt, p.grid, s);
+  }
+  if (p.wide) return hipErrorInvalidValue;
   switch (p.tt) {
     case 1: return launch_tt<EPI, 1>(b, p.nt, p.grid, s);
     case 2: return launch_tt<EPI, 2>(b, p.nt, p.grid, s);

@@ -128,9 +128,6 @@ struct GemmArgs {
   LmPart *lm_part;
   float lm_inv_t;
   int lm_greedy;
-  // token-tile groups per (tile group, K range) (plan_gemm; 1 below 9 token
-  // tiles)
-  int tgroups;
 };
 
 // Row stride of the per-(token, group) sums of squares of a RESID_NORM
@@ -198,7 +195,8 @@ constexpr int gemm_nt_cap(int tt) {
 }
 constexpr int kRedPairs = 16;
 struct GemmPlan {
-  int tt, nt, split, groups, grid, tgroups;
+  int tt, nt, split, groups, grid;
+  int wide;  // k_gemm_wide with this many K parts per workgroup (0: k_gemm)
 };
 GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok);
 // Launches of a planned GEMM, one per epilogue kind (k_gemm_*.hip).

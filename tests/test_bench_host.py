@@ -88,6 +88,8 @@ def test_kernel_classes_of_a_layer(layer, want):
     assert bench.kernel_class("k_walk(int, ...)", "stats") == "accept_walk"
     assert bench.kernel_class("void k_rollback<unsigned short>(...)", "accept_walk") == "rollback"
     assert bench.kernel_class("void k_gemm<3, 3, 8>(sb::GemmArgs)", "norm") == "lm_head"
+    assert bench.kernel_class("void k_gemm_wide<2, 9>(sb::GemmArgs)", "o") == "gate_up"
+    assert bench.kernel_class("void k_gemm_wide<1, 9>(sb::GemmArgs)", "gate_up") == "down"
 
 
 def _write_trace(d, n_steps, n_layers):

@@ -112,6 +112,9 @@ CASES = [
     ("small_h128_bf16", 2047, ("branch", 4, 8)),
     ("gqa128_bf16", 300, ("branch", 4, 4)),
     ("gqa128_bf16", 1, ("chain", 9)),
+    # trees of 145 .. 192 rows (12 token tiles in the wide GEMMs)
+    ("ragged_bf16", 90, ("branch", 10, 17)),
+    ("small_h128_bf16", 500, ("branch", 12, 13)),
     # the largest trees (SB_MAX_ROWS = 256 rows): 15 x 17 branches, a
     # 256-row chain (ancestor bit 255)
     ("small_bf16", 64, ("branch", 15, 17)),
