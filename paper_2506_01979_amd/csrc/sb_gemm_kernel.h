@@ -628,10 +628,12 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm_wide(GemmArgs a) {
   // Chunk c's fragment f = p TT + tt (K part p, token tile tt) sits at KB f
   // of its buffer; wave w moves fragments w + 8 j.  Lane l loads bytes
   // 16 l .. of a fragment (token row r = l / 4, k 8 (l % 4) ..) and stores
-  // them at slot 4 r + ((l % 4) ^ (r / 4 % 4)), so the 8 lanes an LDS read
-  // serves together fall on 8 different bank groups.
-  const int wsw = ((lane >> 2) * 4 + ((lane & 3) ^ ((lane >> 4) & 3))) * 16;
-  const int rsw = ((lane & 15) * 4 + ((lane >> 4) ^ ((lane >> 2) & 3))) * 16;
+  // them at 16-byte slot 4 r + ((l % 4) ^ x(r)), x(r) = (r / 2 ^ r / 8) % 4:
+  // the 8 (16) lanes that a 128-bit LDS access serves per clock then cover
+  // all 32 (64) banks, for the writes and for the operand reads.
+  auto xsw = [](int r) { return ((r >> 1) ^ (r >> 3)) & 3; };
+  const int wsw = ((lane >> 2) * 4 + ((lane & 3) ^ xsw(lane >> 2))) * 16;
+  const int rsw = ((lane & 15) * 4 + ((lane >> 4) ^ xsw(lane & 15))) * 16;
   // per fragment of this wave: its lane offset at k-step 0 of its K part
   // and the part's length (the loop below only adds the chunk)
   int xoff[FPW], xlen[FPW];
@@ -679,11 +681,23 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm_wide(GemmArgs a) {
     }
   };
   // One group of loads per chunk (its activation, then its weights), L
-  // groups ahead: at chunk c the loads issued after its group are L - 1
-  // whole groups.
-  constexpr int AFTER_FULL = (L - 1) * (FPW + NW), AFTER_SHORT = (L - 1) * (FPW - 1 + NW);
+  // groups ahead.  Step c writes chunk c + 1's activation to LDS while it
+  // multiplies chunk c, then one barrier: chunk c + 1 is visible for the
+  // next step and every wave is done with buffer c % 2, which the next step
+  // overwrites.  At step c the loads issued after chunk c + 1's group are
+  // L - 2 whole groups.
+  constexpr int AFTER_FULL = (L - 2) * (FPW + NW), AFTER_SHORT = (L - 2) * (FPW - 1 + NW);
+  auto wait_next = [&]() {
+    if (full)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(AFTER_FULL + FPW + NW) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(AFTER_SHORT + FPW - 1 + NW) : "memory");
+  };
 #pragma unroll
   for (int c = 0; c < L; ++c) issue(c, c);
+  wait_next();  // chunk 0
+  stage(0, 0);
+  lds_barrier();
   __builtin_amdgcn_sched_barrier(0);
   for (int c0 = 0; c0 < nchunk; c0 += L) {
 #pragma unroll
@@ -694,11 +708,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm_wide(GemmArgs a) {
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(AFTER_FULL) : "memory");
       else
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(AFTER_SHORT) : "memory");
-      // buffer i % 2 was last read at chunk c - 2, which every wave finished
-      // before the barrier of chunk c - 1
-      stage(i, i % 2);
-      lds_barrier();
+      stage((i + 1) % L, (i + 1) % 2);
       if (has) mac(i % 2, i);
+      lds_barrier();
       __builtin_amdgcn_sched_barrier(0);
       issue(c + L, i);
     }
