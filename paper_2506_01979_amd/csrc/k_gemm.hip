@@ -29,6 +29,10 @@ constexpr int kNTs[] = {1, 2, 3, 4, 6, 8};
 
 }  // namespace
 
+// Token tiles past which the projections take k_gemm_wide (from 5 token
+// tiles, 13B at 65 rows: QKV 35 -> 46 us, down 37 -> 41, gate/up 61 -> 61).
+constexpr int kWideFrom = 8;
+
 GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
   GemmPlan p{};
   const int nc = ks / 8;
@@ -39,7 +43,7 @@ GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
   // residual projections split K over up to kMaxSplit workgroups per tile
   // group as well.  13B at 129 rows: gate/up 120 -> 78 us, QKV 69 -> 61,
   // down 61 -> 50, O 25 -> 26.
-  if (tt_all > 8 && (epi == EPI_QKV || epi == EPI_SWIGLU || epi == EPI_RESID)) {
+  if (tt_all > kWideFrom && (epi == EPI_QKV || epi == EPI_SWIGLU || epi == EPI_RESID)) {
     const int KS = epi == EPI_QKV ? 4 : 2;
     p.wide = KS;
     p.tt = tt_all <= 9 ? 9 : tt_all <= 12 ? 12 : 16;

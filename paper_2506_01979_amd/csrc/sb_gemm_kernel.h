@@ -588,6 +588,7 @@ struct WideCfg {
   static constexpr int L = FRAG <= 18 ? 6 : FRAG <= 36 ? 4 : 2;     // chunks in flight
   static constexpr int LDS = 2 * FRAG > kGemmWaves * TT ? 2 * FRAG : kGemmWaves * TT;  // KB
   static_assert(L % 2 == 0, "the unrolled chunk steps cover both LDS buffers");
+  static_assert((L - 1) * (FPW + 2) <= 63, "the loads in flight fit the wait counter");
   static_assert(LDS <= 160, "the chunk buffers and the reduction fit LDS");
 };
 

@@ -122,6 +122,8 @@ WORKLOADS = {
                                     kv_from_prefill=False),
     "llama13b_b8k16_p8192": Workload("llama13b_b8k16_p8192", SHAPES["llama13b"], 8192, 8, 16, 0.7,
                                      kv_from_prefill=False),
+    "llama13b_b8k8_p8192": Workload("llama13b_b8k8_p8192", SHAPES["llama13b"], 8192, 8, 8, 0.7,
+                                    kv_from_prefill=False),
     "llama70b_b4k8_p4096": Workload("llama70b_b4k8_p4096", SHAPES["llama70b"], 4096, 4, 8, 0.7,
                                     kv_from_prefill=False),
 }

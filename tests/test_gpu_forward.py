@@ -112,6 +112,9 @@ CASES = [
     ("small_h128_bf16", 2047, ("branch", 4, 8)),
     ("gqa128_bf16", 300, ("branch", 4, 4)),
     ("gqa128_bf16", 1, ("chain", 9)),
+    # more than 16 rounds of (KV head, key range, row block) units: each
+    # workgroup walks the three row blocks of its key range
+    ("heads32_bf16", 11000, ("branch", 8, 16)),
     # trees of 145 .. 192 rows (12 token tiles in the wide GEMMs)
     ("ragged_bf16", 90, ("branch", 10, 17)),
     ("small_h128_bf16", 500, ("branch", 12, 13)),
@@ -139,7 +142,15 @@ def test_verify_forward_parity(api, sname, P, spec):
     n = len(parents)
     ptoks = synth.prefix_tokens(shape.vocab, P)
     kv_len = P - 1
-    if kv_len:
+    if kv_len > 4096:
+        # a long prefix: seeded N(0, 1) keys and values stand in for a
+        # prefill (the oracle's prefill is quadratic in the prefix)
+        gk = np.random.default_rng(P)
+        dims = (shape.n_layers, shape.n_kv_heads, kv_len, shape.head_dim)
+        Kp, Vp = gk.standard_normal(dims), gk.standard_normal(dims)
+        if mode(shape) == "bf16":
+            Kp, Vp = decoder.round_bf16(Kp.astype(np.float32)), decoder.round_bf16(Vp.astype(np.float32))
+    elif kv_len:
         _, Kp, Vp = decoder.prefill(shape, W, ptoks[:-1], mode(shape))
     else:
         Kp = Vp = np.zeros((shape.n_layers, shape.n_kv_heads, 0, shape.head_dim))
