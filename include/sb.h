@@ -214,7 +214,7 @@ sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
  * capture, tight serving loops, harnesses that forbid allocation).
  * Same computation, arguments and results as sb_verify_forward, with the
  * workspace taken from a file-scope device array of the library of
- * SB_NOALLOC_SCRATCH_BYTES bytes (64 MiB), one per device, allocated when
+ * SB_NOALLOC_SCRATCH_BYTES bytes (128 MiB), one per device, allocated when
  * the library's code is loaded on that device and held until the process
  * ends.  The call allocates nothing: its first call on a device (with that
  * device current) looks the array's address up once.
@@ -226,7 +226,7 @@ sb_status sb_verify_forward(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
  * on a device (two streams, two threads) race and must be serialised by
  * the caller.  The array keeps the last call's contents; every value the
  * forward reads from it is written earlier in the same call. */
-#define SB_NOALLOC_SCRATCH_BYTES (64 * 1024 * 1024)
+#define SB_NOALLOC_SCRATCH_BYTES (128 * 1024 * 1024)
 #define SB_NOALLOC_MAX_DEVICES 64
 sb_status sb_verify_forward_noalloc(sb_model *m, const sb_kv_cache *kv, int32_t kv_len,
                                     const int32_t *d_tokens, const int32_t *h_parents,

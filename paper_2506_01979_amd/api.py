@@ -113,7 +113,7 @@ lib.sb_verify_forward.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, C.POINTER(
 lib.sb_verify_forward_noalloc.restype = _i32
 lib.sb_verify_forward_noalloc.argtypes = [_vp, C.POINTER(KVCache), _i32, _vp, C.POINTER(_i32),
                                           _i32, _f, _vp, _vp, _vp]
-SB_NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
+SB_NOALLOC_SCRATCH_BYTES = 128 * 1024 * 1024
 lib.sb_model_set_forward.restype = _i32
 lib.sb_model_set_forward.argtypes = [_vp, _i32]
 lib.sb_softmax_stats.restype = _i32

@@ -207,7 +207,7 @@ def test_draft_host_validation_without_device(api):
 def test_noalloc_rejects_a_step_larger_than_its_scratch_without_device(api):
     """sb_verify_forward_noalloc checks the step's workspace against its
     scratch array before any device call: a 70B-shaped step of 256 rows at
-    a 60000-slot prefix needs more than 64 MiB."""
+    a 60000-slot prefix needs more than 128 MiB."""
     lib = api.lib
     w = api.ModelWeights(1, 1, 1, (api.LayerWeights * 2)(*[api.LayerWeights(1, 1, 1, 1, 1, 1)] * 2))
     from paper_2506_01979_amd import synth
@@ -241,12 +241,12 @@ def _fake_model(api, shape_name, n_layers=None):
 
 @pytest.mark.parametrize("shape,rows,prefixes", [
     ("llama7b", 129, (512, 2048, 4096, 8192)),
-    ("llama13b", 129, (512, 2048, 4096)),
+    ("llama13b", 129, (512, 2048, 4096, 8192)),
     ("llama13b", 65, (8192,)),
     ("llama70b", 33, (512, 4096, 8192)),
 ])
 def test_noalloc_scratch_covers_the_stated_steps(api, shape, rows, prefixes):
-    """The allocation-free entry point's 64 MiB array holds the forward's
+    """The allocation-free entry point's 128 MiB array holds the forward's
     workspace of the steps its documentation names."""
     h, _w = _fake_model(api, shape)
     try:
