@@ -823,6 +823,7 @@ hipError_t launch_epi(const GemmArgs &b, const GemmPlan &p, hipStream_t s) {
     case 2: return launch_tt<EPI, 2>(b, p.nt, p.grid, s);
     case 3: return launch_tt<EPI, 3>(b, p.nt, p.grid, s);
     case 4: return launch_tt<EPI, 4>(b, p.nt, p.grid, s);
+    case 5: return launch_tt<EPI, 5>(b, p.nt, p.grid, s);
     case 6: return launch_tt<EPI, 6>(b, p.nt, p.grid, s);
     case 8: return launch_tt<EPI, 8>(b, p.nt, p.grid, s);
     case 12: return launch_tt<EPI, 12>(b, p.nt, p.grid, s);

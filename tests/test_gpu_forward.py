@@ -112,6 +112,9 @@ CASES = [
     ("small_h128_bf16", 2047, ("branch", 4, 8)),
     ("gqa128_bf16", 300, ("branch", 4, 4)),
     ("gqa128_bf16", 1, ("chain", 9)),
+    # trees of 65 .. 80 rows (5 token tiles)
+    ("small_gqa_bf16", 300, ("branch", 8, 8)),
+    ("small_h128_bf16", 100, ("branch", 5, 15)),
     # more than 16 rounds of (KV head, key range, row block) units: each
     # workgroup walks the three row blocks of its key range
     ("heads32_bf16", 11000, ("branch", 8, 16)),
