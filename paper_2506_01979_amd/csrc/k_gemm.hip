@@ -41,12 +41,13 @@ GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
   const int tt_all = (n_tok + 15) / 16;
   // Wide trees: k_gemm_wide (a wave owns a tile pair over one of KS parts
   // of the workgroup's K range; the activation is staged once per 16 / KS
-  // tiles through LDS).  QKV, with the fewest tiles, takes KS = 4; the
-  // residual projections split K over up to kMaxSplit workgroups per tile
-  // group as well.  13B at 129 rows: gate/up 120 -> 78 us, QKV 69 -> 61,
-  // down 61 -> 50, O 25 -> 26.
+  // tiles through LDS).  QKV and the residual projections, with the fewest
+  // tiles, take KS = 4 (the residual projections: 13.20 -> 13.11 ms per
+  // step against KS = 2); the residual projections also split K over up to
+  // kMaxSplit workgroups per tile group.  13B at 129 rows: gate/up 120 -> 78
+  // us, QKV 69 -> 61, down 61 -> 50, O 25 -> 26 (KS = 2).
   if (tt_all > kWideFrom && (epi == EPI_QKV || epi == EPI_SWIGLU || epi == EPI_RESID)) {
-    const int KS = epi == EPI_QKV ? 4 : 2;
+    const int KS = (epi == EPI_QKV || epi == EPI_RESID) ? 4 : 2;
     p.wide = KS;
     p.tt = tt_all <= 9 ? 9 : tt_all <= 12 ? 12 : 16;
     p.nt = 2;

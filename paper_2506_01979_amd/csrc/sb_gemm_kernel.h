@@ -814,7 +814,7 @@ hipError_t launch_epi(const GemmArgs &b, const GemmPlan &p, hipStream_t s) {
   if constexpr (EPI == EPI_SWIGLU || EPI == EPI_RESID) {
     if (p.wide == 2) return launch_wide_ks<EPI, 2>(b, p.tt, p.grid, s);
   }
-  if constexpr (EPI == EPI_QKV) {
+  if constexpr (EPI == EPI_QKV || EPI == EPI_RESID) {
     if (p.wide == 4) return launch_wide_ks<EPI, 4>(b, p.tt, p.grid, s);
   }
   if (p.wide) return hipErrorInvalidValue;
