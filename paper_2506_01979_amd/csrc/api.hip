@@ -354,10 +354,11 @@ sb_status forward_bf16(sb_model *m, const sb_kv_cache *kv, int kv_len, const int
   // The row softmax statistics come out of the LM head's epilogue as
   // per-(row, workgroup) partials, kept in the delta buffer (free once the
   // final norm has summed it), and one short pass combines them; the
-  // logits are not read again.  Shapes whose partials do not fit there run
-  // the statistics pass over the logits.
+  // logits are not read again.  Shapes whose partials do not fit there, and
+  // trees of more than 128 rows (the LM head in k_gemm_wide), run the
+  // statistics pass over the logits.
   const GemmPlan lp = plan_gemm(EPI_LOGITS, gl.tiles, gl.ks, n);
-  const bool fuse_stats = lp.groups <= kSsGroups &&
+  const bool fuse_stats = !lp.wide && lp.groups <= kSsGroups &&
                           (size_t)n * lp.groups * sizeof(LmPart) <=
                               (size_t)kMaxSplit * L.np * H * sizeof(float);
   if (fuse_stats) {

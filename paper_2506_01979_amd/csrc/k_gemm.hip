@@ -42,11 +42,14 @@ GemmPlan plan_gemm(int epi, int tiles, int ks, int n_tok) {
   // Wide trees: k_gemm_wide (a wave owns a tile pair over one of KS parts
   // of the workgroup's K range; the activation is staged once per 16 / KS
   // tiles through LDS).  QKV and the residual projections, with the fewest
-  // tiles, take KS = 4 (the residual projections: 13.20 -> 13.11 ms per
-  // step against KS = 2); the residual projections also split K over up to
-  // kMaxSplit workgroups per tile group.  13B at 129 rows: gate/up 120 -> 78
-  // us, QKV 69 -> 61, down 61 -> 50, O 25 -> 26 (KS = 2).
-  if (tt_all > kWideFrom && (epi == EPI_QKV || epi == EPI_SWIGLU || epi == EPI_RESID)) {
+  // tiles, take KS = 4; the residual projections also split K over up to
+  // kMaxSplit workgroups per tile group.  The LM head runs without its
+  // fused statistics (the separate pass reads the logits).  13B at 129
+  // rows: gate/up 120 -> 78 us, QKV 69 -> 61, down 61 -> 50 (KS = 2; KS = 4
+  // took the step from 13.20 to 13.11 ms), the LM head 138 + 5 -> 79 + 11
+  // with the statistics pass.
+  if (tt_all > kWideFrom &&
+      (epi == EPI_QKV || epi == EPI_SWIGLU || epi == EPI_RESID || epi == EPI_LOGITS)) {
     const int KS = (epi == EPI_QKV || epi == EPI_RESID) ? 4 : 2;
     p.wide = KS;
     p.tt = tt_all <= 9 ? 9 : tt_all <= 12 ? 12 : 16;

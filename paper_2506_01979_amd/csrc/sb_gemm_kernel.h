@@ -742,7 +742,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm_wide(GemmArgs a) {
         for (int i = 0; i < 4; ++i) v2[i] = __shfl_down(v[i], 32, 64);
         const int tok = tt * 16 + (lane & 15);
         if (lane < 32 && tok < a.n_tok) {
-          if ((EPI == EPI_QKV || EPI == EPI_SWIGLU) && a.rs_in) {
+          if ((EPI == EPI_QKV || EPI == EPI_SWIGLU || EPI == EPI_LOGITS) && a.rs_in) {
             const float r = a.rs_in[tok];
             v *= r;
             v2 *= r;
@@ -811,7 +811,7 @@ hipError_t launch_tt(const GemmArgs &a, int nt, int grid, hipStream_t s) {
 // tiles and tiles per pass).
 template <int EPI>
 hipError_t launch_epi(const GemmArgs &b, const GemmPlan &p, hipStream_t s) {
-  if constexpr (EPI == EPI_SWIGLU || EPI == EPI_RESID) {
+  if constexpr (EPI == EPI_SWIGLU || EPI == EPI_RESID || EPI == EPI_LOGITS) {
     if (p.wide == 2) return launch_wide_ks<EPI, 2>(b, p.tt, p.grid, s);
   }
   if constexpr (EPI == EPI_QKV || EPI == EPI_RESID) {
