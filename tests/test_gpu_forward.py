@@ -118,6 +118,11 @@ CASES = [
     # more than 16 rounds of (KV head, key range, row block) units: each
     # workgroup walks the three row blocks of its key range
     ("heads32_bf16", 11000, ("branch", 8, 16)),
+    # long prefixes over many one-step workgroups (head_dim 64 and 128, one
+    # and three row blocks, grouped queries, up to 95 key ranges)
+    ("heads32_bf16", 3000, ("branch", 8, 16)),
+    ("heads32_bf16", 5000, ("branch", 4, 8)),
+    ("gqa128_bf16", 24000, ("branch", 8, 16)),
     # trees of 145 .. 192 rows (12 token tiles in the wide GEMMs)
     ("ragged_bf16", 90, ("branch", 10, 17)),
     ("small_h128_bf16", 500, ("branch", 12, 13)),
@@ -145,7 +150,7 @@ def test_verify_forward_parity(api, sname, P, spec):
     n = len(parents)
     ptoks = synth.prefix_tokens(shape.vocab, P)
     kv_len = P - 1
-    if kv_len > 4096:
+    if kv_len > 2500:
         # a long prefix: seeded N(0, 1) keys and values stand in for a
         # prefill (the oracle's prefill is quadratic in the prefix)
         gk = np.random.default_rng(P)
