@@ -1,7 +1,7 @@
 """The verify forward without a workspace argument (sb_verify_forward_noalloc,
 for callers that cannot allocate): its scratch array must give exactly what
-the workspace entry point gives, on two calls in a row with the second
-smaller than the first (the array keeps the first call's contents)."""
+the workspace entry point gives, on calls in a row each smaller than the
+one before (the array keeps the previous call's contents)."""
 import numpy as np
 import pytest
 import torch
@@ -39,7 +39,8 @@ def test_noalloc_equals_workspace_entry(api, sname):
     shape = synth.SHAPES[sname]
     W = synth.model_weights(shape)
     m = api.Model(shape, api.dict_tensors(W))
-    for call, (P, B, k) in enumerate(((300, 4, 8), (40, 2, 3))):
+    # a wide tree (129 rows: the wide GEMMs and LM head), then smaller ones
+    for call, (P, B, k) in enumerate(((300, 8, 16), (300, 4, 8), (40, 2, 3))):
         kv_len = P - 1
         parents, toks = _inputs(shape, P, B, k, 10 + call)
         n = len(parents)
