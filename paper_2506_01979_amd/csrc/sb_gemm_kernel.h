@@ -576,9 +576,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void k_gemm(GemmArgs a) {
 // launches (the residual projections, whose tile groups are too few to fill
 // the chip) also give each of `split` workgroups per tile group a
 // contiguous K range; the unit order is K-range-major, so each XCD caches
-// one range of the activation.  (Direct-to-LDS loads move the activation at
-// about 7 bytes per clock per compute unit, which bounded every variant
-// that used them.)
+// one range of the activation.  (Staging by direct-to-LDS loads into
+// separate LDS arrays, one per ring buffer, ran the step equally fast; into
+// one array the compiler waits for every load in flight before each LDS
+// read, since it cannot tell the buffers apart.)
 template <int TT, int KS>
 struct WideCfg {
   static constexpr int PAIRS = kGemmWaves / KS;                     // tile pairs per workgroup
