@@ -113,6 +113,9 @@ hipError_t launch_gemm(int epi, const GemmArgs &a, int tiles, int *split, hipStr
                   epi == EPI_RESID_NORM || epi == EPI_QKV))
     return hipErrorInvalidValue;
   const GemmPlan p = plan_gemm(epi, tiles, a.ks, a.n_tok);
+  // k_gemm_wide has no fused softmax statistics: the caller runs the
+  // separate pass for such shapes
+  if (p.wide && a.lm_part) return hipErrorInvalidValue;
   GemmArgs b = a;
   b.epi = epi;
   b.tiles = tiles;
